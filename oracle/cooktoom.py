@@ -1,0 +1,310 @@
+"""Cook-Toom / Winograd minimal filtering, exactly and in fp64 (test infrastructure only).
+
+Only tests, the smoke check and the benchmark's CPU baseline may import this
+module; the HIP path never does, and its own transform constants are written
+independently of anything here.
+
+Contents, each in the paper's notation where it has one (Sec. 2):
+
+* :func:`cook_toom` -- the exact rational matrices of F(m x m, 3 x 3): the output
+  (inverse) transform A^T (the paper's Z^T), the filter transform G (its W) and
+  the input transform B^T (its X^T), derived from interpolation points.  Only
+  the F(2x2,3x3) input matrix is printed in the paper (Sec. 2.1.1); the rest
+  follows from the construction below, and the m=2 signs are chosen so that
+  B^T equals the printed matrix.
+* :func:`winograd_conv_exact` -- Eq. 1 evaluated over the rationals, region by
+  region, in the loop order of Listing 1 (per output channel, per output region,
+  sum over the input channels in the transform domain, one inverse transform
+  per region).  On integer inputs this must equal the direct definition exactly.
+* fp64 references of each stage of the three-step decomposition of Sec. 2
+  (input transform scattering into the per-position 'A' matrices, the
+  per-position GEMMs with the pre-transformed weights 'B', and the output
+  transform gathering from 'C'), plus the offline weight transform.
+* :func:`input_transform_m2_paper_order_f32` -- the F(2x2,3x3) input transform in
+  fp32 with the exact add/sub sequence the paper prints for it (Sec. 2.1.1): a
+  pass combining rows, then the same pass combining columns.
+
+Transform-domain index: t = xi * alpha + nu for the (xi, nu) element of an
+alpha x alpha region, alpha = m + 2, T = alpha^2.  Tile index p = (n*th + ti)*tw
++ tj with th = ceil(Ho/m), tw = ceil(Wo/m).  Tile (ti, tj) produces output rows
+ti*m .. ti*m+m-1 and reads the input region starting at (ti*m - pad, tj*m - pad);
+values outside the input (padding and the ragged overhang) are zero, and outputs
+beyond Ho x Wo are discarded.
+"""
+from __future__ import annotations
+
+from fractions import Fraction as Q
+from functools import lru_cache
+from math import prod
+
+import numpy as np
+
+R_FILTER = 3  # the method's filter size for this path (3x3 layers)
+
+
+# ----------------------------------------------------------------------------
+# Exact matrices
+# ----------------------------------------------------------------------------
+
+def interpolation_points(m: int) -> list[int]:
+    """Finite interpolation points of F(m, 3); the point at infinity is implied.
+
+    The paper names the Cook-Toom class but not its points.  Reading taken: the
+    smallest-magnitude integer points, {0, 1, -1} for m=2 and {0, 1, -1, 2, -2}
+    for m=4.  Any distinct points give an exact algorithm; the choice only changes
+    fp32 rounding.
+    """
+    if m == 2:
+        return [0, 1, -1]
+    if m == 4:
+        return [0, 1, -1, 2, -2]
+    raise ValueError("m must be 2 or 4")
+
+
+def _solve_consistent(rows: list[list[Q]], rhs: list[Q]) -> list[Q]:
+    """Exact Gauss-Jordan solve of an over-determined, consistent system with a
+    unique solution.  Raises if inconsistent or rank-deficient."""
+    n = len(rows[0])
+    aug = [list(r) + [b] for r, b in zip(rows, rhs)]
+    piv_row = 0
+    pivots = []
+    for col in range(n):
+        sel = next((r for r in range(piv_row, len(aug)) if aug[r][col] != 0), None)
+        if sel is None:
+            raise ArithmeticError("rank-deficient system")
+        aug[piv_row], aug[sel] = aug[sel], aug[piv_row]
+        pv = aug[piv_row][col]
+        aug[piv_row] = [v / pv for v in aug[piv_row]]
+        for r in range(len(aug)):
+            if r != piv_row and aug[r][col] != 0:
+                f = aug[r][col]
+                aug[r] = [a - f * b for a, b in zip(aug[r], aug[piv_row])]
+        pivots.append(col)
+        piv_row += 1
+    for r in range(piv_row, len(aug)):
+        if aug[r][n] != 0:
+            raise ArithmeticError("inconsistent system")
+    return [aug[i][n] for i in range(n)]
+
+
+@lru_cache(maxsize=None)
+def _raw_cook_toom(m: int):
+    r = R_FILTER
+    a = m + r - 1
+    pts = [Q(p) for p in interpolation_points(m)]
+    nf = a - 1  # finite points; the last row/column is the point at infinity
+    # Output transform: evaluate the length-m output polynomial's basis at each
+    # point; the infinity column picks the leading coefficient.
+    AT = [[(pts[j] ** i if j < nf else Q(int(i == m - 1))) for j in range(a)]
+          for i in range(m)]
+    # Filter transform: Lagrange-weighted evaluation of the filter polynomial at
+    # each finite point; the infinity row picks the filter's leading tap.
+    G = []
+    for j in range(nf):
+        den = prod((pts[j] - pts[l] for l in range(nf) if l != j), start=Q(1))
+        G.append([pts[j] ** k / den for k in range(r)])
+    G.append([Q(int(k == r - 1)) for k in range(r)])
+    # Input transform: the unique B^T with sum_j AT[i][j] G[j][k] BT[j][a'] equal
+    # to [a' == i + k] for all i < m, k < r, a' < alpha, i.e. the 1-D algorithm
+    # reproduces y[i] = sum_k g[k] d[i + k] (correlation) for every g and d.
+    E = [[AT[i][j] * G[j][k] for j in range(a)] for i in range(m) for k in range(r)]
+    cols = []
+    for ap in range(a):
+        rhs = [Q(int(ap == i + k)) for i in range(m) for k in range(r)]
+        cols.append(_solve_consistent(E, rhs))
+    BT = [[cols[ap][j] for ap in range(a)] for j in range(a)]
+    return AT, G, BT
+
+
+def cook_toom(m: int):
+    """Exact (A^T, G, B^T) of F(m x m, 3 x 3) as lists of Fractions.
+
+    Sign normalisation: scaling row j of G by s and row j of B^T by 1/s (or
+    column j of A^T by s and row j of B^T by 1/s) leaves the algorithm exact.
+    For m=2 the paper prints B^T; the raw derivation differs from it by the sign
+    of rows 0 and 3, so row 0 is flipped through G and row 3 (the infinity row)
+    through A^T.  For m=4 nothing is printed and the raw derivation is kept.
+    """
+    AT, G, BT = _raw_cook_toom(m)
+    AT = [list(r) for r in AT]
+    G = [list(r) for r in G]
+    BT = [list(r) for r in BT]
+    if m == 2:
+        G[0] = [-v for v in G[0]]
+        BT[0] = [-v for v in BT[0]]
+        for i in range(len(AT)):
+            AT[i][3] = -AT[i][3]
+        BT[3] = [-v for v in BT[3]]
+    return AT, G, BT
+
+
+def matrices_f64(m: int):
+    """(A^T, G, B^T) as fp64 numpy arrays (G's thirds are rounded to fp64)."""
+    AT, G, BT = cook_toom(m)
+    f = lambda M: np.array([[float(v) for v in row] for row in M], dtype=np.float64)
+    return f(AT), f(G), f(BT)
+
+
+# ----------------------------------------------------------------------------
+# Geometry
+# ----------------------------------------------------------------------------
+
+def geometry(N: int, H: int, W: int, pad: int, m: int):
+    """(Ho, Wo, th, tw, P) of a 3x3 stride-1 layer tiled into m x m output regions."""
+    Ho, Wo = H + 2 * pad - 2, W + 2 * pad - 2
+    th, tw = -(-Ho // m), -(-Wo // m)
+    return Ho, Wo, th, tw, N * th * tw
+
+
+# ----------------------------------------------------------------------------
+# Eq. 1 / Listing 1 over the rationals
+# ----------------------------------------------------------------------------
+
+def _mm(A, B):
+    return [[sum((A[i][l] * B[l][j] for l in range(len(B))), Q(0))
+             for j in range(len(B[0]))] for i in range(len(A))]
+
+
+def _tr(A):
+    return [list(r) for r in zip(*A)]
+
+
+def winograd_conv_exact(x, g, pad: int, m: int):
+    """Region-wise multi-channel Winograd convolution over the rationals.
+
+    x: integer/rational array [N][C][H][W]; g: [K][C][3][3].  Returns a nested
+    list [N][K][Ho][Wo] of Fractions.  Pure Python: tiny inputs only.
+    """
+    x = np.asarray(x, dtype=object)
+    g = np.asarray(g, dtype=object)
+    N, C, H, W = x.shape
+    K = g.shape[0]
+    AT, G, BT = cook_toom(m)
+    A, GT, B = _tr(AT), _tr(G), _tr(BT)
+    a = m + 2
+    Ho, Wo, th, tw, _ = geometry(N, H, W, pad, m)
+
+    def pix(n, c, u, v):
+        if 0 <= u < H and 0 <= v < W:
+            return Q(x[n, c, u, v])
+        return Q(0)
+
+    # Offline weight transform W w W^T per (output channel, input channel).
+    U = [[_mm(_mm(G, [[Q(g[k, c, r, s]) for s in range(3)] for r in range(3)]), GT)
+          for c in range(C)] for k in range(K)]
+    # Input transform X^T x X of every (image, channel, region).
+    V = {}
+    for n in range(N):
+        for c in range(C):
+            for ti in range(th):
+                for tj in range(tw):
+                    d = [[pix(n, c, ti * m - pad + u, tj * m - pad + v) for v in range(a)]
+                         for u in range(a)]
+                    V[n, c, ti, tj] = _mm(_mm(BT, d), B)
+    y = [[[[Q(0)] * Wo for _ in range(Ho)] for _ in range(K)] for _ in range(N)]
+    for k in range(K):                               # each output channel
+        for n in range(N):
+            for ti in range(th):
+                for tj in range(tw):                 # each output region
+                    acc = [[Q(0)] * a for _ in range(a)]
+                    for c in range(C):               # sum over input channels
+                        Uc, Vc = U[k][c], V[n, c, ti, tj]
+                        for u in range(a):
+                            for v in range(a):
+                                acc[u][v] += Uc[u][v] * Vc[u][v]   # Hadamard product
+                    out = _mm(_mm(AT, acc), A)       # one inverse transform per region
+                    for i in range(m):
+                        for j in range(m):
+                            oi, oj = ti * m + i, tj * m + j
+                            if oi < Ho and oj < Wo:
+                                y[n][k][oi][oj] = out[i][j]
+    return y
+
+
+# ----------------------------------------------------------------------------
+# fp64 stage references (logical layouts U[T][C][K], V[T][C][P], M[T][K][P])
+# ----------------------------------------------------------------------------
+
+def filter_transform(g: np.ndarray, m: int) -> np.ndarray:
+    """U[t][c][k] = (G g[k,c] G^T)[xi, nu], t = xi*alpha + nu, in fp64."""
+    _, G, _ = matrices_f64(m)
+    g = np.asarray(g, dtype=np.float64)
+    K, C = g.shape[:2]
+    a = m + 2
+    U = np.einsum("ar,kcrs,bs->abck", G, g, G)
+    return np.ascontiguousarray(U.reshape(a * a, C, K))
+
+
+def extract_regions(x: np.ndarray, pad: int, m: int) -> np.ndarray:
+    """d[n, c, ti, tj, u, v] = zero-extended x[n, c, ti*m - pad + u, tj*m - pad + v]."""
+    x = np.asarray(x)
+    N, C, H, W = x.shape
+    a = m + 2
+    _, _, th, tw, _ = geometry(N, H, W, pad, m)
+    Hx, Wx = th * m + 2, tw * m + 2
+    xe = np.zeros((N, C, Hx, Wx), dtype=x.dtype)
+    h1, w1 = min(H, Hx - pad), min(W, Wx - pad)
+    xe[:, :, pad:pad + h1, pad:pad + w1] = x[:, :, :h1, :w1]
+    d = np.empty((N, C, th, tw, a, a), dtype=x.dtype)
+    for ti in range(th):
+        for tj in range(tw):
+            d[:, :, ti, tj] = xe[:, :, ti * m:ti * m + a, tj * m:tj * m + a]
+    return d
+
+
+def input_transform(x: np.ndarray, pad: int, m: int) -> np.ndarray:
+    """V[t][c][p] = (B^T d_{n,c,ti,tj} B)[xi, nu] in fp64, p = (n*th+ti)*tw+tj."""
+    _, _, BT = matrices_f64(m)
+    d = extract_regions(np.asarray(x, dtype=np.float64), pad, m)
+    N, C, th, tw, a, _ = d.shape
+    Vr = np.einsum("au,nctjuv,bv->abcntj", BT, d, BT)
+    return np.ascontiguousarray(Vr.reshape(a * a, C, N * th * tw))
+
+
+def batched_gemm(U: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """M[t] = U[t]^T V[t]: for each of the T positions, [K x C] . [C x P]."""
+    return np.matmul(np.transpose(U, (0, 2, 1)), V)
+
+
+def output_transform(M: np.ndarray, N: int, Ho: int, Wo: int, m: int) -> np.ndarray:
+    """y[n,k,ti*m+i,tj*m+j] = (A^T M_{k,p} A)[i, j], cropped to Ho x Wo, in fp64."""
+    AT, _, _ = matrices_f64(m)
+    T, K, P = M.shape
+    a = m + 2
+    th, tw = -(-Ho // m), -(-Wo // m)
+    Mr = np.asarray(M, dtype=np.float64).reshape(a, a, K, N, th, tw)
+    # labels: t = ti, w = tj; result axes n, k, ti, i, tj, j -> rows ti*m+i, cols tj*m+j
+    Y = np.einsum("iu,uvkntw,jv->nktiwj", AT, Mr, AT)
+    y = Y.reshape(N, K, th * m, tw * m)
+    return np.ascontiguousarray(y[:, :, :Ho, :Wo])
+
+
+def winograd_conv_f64(x: np.ndarray, g: np.ndarray, pad: int, m: int) -> np.ndarray:
+    """The three stages composed in fp64 (weights transformed first, offline)."""
+    N, C, H, W = np.asarray(x).shape
+    Ho, Wo, _, _, _ = geometry(N, H, W, pad, m)
+    U = filter_transform(g, m)
+    V = input_transform(x, pad, m)
+    return output_transform(batched_gemm(U, V), N, Ho, Wo, m)
+
+
+def input_transform_m2_paper_order_f32(x: np.ndarray, pad: int) -> np.ndarray:
+    """F(2x2,3x3) input transform in fp32 with the paper's printed add/sub order.
+
+    Sec. 2.1.1 gives B^T x as four row operations (row0 - row2, row1 + row2,
+    row2 - row1, row1 - row3) and obtains B^T x B by applying the same four
+    operations to the columns of that result.  Every coefficient is +-1, so each
+    output is two levels of correctly rounded fp32 add/sub in this order.
+    Returns V[t][c][p] fp32.
+    """
+    d = extract_regions(np.asarray(x, dtype=np.float32), pad, 2)
+    N, C, th, tw, a, _ = d.shape
+    r = [d[..., i, :] for i in range(4)]           # rows of each region
+    s = [r[0] - r[2], r[1] + r[2], r[2] - r[1], r[1] - r[3]]
+    s = np.stack(s, axis=-2)                       # (B^T d), rows 0..3
+    c = [s[..., :, j] for j in range(4)]           # its columns
+    v = [c[0] - c[2], c[1] + c[2], c[2] - c[1], c[1] - c[3]]
+    V = np.stack(v, axis=-1)                       # (B^T d) B
+    assert V.dtype == np.float32
+    V = np.transpose(V, (4, 5, 1, 0, 2, 3))        # xi, nu, c, n, ti, tj
+    return np.ascontiguousarray(V.reshape(16, C, N * th * tw))
