@@ -1,0 +1,159 @@
+/*
+ * wino.h -- region-wise multi-channel Winograd / Cook-Toom 3x3 convolution on
+ * AMD MI355X (gfx950): F(2x2,3x3) (m = 2) and F(4x4,3x3) (m = 4), stride 1.
+ *
+ * The method (Sec. 2 of Maji et al., "Efficient Winograd or Cook-Toom
+ * Convolution Kernel Implementation on Widely Used Mobile CPUs"): a layer is
+ * Eq. 1 applied region by region -- every (m+2)x(m+2) input region of every
+ * channel is taken to the transform domain, multiplied elementwise with the
+ * transformed filter of each (output, input) channel pair, summed over the input
+ * channels, and taken back once per output region.  The work splits into an
+ * offline weight transform and three per-inference stages (Sec. 2, the
+ * three-step list): input transform (scatter into per-position matrices),
+ * T = (m+2)^2 independent GEMMs contracting over C (Sec. 2.2), and output
+ * transform (gather, inverse transform, write).
+ *
+ * Conventions for every entry point
+ *   - Data pointers are DEVICE pointers owned by the caller.  The library never
+ *     allocates, frees or keeps a pointer after the call returns.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     asynchronously: a return of WINO_OK means "enqueued", not "finished".
+ *   - Arguments are validated before any HIP call.  On failure the call returns
+ *     a negative status, enqueues nothing and leaves all outputs untouched.
+ *   - Launch failures return WINO_ERR_HIP (the HIP error is consumed); faults
+ *     during execution surface at the caller's next synchronisation.
+ *   - Stateless, reentrant and thread-safe; results are bitwise deterministic
+ *     from run to run (no atomics; every reduction has a fixed order).
+ *   - Filter 3x3, stride 1 and symmetric zero padding `pad` >= 0 are fixed by
+ *     the method; Ho = H + 2*pad - 2 and Wo = W + 2*pad - 2 must be >= 1.
+ *     The operation is cross-correlation (no kernel flip):
+ *       y[n,k,i,j] = sum_c sum_{r,s<3} x[n,c,i+r-pad,j+s-pad] * g[k,c,r,s]
+ *     with x read as zero outside [0,H) x [0,W).
+ *   - Floating point is IEEE fp32 storage and fp32 arithmetic (the paper's
+ *     precision, Sec. 3); FMA contraction is allowed; the GEMMs run on fp32 MFMA.
+ *
+ * Tiling (Sec. 2, region decomposition)
+ *   alpha = m + 2, T = alpha^2, th = ceil(Ho/m), tw = ceil(Wo/m),
+ *   P = N*th*tw tiles, tile p = (n*th + ti)*tw + tj covers output rows
+ *   ti*m .. ti*m+m-1 and cols tj*m .. tj*m+m-1 and reads the input region whose
+ *   top-left corner is (ti*m - pad, tj*m - pad).  Outputs past Ho x Wo are
+ *   computed on zero-extended input and discarded.
+ *   Transform-domain element (xi, nu) of a region has index t = xi*alpha + nu.
+ *
+ * Transform-domain layouts (MFMA-native blocking; Cp = roundup(C,4),
+ * Kp = roundup(K,16), Pp = roundup(P,16), CQ = Cp/4, KB = Kp/16, PB = Pp/16)
+ *   U (filters):  float U[KB][CQ][T][64], element (t,c,k) at lane
+ *                 (c%4)*16 + k%16 of block (k/16, c/4, t).  Padding is zero.
+ *   V (inputs):   float V[PB][CQ][T][64], element (t,c,p) at lane
+ *                 (c%4)*16 + p%16 of block (p/16, c/4, t).  Padding is zero.
+ *   M (products): float M[PB][KB][T][64][4], element (t,k,p) at lane
+ *                 16*((k%16)/4) + p%16, slot k%4, of block (p/16, k/16, t).
+ *   Each 64-float (256 B) group is exactly one wave's operand of a 16x16x4 fp32
+ *   MFMA; each 256-float group of M is one wave's accumulator tile.
+ */
+#ifndef WINO_H
+#define WINO_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define WINO_OK                0
+#define WINO_ERR_INVALID_ARG  (-1)   /* null pointer, non-positive size, Ho/Wo < 1, overflow, aliasing */
+#define WINO_ERR_UNSUPPORTED  (-2)   /* m not in {2, 4}, or an unknown flag bit */
+#define WINO_ERR_WORKSPACE    (-3)   /* workspace missing or smaller than required */
+#define WINO_ERR_HIP          (-4)   /* a HIP launch or query failed */
+
+/* ---- flags -------------------------------------------------------------- */
+#define WINO_FLAG_RELU     0x001u   /* y = max(y, 0), applied in the output transform */
+#define WINO_ALGO_AUTO     0x000u   /* let the planner choose (default) */
+#define WINO_ALGO_FUSED    0x100u   /* one kernel: input transform -> GEMMs -> output transform */
+#define WINO_ALGO_STAGED   0x200u   /* three kernels through the workspace (V, then M) */
+#define WINO_ALGO_MASK     0xF00u
+/* Optional overrides of the fused kernel's variant (0 = planner's choice):
+ *   WINO_KSUB(n)   n in {1,2}: 16*n output channels per wave (n = 2 only
+ *                  for m = 2);
+ *   WINO_CSPLIT(n) n in {1,2,4}: waves of a workgroup that split the input
+ *                  channels of one output unit, reduced in a fixed order.
+ * Results of every variant agree to fp32 rounding; unsupported combinations
+ * return WINO_ERR_UNSUPPORTED. */
+#define WINO_KSUB(n)       (((unsigned)(n) & 0xFu) << 12)
+#define WINO_CSPLIT(n)     (((unsigned)(n) & 0xFu) << 16)
+
+/* Human-readable text of a status code (static storage, never NULL). */
+const char* wino_status_string(int status);
+
+/* Library version, 100*major + minor. */
+int wino_version(void);
+
+/* Bytes of the transformed-filter buffer U for (C, K, m): 4*T*Cp*Kp.
+ * Returns 0 if C or K <= 0, m is not 2 or 4, or the size overflows. */
+size_t wino_filter_bytes(int C, int K, int m);
+
+/* Bytes of V (input transform output) and of M (GEMM output) for a layer.
+ * Return 0 on invalid arguments (same rules as wino_conv2d). */
+size_t wino_input_tf_bytes(int N, int C, int H, int W, int pad, int m);
+size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m);
+
+/* Workspace bytes wino_conv2d needs for this layer and algorithm choice
+ * (flags as for wino_conv2d; only the WINO_ALGO_* bits matter).  0 means the
+ * chosen plan needs none (workspace may then be NULL).  Returns (size_t)-1 on
+ * invalid arguments. */
+size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags);
+
+/* Offline filter transform (Eq. 1's W w W^T; Sec. 2, the GEMM step's 'B'
+ * matrices, computed once per weight set and reused).
+ *   g : [K][C][3][3] fp32 (KCRS), read only.
+ *   U : wino_filter_bytes(C,K,m) bytes, written in the U layout above.  Each
+ *       element is G g G^T evaluated in fp64 and rounded once to fp32.
+ * Errors: INVALID_ARG (null, C/K <= 0, overflow), UNSUPPORTED (m), HIP. */
+int wino_filter_transform(const float* g, float* U, int C, int K, int m, void* stream);
+
+/* One 3x3 stride-1 convolution layer (Eq. 1 over all regions; Sec. 2).
+ *   x : [N][C][H][W] fp32 (NCHW), read only.
+ *   U : output of wino_filter_transform with the same (C, K, m), read only.
+ *   y : [N][K][Ho][Wo] fp32 (NCHW), written; must not overlap x.
+ *   flags : WINO_FLAG_RELU and/or one WINO_ALGO_* value.
+ *   workspace / workspace_bytes : device scratch of at least
+ *       wino_workspace_bytes(N,C,H,W,K,pad,m,flags) bytes (V and M of the staged
+ *       algorithm); may be NULL/0 when that is 0.  Contents on return are
+ *       unspecified; calls sharing one workspace must not overlap in time.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */
+int wino_conv2d(const float* x, const float* U, float* y,
+                int N, int C, int H, int W, int K, int pad, int m,
+                unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Stage 1 alone, input transform (Sec. 2.1.1 for m = 2; Eq. 1's X^T x X):
+ * every region of every channel to the transform domain, scattered into the
+ * per-position matrices.
+ *   x : [N][C][H][W] fp32; V : wino_input_tf_bytes(...) bytes, V layout.
+ * For m = 2 each element is computed with the paper's printed add/sub order
+ * (a pass over rows, then the same pass over columns) and is bit-exact. */
+int wino_input_transform(const float* x, float* V, int N, int C, int H, int W,
+                         int pad, int m, void* stream);
+
+/* Stage 2 alone, the T per-position GEMMs (Sec. 2.2):
+ *   M_t[k][p] = sum_c U_t[c][k] * V_t[c][p]  for every t < T.
+ *   U : filter layout for (C, K, m); V : input layout for (N,C,H,W,pad,m);
+ *   M : wino_gemm_out_bytes(N,K,H,W,pad,m) bytes, M layout. */
+int wino_batched_gemm(const float* U, const float* V, float* M,
+                      int N, int C, int H, int W, int K, int pad, int m, void* stream);
+
+/* Stage 3 alone, output transform (Eq. 1's Z^T ( . ) Z; Sec. 2, third step):
+ * gather the T values of every (tile, output channel), inverse-transform, write
+ * the m x m block into y (NCHW), cropped to Ho x Wo.  flags: WINO_FLAG_RELU. */
+int wino_output_transform(const float* M, float* y, int N, int K, int H, int W,
+                          int pad, int m, unsigned flags, void* stream);
+
+/* Glue between the blocks of a VGG-style stack (not part of the method):
+ * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
+int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINO_H */

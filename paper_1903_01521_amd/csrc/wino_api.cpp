@@ -1,0 +1,223 @@
+// C-ABI of libwino: argument validation, layer planning and dispatch.
+// Every check runs before the first HIP call, so invalid calls enqueue nothing.
+#include "../../include/wino.h"
+#include "wino_internal.h"
+
+#include <stdint.h>
+
+using namespace wino;
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t)1 << 40;      // per tensor, well inside size_t
+constexpr int64_t kMaxTiles = ((int64_t)1 << 31) - 64;
+
+constexpr unsigned kKsubShift = 12, kCsplitShift = 16;
+constexpr unsigned kKnownFlags = WINO_FLAG_RELU | WINO_ALGO_MASK | (0xFu << kKsubShift) | (0xFu << kCsplitShift);
+
+// Checked product of non-negative int64 values; false on overflow past kMaxElems.
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > kMaxElems / a) return false;
+    *out = a * b;
+    return *out <= kMaxElems;
+}
+
+int make_geom(int N, int C, int H, int W, int K, int pad, int m, Geom* g) {
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || pad < 0) return WINO_ERR_INVALID_ARG;
+    if (m != 2 && m != 4) return WINO_ERR_UNSUPPORTED;
+    const int64_t Ho = (int64_t)H + 2 * (int64_t)pad - 2;
+    const int64_t Wo = (int64_t)W + 2 * (int64_t)pad - 2;
+    if (Ho < 1 || Wo < 1 || Ho > INT32_MAX / 2 || Wo > INT32_MAX / 2) return WINO_ERR_INVALID_ARG;
+    const int64_t th = (Ho + m - 1) / m, tw = (Wo + m - 1) / m;
+    int64_t t1, P, xin, xout;
+    if (!mul_ok(th, tw, &t1) || !mul_ok(t1, N, &P) || P > kMaxTiles) return WINO_ERR_INVALID_ARG;
+    if (!mul_ok((int64_t)N * C, (int64_t)H * W, &xin)) return WINO_ERR_INVALID_ARG;
+    if (!mul_ok((int64_t)N * K, Ho * Wo, &xout)) return WINO_ERR_INVALID_ARG;
+    const int64_t A = m + 2, T = A * A;
+    const int64_t CQ = (C + 3) / 4, KB = (K + 15) / 16, PB = (P + 15) / 16;
+    int64_t v, mm;
+    if (!mul_ok(PB * CQ, T * 64, &v) || !mul_ok(PB * KB, T * 256, &mm)) return WINO_ERR_INVALID_ARG;
+    g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
+    g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
+    g->A = (int)A; g->T = (int)T;
+    g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
+    return WINO_OK;
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Plan: which algorithm, and which fused-kernel variant.
+struct Plan {
+    unsigned algo;        // WINO_ALGO_FUSED or WINO_ALGO_STAGED
+    FusedCfg cfg;
+};
+
+bool valid_cfg(int m, FusedCfg c) {
+    if (c.csplit != 1 && c.csplit != 2 && c.csplit != 4) return false;
+    if (m == 2) return c.ksub == 1 || c.ksub == 2;
+    return c.ksub == 1;
+}
+
+int make_plan(const Geom& g, unsigned flags, Plan* p) {
+    if (flags & ~kKnownFlags) return WINO_ERR_UNSUPPORTED;
+    const unsigned algo = flags & WINO_ALGO_MASK;
+    if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED)
+        return WINO_ERR_UNSUPPORTED;
+    const int ks_req = (int)((flags >> kKsubShift) & 0xF);
+    const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
+    p->algo = (algo == WINO_ALGO_STAGED) ? WINO_ALGO_STAGED : WINO_ALGO_FUSED;
+    // Fused variant: one wave per (16 tiles x 16*ksub filters) unit; when the
+    // grid has too few units to give every SIMD of the 256 CUs work, split the
+    // channel loop over 2 or 4 waves of a workgroup.
+    FusedCfg c;
+    c.ksub = ks_req ? ks_req : 1;
+    if (cs_req) {
+        c.csplit = cs_req;
+    } else {
+        const long units = (long)g.PB * ((g.KB + c.ksub - 1) / c.ksub);
+        c.csplit = 1;
+        while (c.csplit < 4 && units * c.csplit < 2048 && g.CQ >= 2 * c.csplit) c.csplit *= 2;
+    }
+    if (p->algo == WINO_ALGO_FUSED && !valid_cfg(g.m, c)) return WINO_ERR_UNSUPPORTED;
+    p->cfg = c;
+    return WINO_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? WINO_OK : WINO_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* wino_status_string(int status) {
+    switch (status) {
+        case WINO_OK: return "ok";
+        case WINO_ERR_INVALID_ARG: return "invalid argument";
+        case WINO_ERR_UNSUPPORTED: return "unsupported configuration";
+        case WINO_ERR_WORKSPACE: return "workspace missing or too small";
+        case WINO_ERR_HIP: return "HIP launch error";
+        default: return "unknown status";
+    }
+}
+
+int wino_version(void) { return 100; }
+
+size_t wino_filter_bytes(int C, int K, int m) {
+    if (C <= 0 || K <= 0 || (m != 2 && m != 4)) return 0;
+    int64_t e;
+    if (!mul_ok((int64_t)(C + 3) / 4 * 4, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, (m + 2) * (m + 2), &e))
+        return 0;
+    return (size_t)e * sizeof(float);
+}
+
+size_t wino_input_tf_bytes(int N, int C, int H, int W, int pad, int m) {
+    Geom g;
+    if (make_geom(N, C, H, W, 1, pad, m, &g) != WINO_OK) return 0;
+    return v_elems(g) * sizeof(float);
+}
+
+size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m) {
+    Geom g;
+    if (make_geom(N, 1, H, W, K, pad, m, &g) != WINO_OK) return 0;
+    return m_elems(g) * sizeof(float);
+}
+
+size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags) {
+    Geom g;
+    Plan p;
+    if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
+        return (size_t)-1;
+    if (p.algo == WINO_ALGO_FUSED) return 0;
+    return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
+}
+
+int wino_filter_transform(const float* gw, float* U, int C, int K, int m, void* stream) {
+    if (!gw || !U || C <= 0 || K <= 0) return WINO_ERR_INVALID_ARG;
+    if (m != 2 && m != 4) return WINO_ERR_UNSUPPORTED;
+    const size_t ub = wino_filter_bytes(C, K, m);
+    if (ub == 0) return WINO_ERR_INVALID_ARG;
+    if (overlap(gw, (size_t)K * C * 9 * sizeof(float), U, ub)) return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_filter_transform(gw, U, C, K, m, (hipStream_t)stream));
+}
+
+int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
+                unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    int st = make_geom(N, C, H, W, K, pad, m, &g);
+    if (st != WINO_OK) return st;
+    Plan p;
+    st = make_plan(g, flags, &p);
+    if (st != WINO_OK) return st;
+    const size_t xb = (size_t)N * C * H * W * sizeof(float);
+    const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
+    const size_t ub = wino_filter_bytes(C, K, m);
+    if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
+    const bool relu = (flags & WINO_FLAG_RELU) != 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (p.algo == WINO_ALGO_FUSED) return hip_status(launch_fused(x, U, y, g, p.cfg, relu, s));
+
+    const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
+    const size_t need = vb + m_elems(g) * sizeof(float);
+    if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+    if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+        return WINO_ERR_INVALID_ARG;
+    float* V = (float*)workspace;
+    float* M = (float*)((char*)workspace + vb);
+    st = hip_status(launch_input_transform(x, V, g, s));
+    if (st != WINO_OK) return st;
+    st = hip_status(launch_batched_gemm(U, V, M, g, s));
+    if (st != WINO_OK) return st;
+    return hip_status(launch_output_transform(M, y, g, relu, s));
+}
+
+int wino_input_transform(const float* x, float* V, int N, int C, int H, int W, int pad, int m, void* stream) {
+    if (!x || !V) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    const int st = make_geom(N, C, H, W, 1, pad, m, &g);
+    if (st != WINO_OK) return st;
+    if (overlap(x, (size_t)N * C * H * W * sizeof(float), V, v_elems(g) * sizeof(float)))
+        return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_input_transform(x, V, g, (hipStream_t)stream));
+}
+
+int wino_batched_gemm(const float* U, const float* V, float* M, int N, int C, int H, int W, int K, int pad, int m,
+                      void* stream) {
+    if (!U || !V || !M) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    const int st = make_geom(N, C, H, W, K, pad, m, &g);
+    if (st != WINO_OK) return st;
+    const size_t mb = m_elems(g) * sizeof(float);
+    if (overlap(M, mb, U, wino_filter_bytes(C, K, m)) || overlap(M, mb, V, v_elems(g) * sizeof(float)))
+        return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_batched_gemm(U, V, M, g, (hipStream_t)stream));
+}
+
+int wino_output_transform(const float* M, float* y, int N, int K, int H, int W, int pad, int m, unsigned flags,
+                          void* stream) {
+    if (!M || !y) return WINO_ERR_INVALID_ARG;
+    if (flags & ~WINO_FLAG_RELU) return WINO_ERR_UNSUPPORTED;
+    Geom g;
+    const int st = make_geom(N, 1, H, W, K, pad, m, &g);
+    if (st != WINO_OK) return st;
+    if (overlap(M, m_elems(g) * sizeof(float), y, (size_t)N * K * g.Ho * g.Wo * sizeof(float)))
+        return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_output_transform(M, y, g, (flags & WINO_FLAG_RELU) != 0, (hipStream_t)stream));
+}
+
+int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream) {
+    if (!x || !y || N <= 0 || C <= 0 || H < 2 || W < 2) return WINO_ERR_INVALID_ARG;
+    int64_t e;
+    if (!mul_ok((int64_t)N * C, (int64_t)H * W, &e)) return WINO_ERR_INVALID_ARG;
+    if (overlap(x, (size_t)e * sizeof(float), y, (size_t)N * C * (H / 2) * (W / 2) * sizeof(float)))
+        return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_maxpool2x2(x, y, N, C, H, W, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,38 @@
+// Host-side plan of one layer and the launchers the C-ABI calls.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace wino {
+
+// Geometry of a 3x3 stride-1 layer tiled into m x m output regions, and the
+// blocked transform-domain extents (see the layout notes in wino.h).
+struct Geom {
+    int N, C, H, W, K, pad, m;
+    int Ho, Wo, th, tw;
+    int P;          // tiles, N*th*tw
+    int A, T;       // alpha = m + 2, T = alpha^2
+    int CQ, KB, PB; // 4-channel quads, 16-filter blocks, 16-tile blocks
+};
+
+// Kernel variant of the fused algorithm.
+struct FusedCfg {
+    int ksub;       // 16-filter blocks per wave (accumulators: 4*T*ksub per lane)
+    int csplit;     // waves of one workgroup sharing one output unit, splitting C
+};
+
+size_t filter_elems(int C, int K, int m);                // T*Cp*Kp
+size_t v_elems(const Geom& g);                           // PB*CQ*T*64
+size_t m_elems(const Geom& g);                           // PB*KB*T*256
+
+hipError_t launch_filter_transform(const float* g, float* U, int C, int K, int m, hipStream_t s);
+hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s);
+hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s);
+hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s);
+hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg cfg,
+                        bool relu, hipStream_t s);
+hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s);
+
+}  // namespace wino

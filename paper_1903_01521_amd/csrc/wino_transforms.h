@@ -1,0 +1,165 @@
+// Device-side Cook-Toom transforms for F(2x2,3x3) and F(4x4,3x3).
+//
+// The matrices (Lavin's names; the paper writes X^T for B^T, W for G and Z^T
+// for A^T, Eq. 1):
+//
+//   m = 2, alpha = 4, points {0, 1, -1, inf}; B^T is the matrix the paper prints
+//   for the F(2x2,3x3) input transform (Sec. 2.1.1):
+//     B^T = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1]
+//     G   = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1]
+//     A^T = [1 1 1 0; 0 1 -1 -1]
+//
+//   m = 4, alpha = 6, points {0, 1, -1, 2, -2, inf}:
+//     B^T = [4 0 -5 0 1 0; 0 -4 -4 1 1 0; 0 4 -4 -1 1 0;
+//            0 -2 -1 2 1 0; 0 2 -1 -2 1 0; 0 4 0 -5 0 1]
+//     G   = [1/4 0 0; -1/6 -1/6 -1/6; -1/6 1/6 -1/6;
+//            1/24 1/12 1/6; 1/24 -1/12 1/6; 0 0 1]
+//     A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 0; 0 1 1 4 4 0; 0 1 -1 8 -8 1]
+//
+// Both compute correlation: y[i] = sum_k g[k] d[i+k].  Every 2-D transform is
+// the 1-D transform applied along rows (left factor), then along columns
+// (right factor): B^T d B = ((B^T d)) then .B, and likewise A^T M A.  For m = 2
+// this is the two-pass order the paper prints, so each value is exactly two
+// levels of rounded fp32 add/sub in that order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace wino {
+
+template <int MT> struct Tile {
+    static constexpr int A = MT + 2;   // region side, alpha
+    static constexpr int T = A * A;    // transform-domain elements per region
+};
+
+// ---------------------------------------------------------------- 1-D B^T
+__device__ __forceinline__ void bt_1d(const float (&a)[4], float (&r)[4]) {
+    r[0] = a[0] - a[2];
+    r[1] = a[1] + a[2];
+    r[2] = a[2] - a[1];
+    r[3] = a[1] - a[3];
+}
+
+__device__ __forceinline__ void bt_1d(const float (&a)[6], float (&r)[6]) {
+    // rows of B^T for m = 4, grouped so that shared differences are formed once
+    const float d31 = a[3] - a[1];
+    const float d42 = a[4] - a[2];
+    r[0] = __builtin_fmaf(4.0f, a[0] - a[2], a[4] - a[2]);     //  4a0 - 5a2 + a4
+    r[1] = __builtin_fmaf(-4.0f, a[1] + a[2], a[3] + a[4]);    // -4a1 - 4a2 + a3 + a4
+    r[2] = __builtin_fmaf(4.0f, a[1] - a[2], a[4] - a[3]);     //  4a1 - 4a2 - a3 + a4
+    r[3] = __builtin_fmaf(2.0f, d31, d42);                     // -2a1 - a2 + 2a3 + a4
+    r[4] = __builtin_fmaf(-2.0f, d31, d42);                    //  2a1 - a2 - 2a3 + a4
+    r[5] = __builtin_fmaf(4.0f, a[1] - a[3], a[5] - a[3]);     //  4a1 - 5a3 + a5
+}
+
+// ---------------------------------------------------------------- 1-D A^T
+__device__ __forceinline__ void at_1d(const float (&a)[4], float (&r)[2]) {
+    r[0] = a[0] + a[1] + a[2];
+    r[1] = a[1] - a[2] - a[3];
+}
+
+__device__ __forceinline__ void at_1d(const float (&a)[6], float (&r)[4]) {
+    const float s12 = a[1] + a[2], d12 = a[1] - a[2];
+    const float s34 = a[3] + a[4], d34 = a[3] - a[4];
+    r[0] = a[0] + s12 + s34;                                   // a0 + a1 + a2 + a3 + a4
+    r[1] = __builtin_fmaf(2.0f, d34, d12);                     // a1 - a2 + 2a3 - 2a4
+    r[2] = __builtin_fmaf(4.0f, s34, s12);                     // a1 + a2 + 4a3 + 4a4
+    r[3] = __builtin_fmaf(8.0f, d34, d12) + a[5];              // a1 - a2 + 8a3 - 8a4 + a5
+}
+
+// ---------------------------------------------------------------- 2-D
+// v[xi*A + nu] = (B^T d B)[xi][nu]
+template <int MT>
+__device__ __forceinline__ void input_tf(const float (&d)[MT + 2][MT + 2], float (&v)[(MT + 2) * (MT + 2)]) {
+    constexpr int A = MT + 2;
+    float s[A][A];
+#pragma unroll
+    for (int j = 0; j < A; ++j) {          // along rows: column j of B^T d
+        float col[A], r[A];
+#pragma unroll
+        for (int i = 0; i < A; ++i) col[i] = d[i][j];
+        bt_1d(col, r);
+#pragma unroll
+        for (int i = 0; i < A; ++i) s[i][j] = r[i];
+    }
+#pragma unroll
+    for (int i = 0; i < A; ++i) {          // along columns: row i of (B^T d) B
+        float r[A];
+        bt_1d(s[i], r);
+#pragma unroll
+        for (int j = 0; j < A; ++j) v[i * A + j] = r[j];
+    }
+}
+
+// o[i][j] = (A^T M A)[i][j], M[xi][nu] = mv[xi*A + nu]
+template <int MT>
+__device__ __forceinline__ void output_tf(const float (&mv)[(MT + 2) * (MT + 2)], float (&o)[MT][MT]) {
+    constexpr int A = MT + 2;
+    float s[MT][A];
+#pragma unroll
+    for (int j = 0; j < A; ++j) {          // along rows: column j of A^T M
+        float col[A], r[MT];
+#pragma unroll
+        for (int i = 0; i < A; ++i) col[i] = mv[i * A + j];
+        at_1d(col, r);
+#pragma unroll
+        for (int i = 0; i < MT; ++i) s[i][j] = r[i];
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {         // along columns: row i of (A^T M) A
+        float r[MT];
+        at_1d(s[i], r);
+#pragma unroll
+        for (int j = 0; j < MT; ++j) o[i][j] = r[j];
+    }
+}
+
+// ---------------------------------------------------------------- filter, fp64
+// U = G g G^T evaluated in fp64 with an integer-scaled G (S*G has integer
+// entries: S = 2 for m = 2, S = 24 for m = 4), divided by S^2 once at the end.
+template <int MT> struct GScaled;
+template <> struct GScaled<2> {
+    static constexpr double S2 = 4.0;
+    __device__ static void rows(const double (&a)[3], double (&r)[4]) {
+        r[0] = 2.0 * a[0];
+        r[1] = a[0] + a[1] + a[2];
+        r[2] = a[0] - a[1] + a[2];
+        r[3] = 2.0 * a[2];
+    }
+};
+template <> struct GScaled<4> {
+    static constexpr double S2 = 576.0;
+    __device__ static void rows(const double (&a)[3], double (&r)[6]) {
+        r[0] = 6.0 * a[0];
+        r[1] = -4.0 * (a[0] + a[1] + a[2]);
+        r[2] = -4.0 * (a[0] - a[1] + a[2]);
+        r[3] = a[0] + 2.0 * a[1] + 4.0 * a[2];
+        r[4] = a[0] - 2.0 * a[1] + 4.0 * a[2];
+        r[5] = 24.0 * a[2];
+    }
+};
+
+// u[xi*A + nu] = (G g G^T)[xi][nu] rounded once to fp32
+template <int MT>
+__device__ __forceinline__ void filter_tf(const float (&g)[3][3], float (&u)[(MT + 2) * (MT + 2)]) {
+    constexpr int A = MT + 2;
+    double s[A][3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {          // (S G) g: column j
+        double col[3] = {(double)g[0][j], (double)g[1][j], (double)g[2][j]};
+        double r[A];
+        GScaled<MT>::rows(col, r);
+#pragma unroll
+        for (int i = 0; i < A; ++i) s[i][j] = r[i];
+    }
+#pragma unroll
+    for (int i = 0; i < A; ++i) {          // ((S G) g) (S G)^T: row i
+        double row[3] = {s[i][0], s[i][1], s[i][2]};
+        double r[A];
+        GScaled<MT>::rows(row, r);
+#pragma unroll
+        for (int j = 0; j < A; ++j) u[i * A + j] = (float)(r[j] / GScaled<MT>::S2);
+    }
+}
+
+}  // namespace wino

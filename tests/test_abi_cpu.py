@@ -1,0 +1,107 @@
+"""The C-ABI library loads, exports what include/wino.h declares, and rejects
+invalid arguments before any HIP call (CPU only: no call here reaches a kernel)."""
+import pytest
+
+from paper_1903_01521_amd import binding as B
+
+# A non-null address that is never dereferenced: every call using it carries
+# another invalid argument that validation rejects first.
+FAKE = 0x1000
+
+
+def test_library_exports_every_declared_symbol():
+    names = B.header_functions()
+    assert len(names) >= 12
+    so = B.lib()
+    for n in names:
+        assert hasattr(so, n), n
+
+
+def test_version_and_status_strings():
+    assert B.wino_version() >= 100
+    for st in (B.WINO_OK, B.WINO_ERR_INVALID_ARG, B.WINO_ERR_UNSUPPORTED, B.WINO_ERR_WORKSPACE,
+               B.WINO_ERR_HIP):
+        assert B.wino_status_string(st) and B.wino_status_string(st) != "unknown status"
+    assert B.wino_status_string(12345) == "unknown status"
+
+
+@pytest.mark.parametrize("m,T", [(2, 16), (4, 36)])
+def test_filter_bytes(m, T):
+    assert B.wino_filter_bytes(64, 64, m) == 4 * T * 64 * 64
+    assert B.wino_filter_bytes(3, 20, m) == 4 * T * 4 * 32       # C padded to 4, K to 16
+    assert B.wino_filter_bytes(0, 8, m) == 0
+    assert B.wino_filter_bytes(8, 0, m) == 0
+    assert B.wino_filter_bytes(8, 8, 3) == 0
+
+
+def test_transform_domain_sizes():
+    # N=1, 112x112, pad 1, m=4: 28x28 tiles = 784 -> 49 blocks of 16.
+    assert B.wino_input_tf_bytes(1, 64, 112, 112, 1, 4) == 4 * 49 * 16 * 36 * 64
+    assert B.wino_gemm_out_bytes(1, 64, 112, 112, 1, 4) == 4 * 49 * 4 * 36 * 256
+    # ragged: 57x57 -> 15x15 = 225 tiles -> 15 blocks
+    assert B.wino_input_tf_bytes(1, 48, 57, 57, 1, 4) == 4 * 15 * 12 * 36 * 64
+    assert B.wino_input_tf_bytes(1, 8, 2, 2, 0, 4) == 0         # Ho < 1
+
+
+def test_workspace_bytes():
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_FUSED) == 0
+    staged = B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_STAGED)
+    assert staged >= B.wino_input_tf_bytes(1, 64, 112, 112, 1, 4) + B.wino_gemm_out_bytes(1, 64, 112, 112, 1, 4)
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 3, 0) == 2**64 - 1
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, 0x300) == 2**64 - 1
+
+
+GOOD = dict(N=1, C=4, H=8, W=8, K=4, pad=1, m=4)
+
+
+def _conv(x=FAKE, U=FAKE, y=FAKE + 0x100000, flags=0, ws=None, wsb=0, **kw):
+    a = dict(GOOD)
+    a.update(kw)
+    return B.wino_conv2d(x, U, y, a["N"], a["C"], a["H"], a["W"], a["K"], a["pad"], a["m"],
+                         flags, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), B.WINO_ERR_INVALID_ARG),
+    (dict(U=None), B.WINO_ERR_INVALID_ARG),
+    (dict(y=None), B.WINO_ERR_INVALID_ARG),
+    (dict(N=0), B.WINO_ERR_INVALID_ARG),
+    (dict(C=-1), B.WINO_ERR_INVALID_ARG),
+    (dict(H=0), B.WINO_ERR_INVALID_ARG),
+    (dict(W=0), B.WINO_ERR_INVALID_ARG),
+    (dict(K=0), B.WINO_ERR_INVALID_ARG),
+    (dict(pad=-1), B.WINO_ERR_INVALID_ARG),
+    (dict(H=2, pad=0), B.WINO_ERR_INVALID_ARG),             # Ho = 0
+    (dict(m=3), B.WINO_ERR_UNSUPPORTED),
+    (dict(m=6), B.WINO_ERR_UNSUPPORTED),
+    (dict(flags=0x80000000), B.WINO_ERR_UNSUPPORTED),        # unknown flag bit
+    (dict(flags=0x300), B.WINO_ERR_UNSUPPORTED),             # unknown algorithm
+    (dict(flags=B.WINO_ALGO_FUSED | B.WINO_CSPLIT(3)), B.WINO_ERR_UNSUPPORTED),
+    (dict(flags=B.WINO_ALGO_FUSED | B.WINO_KSUB(2)), B.WINO_ERR_UNSUPPORTED),   # m=4
+    (dict(flags=B.WINO_ALGO_STAGED), B.WINO_ERR_WORKSPACE),  # no workspace
+    (dict(flags=B.WINO_ALGO_STAGED, ws=FAKE + 0x900000, wsb=16), B.WINO_ERR_WORKSPACE),
+    (dict(y=FAKE), B.WINO_ERR_INVALID_ARG),                  # y aliases x
+    (dict(y=FAKE + 64), B.WINO_ERR_INVALID_ARG),             # y overlaps x
+    (dict(N=1 << 20, C=1 << 10, H=1 << 10, W=1 << 10), B.WINO_ERR_INVALID_ARG),   # size overflow
+])
+def test_conv2d_rejects(kw, status):
+    assert _conv(**kw) == status
+
+
+def test_stage_entry_points_reject():
+    assert B.wino_filter_transform(None, FAKE, 4, 4, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform(FAKE, None, 4, 4, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform(FAKE, FAKE + 0x10000, 0, 4, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform(FAKE, FAKE + 0x10000, 4, 4, 5) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_filter_transform(FAKE, FAKE + 4, 4, 4, 4) == B.WINO_ERR_INVALID_ARG    # overlap
+    assert B.wino_input_transform(None, FAKE, 1, 4, 8, 8, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_input_transform(FAKE, FAKE + 0x100000, 1, 4, 8, 8, -2, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_input_transform(FAKE, FAKE + 0x100000, 1, 4, 8, 8, 1, 7) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_batched_gemm(FAKE, None, FAKE, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_batched_gemm(FAKE, FAKE, FAKE + 8, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_output_transform(None, FAKE, 1, 4, 8, 8, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_output_transform(FAKE, FAKE + 0x1000000, 1, 4, 8, 8, 1, 4, 0x100) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_output_transform(FAKE, FAKE + 0x1000000, 0, 4, 8, 8, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_maxpool2x2(FAKE, None, 1, 1, 4, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_maxpool2x2(FAKE, FAKE + 0x10000, 1, 1, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_maxpool2x2(FAKE, FAKE + 4, 1, 1, 4, 4) == B.WINO_ERR_INVALID_ARG     # overlap

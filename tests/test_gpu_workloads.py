@@ -1,0 +1,112 @@
+"""The synthetic workloads at their full sizes, on the GPU, against the fp64 oracle.
+
+Single layers small enough are checked whole; large batches are run whole on the
+GPU and checked on sampled images (each image's output depends only on that
+image).  Stacks are gated per layer -- the oracle recomputes each layer from the
+GPU chain's own input to that layer -- and end to end against the oracle's own
+fp64 chain."""
+import numpy as np
+import pytest
+import torch
+
+import gpu_helpers as h
+from oracle import direct
+from oracle import nn as onn
+from paper_1903_01521_amd import binding as B
+from paper_1903_01521_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+TOL = {2: 1e-4, 4: 1e-3}
+E2E_TOL = 1e-3
+
+
+def _layer(hx: torch.Tensor, g: np.ndarray, L: wl.Layer) -> torch.Tensor:
+    U = h.filter_transform(g, L.m)
+    return h.conv2d(hx, U, L.K, L.pad, L.m, B.WINO_FLAG_RELU if L.relu else 0)
+
+
+def _pool(hy: torch.Tensor) -> torch.Tensor:
+    N, C, H, W = hy.shape
+    out = torch.empty((N, C, H // 2, W // 2), dtype=torch.float32, device=h.DEV)
+    B.check(B.wino_maxpool2x2(hy, out, N, C, H, W), "wino_maxpool2x2")
+    return out
+
+
+def _run_stack(w: wl.Workload, sample):
+    """Run the whole stack on the GPU; gate every layer on the sampled images;
+    return (GPU final output of the samples, the samples' input)."""
+    x, gs = wl.generate(w)
+    hx = h.dev(x)
+    for li, (L, g) in enumerate(zip(w.layers, gs)):
+        print(f"{w.name} layer {li}: C={L.C} K={L.K} {L.H}x{L.W} m={L.m}", flush=True)
+        xin = h.host(hx)[sample].astype(np.float64)
+        hy = _layer(hx, g, L)
+        y = h.host(hy)[sample]
+        ref = direct.conv2d(xin, g, L.pad)
+        if L.relu:
+            ref = onn.relu(ref)
+        err = h.normwise_err(y, ref)
+        print(f"  normwise err {err:.2e}", flush=True)
+        assert err <= TOL[L.m], (li, err)
+        hx = _pool(hy) if L.pool else hy
+    return h.host(hx)[sample], x[sample], gs
+
+
+def _oracle_chain(w: wl.Workload, x: np.ndarray, gs) -> np.ndarray:
+    a = x.astype(np.float64)
+    for L, g in zip(w.layers, gs):
+        a = direct.conv2d(a, g, L.pad)
+        if L.relu:
+            a = onn.relu(a)
+        if L.pool:
+            a = onn.maxpool2x2(a)
+    return a
+
+
+@pytest.mark.parametrize("name", ["f2_n1_c32_k32_56x56", "f4_n1_c64_k64_112x112", "f4_n1_c48_k48_57x57",
+                                  "f4_lowc_n1_c3_k64_224x224"])
+def test_single_layer_whole(name):
+    w = wl.WORKLOADS[name]
+    L = w.first
+    x, (g,) = wl.generate(w)
+    print(f"{name}", flush=True)
+    y = h.host(_layer(h.dev(x), g, L))
+    ref = direct.conv2d(x, g, L.pad)
+    err = h.normwise_err(y, ref)
+    print(f"  normwise err {err:.2e}", flush=True)
+    assert err <= TOL[L.m]
+
+
+@pytest.mark.parametrize("name", ["f4_n64_c256_k256_56x56", "f4_lowc_n64_c3_k64_224x224"])
+def test_large_batch_sampled(name):
+    w = wl.WORKLOADS[name]
+    L = w.first
+    x, (g,) = wl.generate(w)
+    sample = [0, w.N // 2, w.N - 1]
+    print(f"{name} sample {sample}", flush=True)
+    y = h.host(_layer(h.dev(x), g, L))[sample]
+    ref = direct.conv2d(x[sample], g, L.pad)
+    err = h.normwise_err(y, ref)
+    print(f"  normwise err {err:.2e}", flush=True)
+    assert err <= TOL[L.m]
+
+
+def test_resnet_stage_n8():
+    w = wl.WORKLOADS["f4_resnet_stage_n8_c128_28x28"]
+    sample = list(range(w.N))
+    out, x, gs = _run_stack(w, sample)
+    ref = _oracle_chain(w, x, gs)
+    err = h.normwise_err(out, ref)
+    print(f"  end-to-end normwise err {err:.2e}", flush=True)
+    assert err <= E2E_TOL
+
+
+@pytest.mark.parametrize("name,sample", [("vgg16_stack_n1", [0]), ("vgg16_stack_n32", [0, 31])])
+def test_vgg16_stack(name, sample):
+    w = wl.WORKLOADS[name]
+    out, x, gs = _run_stack(w, sample)
+    ref = _oracle_chain(w, x, gs)
+    err = h.normwise_err(out, ref)
+    print(f"  end-to-end normwise err {err:.2e}", flush=True)
+    assert err <= E2E_TOL
