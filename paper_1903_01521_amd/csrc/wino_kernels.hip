@@ -51,31 +51,66 @@ __device__ __forceinline__ TileCoord decode_tile(int p, const Geom& g) {
     return t;
 }
 
-// d = the alpha x alpha region of channel c for tile tc, zero outside the image
-// (covers padding and the ragged overhang), zero for c >= C or a tile past P.
-// Every load is issued at an in-bounds address; invalid lanes read element 0
-// of the plane and discard it.
+// ---- region loads through a per-wave buffer resource -----------------------
+// Offsets are 32-bit byte offsets from the first image a 16-tile block touches.
+// Any offset >= kInvalid lies past the resource's record count, and the buffer
+// unit returns 0 for it: a padded row, column, channel or tile is read as zero
+// without a select.  The host guarantees that every valid offset is below
+// kInvalid (the images one block spans hold < 1 GiB of input).
+constexpr uint32_t kInvalid = 1u << 30;
+constexpr int kRsrcWord3 = 0x00020000;   // raw (unformatted) 32-bit buffer
+
 template <int MT>
-__device__ __forceinline__ void load_region(const float* __restrict__ x, const Geom& g,
-                                            const TileCoord& tc, int c,
-                                            float (&d)[MT + 2][MT + 2]) {
+struct RegionPlan {
+    __amdgpu_buffer_rsrc_t rsrc;     // wave-uniform
+    uint32_t row[MT + 2];            // lane's channel-plane + row byte offset, or kInvalid
+    uint32_t col[MT + 2];            // column byte offset, or kInvalid
+    uint32_t plane_bytes;            // H*W*4: step between channels (soffset units)
+};
+
+// p0 = first tile of the wave's 16-tile block (wave-uniform); tc = lane's tile;
+// cl = lane's channel within a quad.
+template <int MT>
+__device__ __forceinline__ RegionPlan<MT> make_region_plan(const float* __restrict__ x, const Geom& g,
+                                                           int p0, const TileCoord& tc, int cl) {
     constexpr int A = MT + 2;
-    const bool ok = tc.valid && c < g.C;
-    const int r0 = tc.ti * MT - g.pad;
-    const int c0 = tc.tj * MT - g.pad;
-    const float* plane = x + ((size_t)tc.n * g.C + (ok ? c : 0)) * (size_t)g.H * (size_t)g.W;
+    RegionPlan<MT> rp;
+    const int n0 = __builtin_amdgcn_readfirstlane(min(p0, g.P - 1) / (g.th * g.tw));
+    const size_t img = (size_t)g.C * g.H * g.W;
+    const size_t left = ((size_t)g.N - n0) * img * 4;
+    rp.rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(x + (size_t)n0 * img), (short)0,
+                                                (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
+    rp.plane_bytes = (uint32_t)g.H * g.W * 4;
+    const uint32_t plane = ((uint32_t)(tc.n - n0) * g.C + cl) * rp.plane_bytes;
+    const int r0 = tc.ti * MT - g.pad, c0 = tc.tj * MT - g.pad;
 #pragma unroll
     for (int u = 0; u < A; ++u) {
         const int row = r0 + u;
-        const bool rok = ok && row >= 0 && row < g.H;
+        rp.row[u] = (tc.valid && row >= 0 && row < g.H) ? plane + (uint32_t)row * g.W * 4 : kInvalid;
+    }
 #pragma unroll
-        for (int v = 0; v < A; ++v) {
-            const int col = c0 + v;
-            const bool vok = rok && col >= 0 && col < g.W;
-            const size_t off = vok ? (size_t)row * g.W + col : 0;
-            const float val = plane[off];
-            d[u][v] = vok ? val : 0.0f;
-        }
+    for (int v = 0; v < A; ++v) {
+        const int col = c0 + v;
+        rp.col[v] = (col >= 0 && col < g.W) ? (uint32_t)col * 4 : kInvalid;
+    }
+    return rp;
+}
+
+// d = the region of channel quad cq for this lane (channel cq*4 + cl), zero
+// outside the image, past the last channel, and for tiles past P.
+template <int MT>
+__device__ __forceinline__ void load_region(const RegionPlan<MT>& rp, const Geom& g, int cq, int cl,
+                                            float (&d)[MT + 2][MT + 2]) {
+    constexpr int A = MT + 2;
+    const uint32_t chan = (cq * 4 + cl < g.C) ? 0u : kInvalid;
+    const int soff = __builtin_amdgcn_readfirstlane(cq * 4 * (int)rp.plane_bytes);
+#pragma unroll
+    for (int u = 0; u < A; ++u) {
+        const uint32_t rowq = rp.row[u] + chan;
+#pragma unroll
+        for (int v = 0; v < A; ++v)
+            d[u][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                          rp.rsrc, (int)(rowq + rp.col[v]), soff, 0));
     }
 }
 
@@ -141,12 +176,14 @@ template <int MT>
 __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, float* __restrict__ V, Geom g) {
     constexpr int A = MT + 2, T = A * A;
     const int lane = threadIdx.x & 63;
-    const long w = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (w >= (long)g.PB * g.CQ) return;
     const int cq = (int)(w / g.PB), pb = (int)(w % g.PB);
+    const int cl = lane >> 4;
     const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const RegionPlan<MT> rp = make_region_plan<MT>(x, g, pb * 16, tc, cl);
     float d[A][A];
-    load_region<MT>(x, g, tc, cq * 4 + (lane >> 4), d);
+    load_region<MT>(rp, g, cq, cl, d);
     float v[T];
     input_tf<MT>(d, v);
     float* dst = V + (((size_t)pb * g.CQ + cq) * T) * 64 + lane;
@@ -267,7 +304,7 @@ __global__ __launch_bounds__(256) void k_fused(const float* __restrict__ x, cons
     constexpr int UNITS = 4 / CSPLIT;            // output units per workgroup
     constexpr int NB = KSUB * 4;                 // (k-block, slot) output groups per lane
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int cs = wave % CSPLIT;
     const int uw = wave / CSPLIT;
     const int KG = (g.KB + KSUB - 1) / KSUB;
@@ -275,8 +312,8 @@ __global__ __launch_bounds__(256) void k_fused(const float* __restrict__ x, cons
     const bool active = unit < (long)g.PB * KG;
     const int pb = active ? (int)(unit / KG) : 0;
     const int kg = active ? (int)(unit % KG) : 0;
-    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
     const int cl = lane >> 4;
+    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
 
     f32x4 acc[KSUB][T];
 #pragma unroll
@@ -284,21 +321,51 @@ __global__ __launch_bounds__(256) void k_fused(const float* __restrict__ x, cons
 #pragma unroll
         for (int t = 0; t < T; ++t) acc[s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    if (active) {
-        for (int cq = cs; cq < g.CQ; cq += CSPLIT) {
-            float d[A][A];
-            load_region<MT>(x, g, tc, cq * 4 + cl, d);
+    // Channel quads of this wave: cs, cs + CSPLIT, ...  (nq of them).
+    const int nq = (active && cs < g.CQ) ? (g.CQ - cs + CSPLIT - 1) / CSPLIT : 0;
+    if (nq > 0) {
+        const RegionPlan<MT> rp = make_region_plan<MT>(x, g, pb * 16, tc, cl);
+        // U block of (k-block kb, quad cq) starts at ((kb*CQ + cq)*T)*64.  A k-block
+        // past KB (only the last group when KSUB > 1) re-reads block KB-1; its
+        // results belong to filters >= K and are never stored.
+        const float* ublk[KSUB];
+#pragma unroll
+        for (int s = 0; s < KSUB; ++s)
+            ublk[s] = U + ((size_t)min(kg * KSUB + s, g.KB - 1) * g.CQ * T) * 64 + lane;
+        // Region values run one quad ahead in two register stages; each quad's
+        // filter values are requested at the top of its step, so their latency
+        // hides behind the input transform.
+        float xa[A][A], xb[A][A];
+        float ur[KSUB][T];
+        auto load_x = [&](int i, float (&xr)[A][A]) { load_region<MT>(rp, g, cs + i * CSPLIT, cl, xr); };
+        auto load_u = [&](int i) {
+            const size_t q = (size_t)(cs + i * CSPLIT) * T * 64;
+#pragma unroll
+            for (int s = 0; s < KSUB; ++s)
+#pragma unroll
+                for (int t = 0; t < T; ++t) ur[s][t] = ublk[s][q + t * 64];
+        };
+        auto compute = [&](float (&xr)[A][A]) {
             float v[T];
-            input_tf<MT>(d, v);
+            input_tf<MT>(xr, v);
 #pragma unroll
-            for (int s = 0; s < KSUB; ++s) {
-                const int kb = kg * KSUB + s;
-                if (kb < g.KB) {
-                    const float* ub = U + (((size_t)kb * g.CQ + cq) * T) * 64 + lane;
+            for (int s = 0; s < KSUB; ++s)
 #pragma unroll
-                    for (int t = 0; t < T; ++t) acc[s][t] = mfma16x16x4(ub[t * 64], v[t], acc[s][t]);
-                }
-            }
+                for (int t = 0; t < T; ++t) acc[s][t] = mfma16x16x4(ur[s][t], v[t], acc[s][t]);
+        };
+        load_x(0, xa);
+        int i = 0;
+        for (; i + 1 < nq; i += 2) {
+            load_u(i);
+            load_x(i + 1, xb);
+            compute(xa);
+            load_u(i + 1);
+            load_x(min(i + 2, nq - 1), xa);      // past the end: a harmless repeat load
+            compute(xb);
+        }
+        if (i < nq) {
+            load_u(i);
+            compute(xa);
         }
     }
 

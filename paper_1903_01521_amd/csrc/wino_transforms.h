@@ -116,10 +116,13 @@ __device__ __forceinline__ void output_tf(const float (&mv)[(MT + 2) * (MT + 2)]
 
 // ---------------------------------------------------------------- filter, fp64
 // U = G g G^T evaluated in fp64 with an integer-scaled G (S*G has integer
-// entries: S = 2 for m = 2, S = 24 for m = 4), divided by S^2 once at the end.
+// entries: S = 2 for m = 2, S = 24 for m = 4): the two small-integer products
+// are exact or nearly so in fp64, the scale 1/S^2 is applied once as a
+// multiplication (relative error <= 2^-52), and the result is rounded to fp32.
+// Integer-valued results (g a multiple of S^2) come out exact.
 template <int MT> struct GScaled;
 template <> struct GScaled<2> {
-    static constexpr double S2 = 4.0;
+    static constexpr double INV_S2 = 1.0 / 4.0;
     __device__ static void rows(const double (&a)[3], double (&r)[4]) {
         r[0] = 2.0 * a[0];
         r[1] = a[0] + a[1] + a[2];
@@ -128,7 +131,7 @@ template <> struct GScaled<2> {
     }
 };
 template <> struct GScaled<4> {
-    static constexpr double S2 = 576.0;
+    static constexpr double INV_S2 = 1.0 / 576.0;
     __device__ static void rows(const double (&a)[3], double (&r)[6]) {
         r[0] = 6.0 * a[0];
         r[1] = -4.0 * (a[0] + a[1] + a[2]);
@@ -139,7 +142,7 @@ template <> struct GScaled<4> {
     }
 };
 
-// u[xi*A + nu] = (G g G^T)[xi][nu] rounded once to fp32
+// u[xi*A + nu] = (G g G^T)[xi][nu], fp64 inside, rounded to fp32
 template <int MT>
 __device__ __forceinline__ void filter_tf(const float (&g)[3][3], float (&u)[(MT + 2) * (MT + 2)]) {
     constexpr int A = MT + 2;
@@ -158,7 +161,7 @@ __device__ __forceinline__ void filter_tf(const float (&g)[3][3], float (&u)[(MT
         double r[A];
         GScaled<MT>::rows(row, r);
 #pragma unroll
-        for (int j = 0; j < A; ++j) u[i * A + j] = (float)(r[j] / GScaled<MT>::S2);
+        for (int j = 0; j < A; ++j) u[i * A + j] = (float)(r[j] * GScaled<MT>::INV_S2);
     }
 }
 
