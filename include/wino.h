@@ -42,14 +42,17 @@
  *
  * Transform-domain layouts (MFMA-native blocking; Cp = roundup(C,4),
  * Kp = roundup(K,16), Pp = roundup(P,16), CQ = Cp/4, KB = Kp/16, PB = Pp/16)
- *   U (filters):  float U[KB][CQ][T][64], element (t,c,k) at lane
- *                 (c%4)*16 + k%16 of block (k/16, c/4, t).  Padding is zero.
- *   V (inputs):   float V[PB][CQ][T][64], element (t,c,p) at lane
- *                 (c%4)*16 + p%16 of block (p/16, c/4, t).  Padding is zero.
+ *   U (filters):  float U[KB][CQ][T/4][64][4], element (t,c,k) at lane
+ *                 (c%4)*16 + k%16, slot t%4, of group (k/16, c/4, t/4).
+ *                 Padding is zero.
+ *   V (inputs):   float V[PB][CQ][T/4][64][4], element (t,c,p) at lane
+ *                 (c%4)*16 + p%16, slot t%4, of group (p/16, c/4, t/4).
+ *                 Padding is zero.
  *   M (products): float M[PB][KB][T][64][4], element (t,k,p) at lane
  *                 16*((k%16)/4) + p%16, slot k%4, of block (p/16, k/16, t).
- *   Each 64-float (256 B) group is exactly one wave's operand of a 16x16x4 fp32
- *   MFMA; each 256-float group of M is one wave's accumulator tile.
+ *   For one position t, the 64 lanes of a U or V group are exactly one wave's
+ *   operand of a 16x16x4 fp32 MFMA, and a lane's 4 consecutive positions are
+ *   one 16-byte word; each 256-float block of M is one wave's accumulator tile.
  */
 #ifndef WINO_H
 #define WINO_H
@@ -74,13 +77,15 @@ extern "C" {
 #define WINO_ALGO_STAGED   0x200u   /* three kernels through the workspace (V, then M) */
 #define WINO_ALGO_MASK     0xF00u
 /* Optional overrides of the fused kernel's variant (0 = planner's choice):
- *   WINO_KSUB(n)   n in {1,2}: 16*n output channels per wave (n = 2 only
- *                  for m = 2);
- *   WINO_CSPLIT(n) n in {1,2,4}: waves of a workgroup that split the input
- *                  channels of one output unit, reduced in a fixed order.
+ *   WINO_BLOCK_1x16 / WINO_BLOCK_4x4: a workgroup's 16 tiles are one row of 16
+ *                  tiles, or a 4 x 4 square of tiles;
+ *   WINO_CSPLIT(n) n in {1,2,4,8} (m = 2) or {1,2,4} (m = 4): waves of a
+ *                  workgroup that split the input channels of one filter
+ *                  block, reduced in a fixed order.
  * Results of every variant agree to fp32 rounding; unsupported combinations
  * return WINO_ERR_UNSUPPORTED. */
-#define WINO_KSUB(n)       (((unsigned)(n) & 0xFu) << 12)
+#define WINO_BLOCK_1x16    0x1000u
+#define WINO_BLOCK_4x4     0x2000u
 #define WINO_CSPLIT(n)     (((unsigned)(n) & 0xFu) << 16)
 
 /* Human-readable text of a status code (static storage, never NULL). */
@@ -108,7 +113,7 @@ size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, u
  * matrices, computed once per weight set and reused).
  *   g : [K][C][3][3] fp32 (KCRS), read only.
  *   U : wino_filter_bytes(C,K,m) bytes, written in the U layout above.  Each
- *       element is G g G^T evaluated in fp64 and rounded once to fp32.
+ *       element is G g G^T evaluated in fp64 and rounded to fp32.
  * Errors: INVALID_ARG (null, C/K <= 0, overflow), UNSUPPORTED (m), HIP. */
 int wino_filter_transform(const float* g, float* U, int C, int K, int m, void* stream);
 

@@ -31,8 +31,8 @@ WINO_ALGO_STAGED = 0x200
 WINO_ALGO_MASK = 0xF00
 
 
-def WINO_KSUB(n: int) -> int:
-    return (n & 0xF) << 12
+WINO_BLOCK_1x16 = 0x1000
+WINO_BLOCK_4x4 = 0x2000
 
 
 def WINO_CSPLIT(n: int) -> int:

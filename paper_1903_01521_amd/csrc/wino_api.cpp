@@ -12,8 +12,8 @@ namespace {
 constexpr int64_t kMaxElems = (int64_t)1 << 40;      // per tensor, well inside size_t
 constexpr int64_t kMaxTiles = ((int64_t)1 << 31) - 64;
 
-constexpr unsigned kKsubShift = 12, kCsplitShift = 16;
-constexpr unsigned kKnownFlags = WINO_FLAG_RELU | WINO_ALGO_MASK | (0xFu << kKsubShift) | (0xFu << kCsplitShift);
+constexpr unsigned kBlockMask = WINO_BLOCK_1x16 | WINO_BLOCK_4x4, kCsplitShift = 16;
+constexpr unsigned kKnownFlags = WINO_FLAG_RELU | WINO_ALGO_MASK | kBlockMask | (0xFu << kCsplitShift);
 
 // Checked product of non-negative int64 values; false on overflow past kMaxElems.
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
@@ -58,10 +58,22 @@ struct Plan {
     FusedCfg cfg;
 };
 
+// Row groups per unit of the fused kernel: m = 2 keeps all 16 positions in one
+// wave, m = 4 splits the 36 positions over two waves.
+int row_groups(int m) { return m == 2 ? 1 : 2; }
+
 bool valid_cfg(int m, FusedCfg c) {
-    if (c.csplit != 1 && c.csplit != 2 && c.csplit != 4) return false;
-    if (m == 2) return c.ksub == 1 || c.ksub == 2;
-    return c.ksub == 1;
+    if (c.csplit != 1 && c.csplit != 2 && c.csplit != 4 && c.csplit != 8) return false;
+    if (row_groups(m) * c.csplit > 8) return false;
+    return c.bw == 16 || c.bw == 4;
+}
+
+// Workgroups of the fused kernel for a variant: tile blocks x filter groups.
+long fused_workgroups(const Geom& g, FusedCfg c) {
+    const int bh = 16 / c.bw;
+    const long nt = (long)g.N * ((g.th + bh - 1) / bh) * ((g.tw + c.bw - 1) / c.bw);
+    const int kgw = 8 / (row_groups(g.m) * c.csplit);
+    return nt * ((g.KB + kgw - 1) / kgw);
 }
 
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
@@ -69,20 +81,22 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
     const unsigned algo = flags & WINO_ALGO_MASK;
     if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED)
         return WINO_ERR_UNSUPPORTED;
-    const int ks_req = (int)((flags >> kKsubShift) & 0xF);
+    const unsigned blk = flags & kBlockMask;
+    if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
     p->algo = (algo == WINO_ALGO_STAGED) ? WINO_ALGO_STAGED : WINO_ALGO_FUSED;
-    // Fused variant: one wave per (16 tiles x 16*ksub filters) unit; when the
-    // grid has too few units to give every SIMD of the 256 CUs work, split the
-    // channel loop over 2 or 4 waves of a workgroup.
+    // Fused variant.  Tile blocks: a row of 16 tiles when the tile grid is at
+    // least 12 wide, else 4 x 4.  Channel split: the smallest that gives the
+    // 256 CUs a workgroup each (more filter blocks per workgroup share the
+    // staged input patch), else the largest available.
     FusedCfg c;
-    c.ksub = ks_req ? ks_req : 1;
+    c.bw = blk == WINO_BLOCK_1x16 ? 16 : blk == WINO_BLOCK_4x4 ? 4 : (g.tw >= 12 ? 16 : 4);
     if (cs_req) {
         c.csplit = cs_req;
     } else {
-        const long units = (long)g.PB * ((g.KB + c.ksub - 1) / c.ksub);
+        const int max_cs = 8 / row_groups(g.m);
         c.csplit = 1;
-        while (c.csplit < 4 && units * c.csplit < 2048 && g.CQ >= 2 * c.csplit) c.csplit *= 2;
+        while (c.csplit < max_cs && fused_workgroups(g, c) < 240) c.csplit *= 2;
     }
     if (p->algo == WINO_ALGO_FUSED && !valid_cfg(g.m, c)) return WINO_ERR_UNSUPPORTED;
     p->cfg = c;

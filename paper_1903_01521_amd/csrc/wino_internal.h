@@ -19,8 +19,17 @@ struct Geom {
 
 // Kernel variant of the fused algorithm.
 struct FusedCfg {
-    int ksub;       // 16-filter blocks per wave (accumulators: 4*T*ksub per lane)
-    int csplit;     // waves of one workgroup sharing one output unit, splitting C
+    int csplit;     // waves of one workgroup splitting the channel quads of a unit
+    int bw;         // tile-block width: 16 (1 x 16 tiles) or 4 (4 x 4 tiles)
+};
+
+// Runtime part of the fused kernel's work decomposition (host-computed).
+struct FusedTiling {
+    int nbh, nbw;   // tile blocks per image along rows / columns
+    int nt;         // tile blocks in the batch
+    int nkg;        // filter groups (each 16 * 8/(row groups * csplit) filters)
+    int per;        // work items per XCD, ceil(nt * nkg / 8)
+    int nsteps;     // channel steps, ceil(CQ / csplit)
 };
 
 size_t filter_elems(int C, int K, int m);                // T*Cp*Kp

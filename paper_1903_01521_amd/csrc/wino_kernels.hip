@@ -21,6 +21,8 @@
 // for all T positions, and after the channel loop holds the T accumulators of
 // tile l%16 for output channels 4*(l/16) .. 4*(l/16)+3 -- everything the output
 // transform of those four (tile, channel) pairs needs, in its own registers.
+#include <type_traits>
+
 #include "wino_internal.h"
 #include "wino_transforms.h"
 
@@ -114,34 +116,47 @@ __device__ __forceinline__ void load_region(const RegionPlan<MT>& rp, const Geom
     }
 }
 
+// Write output row i (MT values) of the block of (tile tc, output channel k),
+// cropped to Ho x Wo.
+template <int MT>
+__device__ __forceinline__ void store_row(float* __restrict__ y, const Geom& g, const TileCoord& tc, int k,
+                                          int i, const float (&o)[MT], bool relu, bool vec_ok) {
+    const int oi = tc.ti * MT + i, oj0 = tc.tj * MT;
+    if (!tc.valid || k >= g.K || oi >= g.Ho) return;
+    float* row = y + (((size_t)tc.n * g.K + k) * (size_t)g.Ho + oi) * (size_t)g.Wo + oj0;
+    float v[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) v[j] = relu ? fmaxf(o[j], 0.0f) : o[j];
+    if (vec_ok && oj0 + MT <= g.Wo) {
+        if constexpr (MT == 4) {
+            *(float4*)row = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+            *(float2*)row = make_float2(v[0], v[1]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+            if (oj0 + j < g.Wo) row[j] = v[j];
+    }
+}
+
 // Write the m x m output block of (tile tc, output channel k), cropped to Ho x Wo.
 template <int MT>
 __device__ __forceinline__ void store_block(float* __restrict__ y, const Geom& g,
                                             const TileCoord& tc, int k,
                                             const float (&o)[MT][MT], bool relu, bool vec_ok) {
-    if (!tc.valid || k >= g.K) return;
-    const int oi0 = tc.ti * MT, oj0 = tc.tj * MT;
-    float* base = y + ((size_t)tc.n * g.K + k) * (size_t)g.Ho * (size_t)g.Wo;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-        const int oi = oi0 + i;
-        if (oi >= g.Ho) break;
-        float* row = base + (size_t)oi * g.Wo + oj0;
-        float v[MT];
+    for (int i = 0; i < MT; ++i) store_row<MT>(y, g, tc, k, i, o[i], relu, vec_ok);
+}
+
+// Store a lane's T transform-domain values into one (block, quad) group of the
+// U/V layout [T/4][64][4]: one 16-byte store per group of four positions.
+template <int T>
+__device__ __forceinline__ void store_t4(float* __restrict__ blk, int lane, const float (&v)[T]) {
 #pragma unroll
-        for (int j = 0; j < MT; ++j) v[j] = relu ? fmaxf(o[i][j], 0.0f) : o[i][j];
-        if (vec_ok && oj0 + MT <= g.Wo) {
-            if constexpr (MT == 4) {
-                *(float4*)row = make_float4(v[0], v[1], v[2], v[3]);
-            } else {
-                *(float2*)row = make_float2(v[0], v[1]);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < MT; ++j)
-                if (oj0 + j < g.Wo) row[j] = v[j];
-        }
-    }
+    for (int g4 = 0; g4 < T / 4; ++g4)
+        *(float4*)(blk + ((size_t)g4 * 64 + lane) * 4) =
+            make_float4(v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
 }
 
 // ------------------------------------------------------------------ filter
@@ -164,9 +179,7 @@ __global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, fl
         for (int s = 0; s < 3; ++s) gg[r][s] = ok ? src[r * 3 + s] : 0.0f;
     float u[T];
     filter_tf<MT>(gg, u);
-    float* dst = U + ((size_t)w * T) * 64 + lane;
-#pragma unroll
-    for (int t = 0; t < T; ++t) dst[t * 64] = u[t];
+    store_t4<T>(U + (size_t)w * T * 64, lane, u);
 }
 
 // ------------------------------------------------------------------ input
@@ -186,52 +199,63 @@ __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, floa
     load_region<MT>(rp, g, cq, cl, d);
     float v[T];
     input_tf<MT>(d, v);
-    float* dst = V + (((size_t)pb * g.CQ + cq) * T) * 64 + lane;
-#pragma unroll
-    for (int t = 0; t < T; ++t) dst[t * 64] = v[t];
+    store_t4<T>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, v);
 }
 
 // ------------------------------------------------------------------ GEMM
-// Per transform position t: M_t[k][p] = sum_c U_t[c][k] V_t[c][p].
-// Workgroup tile: 4 k-blocks x 4 p-blocks (64 x 64), four waves each 2 x 2
-// blocks of 16 x 16.  Channels advance 16 at a time (4 quads) through a double
-// buffer in LDS; the next chunk is fetched into registers while the current
-// one feeds the MFMAs.
+// M_t[k][p] = sum_c U_t[c][k] V_t[c][p] for each transform position t.
+// Workgroup: 4 positions (one t/4 group) x 4 k-blocks x 4 p-blocks (64 x 64),
+// four waves, each 2 x 2 blocks of 16 x 16 for all 4 positions (16
+// accumulator tiles).  Channels advance 16 at a time (4 quads) through a double
+// buffer in LDS; the next chunk is fetched into registers while the current one
+// feeds the MFMAs.  In LDS a lane's 4 positions are one 16-byte word, so each
+// MFMA operand quadruple is one ds_read_b128.
 __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
                                               float* __restrict__ M, Geom g) {
-    __shared__ float As[2][4][4][64];   // [buf][quad][k-block][lane]
-    __shared__ float Bs[2][4][4][64];   // [buf][quad][p-block][lane]
-    const int t = blockIdx.y;
+    __shared__ float4 As[2][4][4][64];   // [buf][quad][k-block][lane] -> 4 positions
+    __shared__ float4 Bs[2][4][4][64];   // [buf][quad][p-block][lane]
+    const int tg = blockIdx.y;           // positions 4*tg .. 4*tg+3
+    const int T = g.T, TG = g.T / 4;
     const int KB4 = (g.KB + 3) >> 2;
     const int pb0 = (int)(blockIdx.x / KB4) * 4;
     const int kb0 = (int)(blockIdx.x % KB4) * 4;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wk = wave >> 1, wp = wave & 1;
-    const int lblk = tid >> 4, lq = tid & 15, lcq = lblk >> 2, lbi = lblk & 3;
     const int nchunks = (g.CQ + 3) >> 2;
-    const int T = g.T;
 
-    float4 ra, rb;
+    // Loader: each chunk is 16 A blocks + 16 B blocks of 64 float4; thread tid
+    // moves float4 number (tid & 63) of blocks (tid >> 6) + 4*i, i < 4.
+    float4 ra[4], rb[4];
     auto fetch = [&](int chunk) {
-        const int cq = chunk * 4 + lcq;
-        const int kb = kb0 + lbi, pb = pb0 + lbi;
-        ra = make_float4(0.f, 0.f, 0.f, 0.f);
-        rb = ra;
-        if (cq < g.CQ && kb < g.KB)
-            ra = *(const float4*)(U + (((size_t)kb * g.CQ + cq) * T + t) * 64 + lq * 4);
-        if (cq < g.CQ && pb < g.PB)
-            rb = *(const float4*)(V + (((size_t)pb * g.CQ + cq) * T + t) * 64 + lq * 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int blk = (tid >> 6) + 4 * i;          // = quad * 4 + block
+            const int cq = chunk * 4 + (blk >> 2), bi = blk & 3;
+            const int kb = kb0 + bi, pb = pb0 + bi;
+            ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            rb[i] = ra[i];
+            if (cq < g.CQ && kb < g.KB)
+                ra[i] = *(const float4*)(U + ((((size_t)kb * g.CQ + cq) * TG + tg) * 64 + lane) * 4);
+            if (cq < g.CQ && pb < g.PB)
+                rb[i] = *(const float4*)(V + ((((size_t)pb * g.CQ + cq) * TG + tg) * 64 + lane) * 4);
+        }
     };
     auto stage = [&](int buf) {
-        *(float4*)&As[buf][lcq][lbi][lq * 4] = ra;
-        *(float4*)&Bs[buf][lcq][lbi][lq * 4] = rb;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int blk = (tid >> 6) + 4 * i;
+            As[buf][blk >> 2][blk & 3][lane] = ra[i];
+            Bs[buf][blk >> 2][blk & 3][lane] = rb[i];
+        }
     };
 
-    f32x4 acc[2][2];
+    f32x4 acc[4][2][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     fetch(0);
     stage(0);
@@ -241,27 +265,32 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
         if (ch + 1 < nchunks) fetch(ch + 1);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float a0 = As[buf][q][wk * 2 + 0][lane];
-            const float a1 = As[buf][q][wk * 2 + 1][lane];
-            const float b0 = Bs[buf][q][wp * 2 + 0][lane];
-            const float b1 = Bs[buf][q][wp * 2 + 1][lane];
-            acc[0][0] = mfma16x16x4(a0, b0, acc[0][0]);
-            acc[0][1] = mfma16x16x4(a0, b1, acc[0][1]);
-            acc[1][0] = mfma16x16x4(a1, b0, acc[1][0]);
-            acc[1][1] = mfma16x16x4(a1, b1, acc[1][1]);
+            const float4 a0 = As[buf][q][wk * 2 + 0][lane];
+            const float4 a1 = As[buf][q][wk * 2 + 1][lane];
+            const float4 b0 = Bs[buf][q][wp * 2 + 0][lane];
+            const float4 b1 = Bs[buf][q][wp * 2 + 1][lane];
+            const float av[2][4] = {{a0.x, a0.y, a0.z, a0.w}, {a1.x, a1.y, a1.z, a1.w}};
+            const float bv[2][4] = {{b0.x, b0.y, b0.z, b0.w}, {b1.x, b1.y, b1.z, b1.w}};
+#pragma unroll
+            for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) acc[t4][i][j] = mfma16x16x4(av[i][t4], bv[j][t4], acc[t4][i][j]);
         }
         if (ch + 1 < nchunks) stage(buf ^ 1);
         __syncthreads();
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int t4 = 0; t4 < 4; ++t4)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
-            if (kb < g.KB && pb < g.PB)
-                *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + t) * 256 + lane * 4) = acc[i][j];
-        }
-    }
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
+                if (kb < g.KB && pb < g.PB)
+                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
+            }
 }
 
 // ------------------------------------------------------------------ output
@@ -293,134 +322,354 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 }
 
 // ------------------------------------------------------------------ fused
-// Output unit of a wave: 16 tiles (one p-block) x 16*KSUB output channels, all
-// T positions.  CSPLIT waves of a workgroup share one unit and take every
-// CSPLIT-th channel quad; their partial results are output-transformed (the
-// transform is linear) and summed through LDS in wave order 0, 1, ...
-template <int MT, int KSUB, int CSPLIT>
-__global__ __launch_bounds__(256) void k_fused(const float* __restrict__ x, const float* __restrict__ U,
-                                               float* __restrict__ y, Geom g, int relu, int vec_ok) {
-    constexpr int A = MT + 2, T = A * A;
-    constexpr int UNITS = 4 / CSPLIT;            // output units per workgroup
-    constexpr int NB = KSUB * 4;                 // (k-block, slot) output groups per lane
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int cs = wave % CSPLIT;
-    const int uw = wave / CSPLIT;
-    const int KG = (g.KB + KSUB - 1) / KSUB;
-    const long unit = (long)blockIdx.x * UNITS + uw;
-    const bool active = unit < (long)g.PB * KG;
-    const int pb = active ? (int)(unit / KG) : 0;
-    const int kg = active ? (int)(unit % KG) : 0;
+// One workgroup of 8 waves computes one tile block (16 tiles: 1 x 16 or 4 x 4)
+// for KGW 16-filter blocks, over all channels, all T positions, start to end.
+// The 8 waves are (filter block kw) x (row group h of TS) x (channel split cs
+// of CS): wave h owns transform-domain rows [h*A/TS, (h+1)*A/TS), i.e. T/TS
+// accumulators per lane.
+//
+// The channel loop advances QS = KGW*CS = 8/TS quads per step.  Within a step,
+// quad j = kw*CS + cs is input-transformed by wave (kw, h, cs) for its rows --
+// every wave transforms exactly one region set per step -- and each wave then
+// multiplies the KGW quads of its channel split (j = kw'*CS + cs) with its own
+// filter block.  With KGW > 1 the transforms are exchanged through LDS, one
+// step ahead (double-buffered); with KGW = 1 they stay in registers.
+//
+// The halo'd input patch of a step comes straight into LDS (buffer loads with
+// an LDS destination, no register round trip) two steps ahead, in three stages
+// that are distinct LDS objects, so the compiler can see that reading one stage
+// never waits for loads still landing in another.  Rows, columns and channels
+// outside the image and the alignment columns are offsets past the buffer
+// record and read as 0.  Filters go straight to registers, one quad ahead (no
+// other wave uses them), one 16-byte load per 4 positions.  The region's input
+// transform gives exactly the B operand of v_mfma_f32_16x16x4_f32.  At the end
+// each wave applies its share of A^T M A (linear in M) and the TS*CS shares of
+// a filter block are summed through LDS in a fixed binary tree.
+template <int MT, int TS, int CS, int BW>
+struct FusedShape {
+    static constexpr int A = MT + 2, T = A * A, RN = A / TS, TH = RN * A;
+    static constexpr int PARTS = TS * CS, KGW = 8 / PARTS, BH = 16 / BW;
+    static constexpr int QS = KGW * CS;                    // quads per step (= 8 / TS)
+    static constexpr bool SHARE = KGW > 1;                 // transforms exchanged through LDS
+    static constexpr int PR = BH * MT + 2;                 // patch rows
+    static constexpr int PC = BW * MT + 2;                 // patch columns
+    static constexpr int PCP = (PC + 3) / 4 * 4;           // padded: 16-byte aligned rows
+    static constexpr int XS = 4 * QS * PR * PCP;           // patch floats per step
+    static constexpr int JX = (XS + 511) / 512;            // patch loads per thread per step
+    static constexpr int XSP = JX * 512;
+    static constexpr int VSZ = TS * QS * TH * 64;          // floats of one transform stage
+    static constexpr int NV = 4 * MT * MT;                 // output values per lane
+    static constexpr int REDT = (PARTS / 2) * KGW * NV * 64;   // first reduction round
+    static constexpr int VSN = (SHARE ? 2 * VSZ : 0) > REDT ? (SHARE ? 2 * VSZ : 0) : REDT;
+    static_assert(KGW * PARTS == 8, "8 waves per workgroup");
+    static_assert(T % 4 == 0, "positions come in groups of 4");
+    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4 || PARTS == 8, "binary reduction tree");
+};
+
+// s_waitcnt immediate: vmcnt <= n, lgkmcnt = 0, expcnt unconstrained.
+template <int n>
+__device__ __forceinline__ void wait_vm_lds() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (0 << 8) | (((n >> 4) & 3) << 14));
+}
+
+// Workgroup barrier without the release fence of __syncthreads(): that fence
+// would also wait for the direct-to-LDS loads still in flight for later steps.
+// Callers first wait for exactly the loads (vmcnt) and LDS operations
+// (lgkmcnt) the other waves need; the memory clobber keeps the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int R> using IC = std::integral_constant<int, R>;
+
+template <int MT, int TS, int CS, int BW, int H>
+__device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
+                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW>::JX],
+                                            uint32_t step_b, const float* __restrict__ U, const Geom& g,
+                                            const FusedTiling& ft, int kb, int wave, int lane, int kw, int cs,
+                                            int bi, int bj, float* xs0, float* xs1, float* xs2, float* vs,
+                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW>::TH]) {
+    using S = FusedShape<MT, TS, CS, BW>;
+    constexpr int A = S::A, RN = S::RN, X0 = H * RN, TH = S::TH, T = S::T, QS = S::QS, KGW = S::KGW;
+    constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;   // this row group's position groups
     const int cl = lane >> 4;
-    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const int jt = kw * CS + cs;          // the quad this wave transforms in every step
 
-    f32x4 acc[KSUB][T];
+    auto xstage = [&](auto rc) -> float* {
+        constexpr int R = decltype(rc)::value % 3;
+        if constexpr (R == 0) return xs0;
+        else if constexpr (R == 1) return xs1;
+        else return xs2;
+    };
+    // Patch of step j -> stage j % 3 (a step past the last reads zeros into a
+    // stage nobody reads, so every step issues exactly JX loads).
+    auto issue_x = [&](auto rc, int j) {
+        float* xs = xstage(rc);
+        const uint32_t cbase = (uint32_t)j * step_b;
 #pragma unroll
-    for (int s = 0; s < KSUB; ++s)
+        for (int i = 0; i < S::JX; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + i * 512 + wave * 64, 4, xoff[i] + cbase, 0, 0, 0);
+    };
+    // Filters of (step j, quad slot q): a quad past CQ repeats a valid block (it
+    // meets zero regions); past the last step it repeats the last step.
+    const float* ubase = U + ((size_t)kb * g.CQ * (T / 4) + G0) * 256 + lane * 4;
+    auto load_u = [&](int j, int q, f32x4 (&ug)[NG]) {
+        const int cq = min(min(j, ft.nsteps - 1) * QS + q, g.CQ - 1);
+        const float* p = ubase + (size_t)cq * (T / 4) * 256;
 #pragma unroll
-        for (int t = 0; t < T; ++t) acc[s][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Channel quads of this wave: cs, cs + CSPLIT, ...  (nq of them).
-    const int nq = (active && cs < g.CQ) ? (g.CQ - cs + CSPLIT - 1) / CSPLIT : 0;
-    if (nq > 0) {
-        const RegionPlan<MT> rp = make_region_plan<MT>(x, g, pb * 16, tc, cl);
-        // U block of (k-block kb, quad cq) starts at ((kb*CQ + cq)*T)*64.  A k-block
-        // past KB (only the last group when KSUB > 1) re-reads block KB-1; its
-        // results belong to filters >= K and are never stored.
-        const float* ublk[KSUB];
+        for (int i = 0; i < NG; ++i) ug[i] = *(const f32x4*)(p + i * 256);
+    };
+    auto transform = [&](auto rc, float (&v)[TH]) {
+        const float* wp = xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT;
+        float d[A][A];
 #pragma unroll
-        for (int s = 0; s < KSUB; ++s)
-            ublk[s] = U + ((size_t)min(kg * KSUB + s, g.KB - 1) * g.CQ * T) * 64 + lane;
-        // Region values run one quad ahead in two register stages; each quad's
-        // filter values are requested at the top of its step, so their latency
-        // hides behind the input transform.
-        float xa[A][A], xb[A][A];
-        float ur[KSUB][T];
-        auto load_x = [&](int i, float (&xr)[A][A]) { load_region<MT>(rp, g, cs + i * CSPLIT, cl, xr); };
-        auto load_u = [&](int i) {
-            const size_t q = (size_t)(cs + i * CSPLIT) * T * 64;
-#pragma unroll
-            for (int s = 0; s < KSUB; ++s)
-#pragma unroll
-                for (int t = 0; t < T; ++t) ur[s][t] = ublk[s][q + t * 64];
-        };
-        auto compute = [&](float (&xr)[A][A]) {
-            float v[T];
-            input_tf<MT>(xr, v);
-#pragma unroll
-            for (int s = 0; s < KSUB; ++s)
-#pragma unroll
-                for (int t = 0; t < T; ++t) acc[s][t] = mfma16x16x4(ur[s][t], v[t], acc[s][t]);
-        };
-        load_x(0, xa);
-        int i = 0;
-        for (; i + 1 < nq; i += 2) {
-            load_u(i);
-            load_x(i + 1, xb);
-            compute(xa);
-            load_u(i + 1);
-            load_x(min(i + 2, nq - 1), xa);      // past the end: a harmless repeat load
-            compute(xb);
-        }
-        if (i < nq) {
-            load_u(i);
-            compute(xa);
-        }
-    }
-
-    if constexpr (CSPLIT == 1) {
-        if (!active) return;
-#pragma unroll
-        for (int s = 0; s < KSUB; ++s) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float m1[T];
-#pragma unroll
-                for (int t = 0; t < T; ++t) m1[t] = acc[s][t][r];
-                float o[MT][MT];
-                output_tf<MT>(m1, o);
-                store_block<MT>(y, g, tc, (kg * KSUB + s) * 16 + 4 * cl + r, o, relu != 0, vec_ok != 0);
+        for (int u = 0; u < A; ++u) {
+            const float* row = wp + u * S::PCP;
+            if constexpr (MT == 4) {
+                const float4 a4 = *(const float4*)row;
+                const float2 b2 = *(const float2*)(row + 4);
+                d[u][0] = a4.x; d[u][1] = a4.y; d[u][2] = a4.z; d[u][3] = a4.w; d[u][4] = b2.x; d[u][5] = b2.y;
+            } else {
+                const float2 a2 = *(const float2*)row;
+                const float2 b2 = *(const float2*)(row + 2);
+                d[u][0] = a2.x; d[u][1] = a2.y; d[u][2] = b2.x; d[u][3] = b2.y;
             }
         }
+        input_tf_rows<MT, X0, RN>(d, v);
+    };
+    auto mfma_quad = [&](const float (&v)[TH], const f32x4 (&ug)[NG]) {
+#pragma unroll
+        for (int t = 0; t < TH; ++t) {
+            const int idx = X0 * A + t;
+            acc[t] = mfma16x16x4(ug[idx / 4 - G0][idx % 4], v[t], acc[t]);
+        }
+    };
+
+    f32x4 ua[NG], ub[NG];
+    if constexpr (!S::SHARE) {
+        // Step s: transform quad cs of step s (patch landed two steps ago), one
+        // quad of MFMAs; filters one step ahead.
+        constexpr int WAITN = S::JX + NG;     // loads issued in the previous step
+        issue_x(IC<0>{}, 0);
+        issue_x(IC<1>{}, 1);
+        load_u(0, cs, ua);
+        auto step = [&](auto rc, int s) {  // s % 3 == R
+            constexpr int R = decltype(rc)::value;
+            wait_vm_lds<WAITN>();          // patch of step s has landed (for this wave)
+            wg_barrier();                  // ... for every wave; step s-1 is fully consumed
+            issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
+            load_u(s + 1, cs, ub);
+            __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's work
+            float v[TH];
+            transform(IC<R>{}, v);
+            mfma_quad(v, ua);
+#pragma unroll
+            for (int i = 0; i < NG; ++i) ua[i] = ub[i];
+        };
+        int s = 0;
+        for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
+            step(IC<0>{}, s);
+            step(IC<1>{}, s + 1);
+            step(IC<2>{}, s + 2);
+        }
+        if (s < ft.nsteps) step(IC<0>{}, s);
+        if (s + 1 < ft.nsteps) step(IC<1>{}, s + 1);
     } else {
-        static_assert(NB % CSPLIT == 0, "each wave must own whole output groups");
-        __shared__ float red[UNITS][CSPLIT][NB][MT * MT][64];
+        // Step s: transform quad jt of step s+1 into V stage (s+1)&1, then for
+        // each filter-block slot kw' the MFMAs of quad kw'*CS + cs of step s from
+        // V stage s&1.  V stage (j&1) holds [(h*QS + quad)][t][64].
+        constexpr int WAITN = S::JX + KGW * NG;    // loads issued in the previous step
+        float* vbase = vs + (H * QS) * TH * 64 + lane;
+        auto put_v = [&](int j, const float (&v)[TH]) {
+            float* p = vbase + (j & 1) * S::VSZ + jt * TH * 64;
 #pragma unroll
-        for (int s = 0; s < KSUB; ++s) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float m1[T];
-#pragma unroll
-                for (int t = 0; t < T; ++t) m1[t] = acc[s][t][r];
-                float o[MT][MT];
-                output_tf<MT>(m1, o);
-#pragma unroll
-                for (int i = 0; i < MT; ++i)
-#pragma unroll
-                    for (int j = 0; j < MT; ++j) red[uw][cs][s * 4 + r][i * MT + j][lane] = o[i][j];
-            }
+            for (int t = 0; t < TH; ++t) p[t * 64] = v[t];
+        };
+        issue_x(IC<0>{}, 0);
+        issue_x(IC<1>{}, 1);
+        issue_x(IC<2>{}, 2);
+        load_u(0, cs, ua);
+        wait_vm_lds<2 * S::JX + NG>();       // step 0's patch has landed
+        wg_barrier();
+        {
+            float v[TH];
+            transform(IC<0>{}, v);
+            put_v(0, v);
         }
-        __syncthreads();
-        if (!active) return;
-        constexpr int PER = NB / CSPLIT;
+        auto step = [&](auto rc, int s) {  // s % 3 == R
+            constexpr int R = decltype(rc)::value;
+            wait_vm_lds<WAITN>();          // step s+1's patch has landed; V(s) written
+            wg_barrier();                  // ... by everyone; step s-1 is fully consumed
+            issue_x(IC<R>{}, s + 3);       // stage R held step s's patch, transformed at step s-1
+            if (s + 1 < ft.nsteps) {
+                float v[TH];
+                transform(IC<(R + 1) % 3>{}, v);
+                put_v(s + 1, v);
+            }
+            // Quad slots k2 = 0 .. KGW-1: the V values and filters of slot k2+1
+            // are requested before slot k2's MFMAs (scheduling barriers keep the
+            // compiler from sinking them back next to their uses).
+            const float* vp = vbase + (s & 1) * S::VSZ + cs * TH * 64;
+            float va[TH], vb[TH];
 #pragma unroll
-        for (int b = 0; b < PER; ++b) {
-            const int grp = cs * PER + b;        // (k-block s, slot r) = (grp / 4, grp % 4)
-            float o[MT][MT];
+            for (int t = 0; t < TH; ++t) va[t] = vp[t * 64];
 #pragma unroll
-            for (int i = 0; i < MT; ++i)
+            for (int k2 = 0; k2 < KGW; ++k2) {
+                f32x4 (&ucur)[NG] = (k2 & 1) ? ub : ua;
+                f32x4 (&unext)[NG] = (k2 & 1) ? ua : ub;
+                float (&vcur)[TH] = (k2 & 1) ? vb : va;
+                float (&vnext)[TH] = (k2 & 1) ? va : vb;
+                if (k2 + 1 < KGW) {
+                    load_u(s, (k2 + 1) * CS + cs, unext);
+                    const float* p = vp + (k2 + 1) * CS * TH * 64;
 #pragma unroll
-                for (int j = 0; j < MT; ++j) {
-                    float sum = red[uw][0][grp][i * MT + j][lane];
-#pragma unroll
-                    for (int q = 1; q < CSPLIT; ++q) sum += red[uw][q][grp][i * MT + j][lane];
-                    o[i][j] = sum;
+                    for (int t = 0; t < TH; ++t) vnext[t] = p[t * 64];
+                } else {
+                    load_u(s + 1, cs, unext);
                 }
-            store_block<MT>(y, g, tc, (kg * KSUB + grp / 4) * 16 + 4 * cl + (grp % 4), o,
-                            relu != 0, vec_ok != 0);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_quad(vcur, ucur);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (KGW & 1) {       // keep "ua holds the current filters" at step starts
+#pragma unroll
+                for (int i = 0; i < NG; ++i) ua[i] = ub[i];
+            }
+        };
+        int s = 0;
+        for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
+            step(IC<0>{}, s);
+            step(IC<1>{}, s + 1);
+            step(IC<2>{}, s + 2);
+        }
+        if (s < ft.nsteps) step(IC<0>{}, s);
+        if (s + 1 < ft.nsteps) step(IC<1>{}, s + 1);
+    }
+    __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
+}
+
+// o[r] = this wave's share of the m x m output of (tile, filter 16*kb + 4*cl + r)
+template <int MT, int TS, int CS, int BW, int H>
+__device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS, CS, BW>::TH],
+                                            float (&o)[4][MT][MT]) {
+    using S = FusedShape<MT, TS, CS, BW>;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float m1[S::TH];
+#pragma unroll
+        for (int t = 0; t < S::TH; ++t) m1[t] = acc[t][r];
+        output_tf_rows<MT, H * S::RN, S::RN>(m1, o[r]);
+    }
+}
+
+template <int MT, int TS, int CS, int BW>
+__global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, const float* __restrict__ U,
+                                               float* __restrict__ y, Geom g, FusedTiling ft, int relu,
+                                               int vec_ok) {
+    using S = FusedShape<MT, TS, CS, BW>;
+    constexpr int PARTS = S::PARTS, KGW = S::KGW, NV = S::NV;
+    __shared__ float4 xs0[S::XSP / 4], xs1[S::XSP / 4], xs2[S::XSP / 4];   // patch stages
+    __shared__ float4 vs[S::VSN / 4 > 0 ? S::VSN / 4 : 1];                 // transforms, then reduction
+
+    // Work item, XCD-aware: workgroups go round-robin to the 8 XCDs, so XCD
+    // (b % 8) gets the contiguous run [xcd*per, (xcd+1)*per) of the filter-group-
+    // major order; its L2 then holds the filters of one or two groups.
+    const int b = blockIdx.x;
+    const int item = (b & 7) * ft.per + (b >> 3);
+    if (item >= ft.nt * ft.nkg) return;
+    const int kgi = item / ft.nt, tb = item - kgi * ft.nt;
+    const int per_img = ft.nbh * ft.nbw;
+    const int n = tb / per_img, r2 = tb - n * per_img;
+    const int ti0 = (r2 / ft.nbw) * S::BH, tj0 = (r2 % ft.nbw) * BW;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kw = wave / PARTS, part = wave % PARTS, h = part % TS, cs = part / TS;
+    const int kb = min(kgi * KGW + kw, g.KB - 1);    // a block past KB only re-reads KB-1; never stored
+    const int l16 = lane & 15, bi = l16 / BW, bj = l16 % BW, cl = lane >> 4;
+    TileCoord tc;
+    tc.n = n;
+    tc.ti = ti0 + bi;
+    tc.tj = tj0 + bj;
+    tc.valid = tc.ti < g.th && tc.tj < g.tw;
+
+    // Patch element e = j*512 + tid of [4*QS channels][PR][PCP]: its byte offset
+    // in image n for step 0 (kInvalid outside the image or past the row).
+    const size_t img = (size_t)g.C * g.H * g.W;
+    const size_t img_b = img * 4;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + (size_t)n * img), (short)0, (int)(img_b < kInvalid ? img_b : kInvalid), kRsrcWord3);
+    const uint32_t plane_b = (uint32_t)g.H * g.W * 4;
+    uint32_t xoff[S::JX];
+#pragma unroll
+    for (int j = 0; j < S::JX; ++j) {
+        const int e = j * 512 + tid;
+        const int ch = e / (S::PR * S::PCP), rem = e % (S::PR * S::PCP);
+        const int r = rem / S::PCP, c = rem % S::PCP;
+        const int row = ti0 * MT - g.pad + r, col = tj0 * MT - g.pad + c;
+        const bool ok = e < S::XS && c < S::PC && row >= 0 && row < g.H && col >= 0 && col < g.W;
+        xoff[j] = ok ? (uint32_t)ch * plane_b + ((uint32_t)row * g.W + col) * 4 : kInvalid;
+    }
+    const uint32_t step_b = 4u * S::QS * plane_b;
+
+    f32x4 acc[S::TH];
+#pragma unroll
+    for (int t = 0; t < S::TH; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float o[4][MT][MT];
+    float* xs0f = (float*)xs0;
+    float* xs1f = (float*)xs1;
+    float* xs2f = (float*)xs2;
+    float* vsf = (float*)vs;
+    if constexpr (TS == 1) {
+        fused_steps<MT, TS, CS, BW, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
+                                       xs2f, vsf, acc);
+        fused_share<MT, TS, CS, BW, 0>(acc, o);
+    } else {
+        if (h == 0) {
+            fused_steps<MT, TS, CS, BW, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
+                                           xs1f, xs2f, vsf, acc);
+            fused_share<MT, TS, CS, BW, 0>(acc, o);
+        } else {
+            fused_steps<MT, TS, CS, BW, 1>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
+                                           xs1f, xs2f, vsf, acc);
+            fused_share<MT, TS, CS, BW, 1>(acc, o);
         }
     }
+
+    const int kbase = (kgi * KGW + kw) * 16 + 4 * cl;   // filters of this lane's slots r = 0..3
+    if constexpr (PARTS > 1) {
+        // Binary tree over the parts of each filter block: in the round with
+        // stride half, part p in [half, 2*half) publishes its share and part
+        // p - half adds it.  Slot layout red[kw][p - half][v][lane],
+        // v = (r*MT + i)*MT + j.
+        float* red = vsf;
+#pragma unroll
+        for (int half = PARTS / 2; half >= 1; half /= 2) {
+            __syncthreads();
+            if (part >= half && part < 2 * half) {
+                float* slot = red + ((size_t)(kw * (PARTS / 2) + part - half) * NV) * 64 + lane;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < MT; ++j) slot[((r * MT + i) * MT + j) * 64] = o[r][i][j];
+            }
+            __syncthreads();
+            if (part < half) {
+                const float* slot = red + ((size_t)(kw * (PARTS / 2) + part) * NV) * 64 + lane;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < MT; ++j) o[r][i][j] += slot[((r * MT + i) * MT + j) * 64];
+            }
+        }
+        if (part != 0) return;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[r], relu != 0, vec_ok != 0);
 }
 
 // ------------------------------------------------------------------ maxpool
@@ -463,7 +712,7 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
 
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s) {
     const long tiles = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4);
-    const dim3 grid((unsigned)tiles, (unsigned)g.T), block(256);
+    const dim3 grid((unsigned)tiles, (unsigned)(g.T / 4)), block(256);
     hipLaunchKernelGGL(k_gemm, grid, block, 0, s, U, V, M, g);
     return hipGetLastError();
 }
@@ -479,31 +728,42 @@ hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool
     return hipGetLastError();
 }
 
-template <int MT, int KSUB, int CSPLIT>
+template <int MT, int TS, int CS, int BW>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
                                  hipStream_t s) {
-    const int KG = (g.KB + KSUB - 1) / KSUB;
-    const long units = (long)g.PB * KG;
-    constexpr int UNITS = 4 / CSPLIT;
-    const dim3 grid((unsigned)((units + UNITS - 1) / UNITS)), block(256);
+    using S = FusedShape<MT, TS, CS, BW>;
+    FusedTiling ft;
+    ft.nbh = (g.th + S::BH - 1) / S::BH;
+    ft.nbw = (g.tw + BW - 1) / BW;
+    ft.nt = g.N * ft.nbh * ft.nbw;
+    ft.nkg = (g.KB + S::KGW - 1) / S::KGW;
+    ft.per = (int)(((long)ft.nt * ft.nkg + 7) / 8);
+    ft.nsteps = (g.CQ + S::QS - 1) / S::QS;
+    const dim3 grid((unsigned)(8 * ft.per)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
-    hipLaunchKernelGGL((k_fused<MT, KSUB, CSPLIT>), grid, block, 0, s, x, U, y, g, (int)relu, vec_ok);
+    hipLaunchKernelGGL((k_fused<MT, TS, CS, BW>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok);
     return hipGetLastError();
 }
 
 hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg c, bool relu,
                         hipStream_t s) {
-#define WINO_FUSED_CASE(MT, KS, CS) \
-    if (g.m == MT && c.ksub == KS && c.csplit == CS) return fused_instance<MT, KS, CS>(x, U, y, g, relu, s);
-    WINO_FUSED_CASE(2, 1, 1)
-    WINO_FUSED_CASE(2, 1, 2)
-    WINO_FUSED_CASE(2, 1, 4)
-    WINO_FUSED_CASE(2, 2, 1)
-    WINO_FUSED_CASE(2, 2, 2)
-    WINO_FUSED_CASE(2, 2, 4)
-    WINO_FUSED_CASE(4, 1, 1)
-    WINO_FUSED_CASE(4, 1, 2)
-    WINO_FUSED_CASE(4, 1, 4)
+    // m = 2: all 16 positions per wave; m = 4: two row groups of 18 positions.
+#define WINO_FUSED_CASE(MT, TS, CS, BW) \
+    if (g.m == MT && c.csplit == CS && c.bw == BW) return fused_instance<MT, TS, CS, BW>(x, U, y, g, relu, s);
+    WINO_FUSED_CASE(2, 1, 1, 16)
+    WINO_FUSED_CASE(2, 1, 2, 16)
+    WINO_FUSED_CASE(2, 1, 4, 16)
+    WINO_FUSED_CASE(2, 1, 8, 16)
+    WINO_FUSED_CASE(2, 1, 1, 4)
+    WINO_FUSED_CASE(2, 1, 2, 4)
+    WINO_FUSED_CASE(2, 1, 4, 4)
+    WINO_FUSED_CASE(2, 1, 8, 4)
+    WINO_FUSED_CASE(4, 2, 1, 16)
+    WINO_FUSED_CASE(4, 2, 2, 16)
+    WINO_FUSED_CASE(4, 2, 4, 16)
+    WINO_FUSED_CASE(4, 2, 1, 4)
+    WINO_FUSED_CASE(4, 2, 2, 4)
+    WINO_FUSED_CASE(4, 2, 4, 4)
 #undef WINO_FUSED_CASE
     return hipErrorInvalidValue;
 }

@@ -114,6 +114,97 @@ __device__ __forceinline__ void output_tf(const float (&mv)[(MT + 2) * (MT + 2)]
     }
 }
 
+// ---------------------------------------------------------------- row subsets
+// A wave that owns only transform-domain rows X0 .. X0+RN-1 needs only those
+// rows of B^T d B, and its share of A^T M A (the output transform is linear in
+// M, so the shares of all row groups add up to the full result).
+
+// v[(xi - X0)*A + nu] = (B^T d B)[xi][nu] for xi in [X0, X0+RN).  The first pass
+// evaluates the full 1-D transform per column; unused rows are dead code.
+template <int MT, int X0, int RN>
+__device__ __forceinline__ void input_tf_rows(const float (&d)[MT + 2][MT + 2], float (&v)[RN * (MT + 2)]) {
+    constexpr int A = MT + 2;
+    float s[RN][A];
+#pragma unroll
+    for (int j = 0; j < A; ++j) {
+        float col[A], r[A];
+#pragma unroll
+        for (int i = 0; i < A; ++i) col[i] = d[i][j];
+        bt_1d(col, r);
+#pragma unroll
+        for (int i = 0; i < RN; ++i) s[i][j] = r[X0 + i];
+    }
+#pragma unroll
+    for (int i = 0; i < RN; ++i) {
+        float r[A];
+        bt_1d(s[i], r);
+#pragma unroll
+        for (int j = 0; j < A; ++j) v[i * A + j] = r[j];
+    }
+}
+
+// r[i] = sum over xi in [X0, X0+RN) of A^T[i][xi] * a[xi - X0]
+template <int MT, int X0, int RN> struct AtRows;
+template <> struct AtRows<2, 0, 4> {
+    __device__ static void f(const float (&a)[4], float (&r)[2]) { at_1d(a, r); }
+};
+template <> struct AtRows<4, 0, 6> {
+    __device__ static void f(const float (&a)[6], float (&r)[4]) { at_1d(a, r); }
+};
+template <> struct AtRows<2, 0, 2> {            // rows 0, 1 of A^T = [1 1 1 0; 0 1 -1 -1]
+    __device__ static void f(const float (&a)[2], float (&r)[2]) {
+        r[0] = a[0] + a[1];
+        r[1] = a[1];
+    }
+};
+template <> struct AtRows<2, 2, 2> {            // rows 2, 3
+    __device__ static void f(const float (&a)[2], float (&r)[2]) {
+        r[0] = a[0];
+        r[1] = -a[0] - a[1];
+    }
+};
+template <> struct AtRows<4, 0, 3> {            // rows 0, 1, 2 of the m = 4 A^T
+    __device__ static void f(const float (&a)[3], float (&r)[4]) {
+        const float s12 = a[1] + a[2], d12 = a[1] - a[2];
+        r[0] = a[0] + s12;
+        r[1] = d12;
+        r[2] = s12;
+        r[3] = d12;
+    }
+};
+template <> struct AtRows<4, 3, 3> {            // rows 3, 4, 5
+    __device__ static void f(const float (&a)[3], float (&r)[4]) {
+        const float s34 = a[0] + a[1], d34 = a[0] - a[1];
+        r[0] = s34;
+        r[1] = 2.0f * d34;
+        r[2] = 4.0f * s34;
+        r[3] = __builtin_fmaf(8.0f, d34, a[2]);
+    }
+};
+
+// o = A^T M' A where M' keeps rows [X0, X0+RN) of M (mv holds just those rows).
+template <int MT, int X0, int RN>
+__device__ __forceinline__ void output_tf_rows(const float (&mv)[RN * (MT + 2)], float (&o)[MT][MT]) {
+    constexpr int A = MT + 2;
+    float s[MT][A];
+#pragma unroll
+    for (int j = 0; j < A; ++j) {
+        float col[RN], r[MT];
+#pragma unroll
+        for (int i = 0; i < RN; ++i) col[i] = mv[i * A + j];
+        AtRows<MT, X0, RN>::f(col, r);
+#pragma unroll
+        for (int i = 0; i < MT; ++i) s[i][j] = r[i];
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+        float r[MT];
+        at_1d(s[i], r);
+#pragma unroll
+        for (int j = 0; j < MT; ++j) o[i][j] = r[j];
+    }
+}
+
 // ---------------------------------------------------------------- filter, fp64
 // U = G g G^T evaluated in fp64 with an integer-scaled G (S*G has integer
 // entries: S = 2 for m = 2, S = 24 for m = 4): the two small-integer products

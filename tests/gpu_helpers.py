@@ -77,20 +77,20 @@ def _pad_counts(C, K, P):
 
 
 def unpack_U(U: np.ndarray, C: int, K: int, m: int, crop=True) -> np.ndarray:
-    """U[KB][CQ][T][64] (lane = (c%4)*16 + k%16) -> logical [T][C][K]."""
+    """U[KB][CQ][T/4][64][4] (lane = (c%4)*16 + k%16, slot t%4) -> logical [T][C][K]."""
     T = (m + 2) ** 2
     CQ, KB, _ = _pad_counts(C, K, 1)
-    a = U[:KB * CQ * T * 64].reshape(KB, CQ, T, 4, 16)           # kb, cq, t, cl, kl
-    a = a.transpose(2, 1, 3, 0, 4).reshape(T, CQ * 4, KB * 16)   # t, c, k
+    a = U[:KB * CQ * T * 64].reshape(KB, CQ, T // 4, 4, 16, 4)           # kb, cq, tg, cl, kl, tt
+    a = a.transpose(2, 5, 1, 3, 0, 4).reshape(T, CQ * 4, KB * 16)        # t, c, k
     return a[:, :C, :K] if crop else a
 
 
 def unpack_V(V: np.ndarray, C: int, P: int, m: int, crop=True) -> np.ndarray:
-    """V[PB][CQ][T][64] (lane = (c%4)*16 + p%16) -> logical [T][C][P]."""
+    """V[PB][CQ][T/4][64][4] (lane = (c%4)*16 + p%16, slot t%4) -> logical [T][C][P]."""
     T = (m + 2) ** 2
     CQ, _, PB = _pad_counts(C, 1, P)
-    a = V[:PB * CQ * T * 64].reshape(PB, CQ, T, 4, 16)           # pb, cq, t, cl, pl
-    a = a.transpose(2, 1, 3, 0, 4).reshape(T, CQ * 4, PB * 16)   # t, c, p
+    a = V[:PB * CQ * T * 64].reshape(PB, CQ, T // 4, 4, 16, 4)           # pb, cq, tg, cl, pl, tt
+    a = a.transpose(2, 5, 1, 3, 0, 4).reshape(T, CQ * 4, PB * 16)        # t, c, p
     return a[:, :C, :P] if crop else a
 
 

@@ -77,7 +77,8 @@ def _conv(x=FAKE, U=FAKE, y=FAKE + 0x100000, flags=0, ws=None, wsb=0, **kw):
     (dict(flags=0x80000000), B.WINO_ERR_UNSUPPORTED),        # unknown flag bit
     (dict(flags=0x300), B.WINO_ERR_UNSUPPORTED),             # unknown algorithm
     (dict(flags=B.WINO_ALGO_FUSED | B.WINO_CSPLIT(3)), B.WINO_ERR_UNSUPPORTED),
-    (dict(flags=B.WINO_ALGO_FUSED | B.WINO_KSUB(2)), B.WINO_ERR_UNSUPPORTED),   # m=4
+    (dict(flags=B.WINO_ALGO_FUSED | B.WINO_CSPLIT(8)), B.WINO_ERR_UNSUPPORTED),  # m=4: 2 x 8 > 8 waves
+    (dict(flags=B.WINO_BLOCK_1x16 | B.WINO_BLOCK_4x4), B.WINO_ERR_UNSUPPORTED),  # two block shapes
     (dict(flags=B.WINO_ALGO_STAGED), B.WINO_ERR_WORKSPACE),  # no workspace
     (dict(flags=B.WINO_ALGO_STAGED, ws=FAKE + 0x900000, wsb=16), B.WINO_ERR_WORKSPACE),
     (dict(y=FAKE), B.WINO_ERR_INVALID_ARG),                  # y aliases x

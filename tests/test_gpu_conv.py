@@ -18,13 +18,12 @@ ELEM = {2: 2e-5, 4: 2e-4}
 
 F = B.WINO_ALGO_FUSED
 VARIANTS = {
-    2: [("auto", 0), ("staged", B.WINO_ALGO_STAGED),
-        ("f_k1c1", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(1)), ("f_k1c2", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(2)),
-        ("f_k1c4", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(4)), ("f_k2c1", F | B.WINO_KSUB(2) | B.WINO_CSPLIT(1)),
-        ("f_k2c2", F | B.WINO_KSUB(2) | B.WINO_CSPLIT(2)), ("f_k2c4", F | B.WINO_KSUB(2) | B.WINO_CSPLIT(4))],
-    4: [("auto", 0), ("staged", B.WINO_ALGO_STAGED),
-        ("f_k1c1", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(1)), ("f_k1c2", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(2)),
-        ("f_k1c4", F | B.WINO_KSUB(1) | B.WINO_CSPLIT(4))],
+    2: [("auto", 0), ("staged", B.WINO_ALGO_STAGED)]
+       + [(f"f_b{bn}c{c}", F | bf | B.WINO_CSPLIT(c))
+          for bn, bf in (("16", B.WINO_BLOCK_1x16), ("4x4", B.WINO_BLOCK_4x4)) for c in (1, 2, 4, 8)],
+    4: [("auto", 0), ("staged", B.WINO_ALGO_STAGED)]
+       + [(f"f_b{bn}c{c}", F | bf | B.WINO_CSPLIT(c))
+          for bn, bf in (("16", B.WINO_BLOCK_1x16), ("4x4", B.WINO_BLOCK_4x4)) for c in (1, 2, 4)],
 }
 
 # (N, C, H, W, K, pad): the worked example's shape (3x6x6 input, 4 filters, valid
