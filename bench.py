@@ -6,15 +6,31 @@ the convolution (input transform -> T GEMMs -> output transform) of every 3x3
 layer in the workload (plus the 2x2 pools of a stack).  Prints one JSON line.
 
 Metric: effective GFLOP/s = direct-convolution FLOPs (2*N*K*C*9*Ho*Wo per layer)
-divided by the step time.  Also reported: the roofline position of the
-dominant kernel (its average duration from HIP events on the launch stream), and
-the fp64 CPU oracle timed on this host on a bounded sample.
+divided by the step time, with eager launches (``--graph`` replays a HIP graph
+of 10 steps instead; the eager and the other figure are both reported).  Also
+reported:
+
+* ``roofline``: the dominant kernel's algorithmic bytes (or FLOPs) per launch
+  over its average launch duration, timed with HIP events around a graph of
+  back-to-back launches of that kernel on its own stream; ``traffic`` is the HBM
+  bytes per launch that rocprofv3's FETCH_SIZE / WRITE_SIZE counters measured
+  for it (scaled by what they read for a plain device copy of known size), read
+  from the committed counter summary under profiles/ -- or null when that
+  summary was taken on other kernel sources than the ones built here.
+* ``cpu_baseline``: the fp64 CPU oracle on this host's cores, on a bounded
+  sample of the same workload.
+
+``--pmc-summary FETCH_DIR WRITE_DIR`` turns two rocprofv3 --pmc runs of this
+script (one with FETCH_SIZE, one with WRITE_SIZE, csv output) into that
+committed summary.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
-import math
 import os
 import sys
 import time
@@ -23,10 +39,29 @@ import numpy as np
 
 HBM_PEAK = 8.0e12          # B/s, MI355X HBM3E
 FP32_MFMA_PEAK = 157.3e12  # FLOP/s, MI355X dense fp32 matrix
+COPY_BYTES = 64 << 20      # size of the plain copy that calibrates the byte counters
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "paper_1903_01521_amd", "csrc")
+PROFILES = os.path.join(HERE, "profiles")
+
+# Kernel-name prefixes as rocprofv3 reports them, per kind of launch.
+KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused",
+                "input": "void wino::k_input", "gemm": "void wino::k_gemm",
+                "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2"}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def sources_hash() -> str:
+    """sha256 over the HIP sources and host planner that define the kernels and launches."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(CSRC, "*"))):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(os.path.basename(f).encode())
+            h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def layer_numbers(N, L):
@@ -35,13 +70,12 @@ def layer_numbers(N, L):
     th, tw = -(-Ho // L.m), -(-Wo // L.m)
     P = N * th * tw
     T = (L.m + 2) ** 2
-    Cp, Kp = -(-L.C // 4) * 4, -(-L.K // 16) * 16
     f = dict(Ho=Ho, Wo=Wo, P=P, T=T)
     f["direct_flops"] = 2 * N * L.K * L.C * 9 * Ho * Wo
     f["gemm_flops"] = 2 * T * P * L.C * L.K
-    x_b, y_b, u_b = 4 * N * L.C * L.H * L.W, 4 * N * L.K * Ho * Wo, 4 * T * Cp * Kp
+    x_b, y_b, u_b = 4 * N * L.C * L.H * L.W, 4 * N * L.K * Ho * Wo, 4 * T * L.C * L.K
     v_b, m_b = 4 * T * P * L.C, 4 * T * P * L.K
-    # minimum HBM bytes per kernel (what the method must move, padding excluded)
+    # minimum HBM bytes per kernel launch (what the method must move, padding excluded)
     f["bytes"] = {
         "filter": 4 * L.K * L.C * 9 + u_b,
         "fused": x_b + u_b + y_b,
@@ -62,24 +96,133 @@ def roofline(kind, nums, seconds):
     if t_mfma >= t_hbm and fl > 0:
         ach = fl / seconds / 1e12
         return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK / 1e12,
-                "unit": "TFLOP/s", "frac": round(ach / (FP32_MFMA_PEAK / 1e12), 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(ach / (FP32_MFMA_PEAK / 1e12), 4), "traffic": None,
+                "algorithmic_flops": fl, "algorithmic_bytes": b}
     ach = b / seconds / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-            "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None}
+            "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None,
+            "algorithmic_flops": fl, "algorithmic_bytes": b}
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(PROFILES, f"traffic_{workload}.txt")
+
+
+def read_traffic(workload: str, kind: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary, or None if there is none or it was taken on other sources."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("sources_sha256") != sources_hash():
+        return None, "kernel sources changed since the counters were taken"
+    if kv.get("kind") != kind:
+        return None, f"counter summary covers {kv.get('kind')}, not {kind}"
+    return int(float(kv["traffic_bytes_per_launch"])), path
+
+
+def pmc_rows(d: str):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        rows.extend(csv.DictReader(open(f)))
+    return rows
+
+
+def pmc_summary(args):
+    """Summarise a FETCH_SIZE run and a WRITE_SIZE run of this script."""
+    from paper_1903_01521_amd import workloads as wl
+    name = args.workload or wl.DEFAULT_BENCH
+    w = wl.WORKLOADS[name]
+    nums = [layer_numbers(w.N, L) for L in w.layers]
+    kind = args.kind
+    prefix = KERNEL_NAMES[kind]
+    out = {}
+    for counter, d in (("FETCH_SIZE", args.pmc_summary[0]), ("WRITE_SIZE", args.pmc_summary[1])):
+        rows = [r for r in pmc_rows(d) if r["Counter_Name"] == counter]
+        # the calibration launches: torch's elementwise negation over COPY_BYTES
+        kern = [float(r["Counter_Value"]) for r in rows if r["Kernel_Name"].startswith(prefix)]
+        copy = [float(r["Counter_Value"]) for r in rows
+                if "neg" in r["Kernel_Name"].lower() and int(r["Grid_Size"]) * 16 >= COPY_BYTES // 4]
+        if not kern or not copy:
+            raise SystemExit(f"{counter}: {len(kern)} {kind} dispatches, {len(copy)} copy dispatches in {d}")
+        out[counter] = (float(np.mean(kern)), len(kern), float(np.median(copy)), len(copy),
+                        sorted(set(r["Kernel_Name"] for r in rows if r["Kernel_Name"].startswith(prefix))))
+    fk, fn_, fc, fcn, names = out["FETCH_SIZE"]
+    wk, wn, wc, wcn, _ = out["WRITE_SIZE"]
+    fscale = fc * 1024 / COPY_BYTES
+    wscale = wc * 1024 / COPY_BYTES
+    traffic = fk * 1024 / fscale + wk * 1024 / wscale
+    alg = sum(f["bytes"][kind] for f in nums) / len(nums)
+    lines = [
+        f"# HBM traffic per launch of the {kind} kernel on workload {name}",
+        "# from two rocprofv3 PMC runs of bench.py on one MI355X (commands below), each",
+        f"# counter scaled by what it reads for a plain streaming kernel over {COPY_BYTES} bytes.",
+        "#   cd /tmp && export TMPDIR=/tmp",
+        f"#   timeout -s KILL 60 rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/fetch -o run -- "
+        f"python3 <repo>/bench.py --workload {name} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
+        f"#   timeout -s KILL 60 rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/write -o run -- "
+        f"python3 <repo>/bench.py --workload {name} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
+        f"#   python3 bench.py --workload {name} --kind {kind} --pmc-summary <out>/fetch <out>/write",
+        f"workload: {name}",
+        f"kind: {kind}",
+        f"kernels: {' | '.join(names)}",
+        f"sources_sha256: {sources_hash()}",
+        f"dispatches_fetch: {fn_}",
+        f"dispatches_write: {wn}",
+        f"fetch_kib_per_dispatch: {fk:.1f}",
+        f"write_kib_per_dispatch: {wk:.1f}",
+        f"copy_bytes: {COPY_BYTES}",
+        f"copy_fetch_kib: {fc:.1f} (median of {fcn})",
+        f"copy_write_kib: {wc:.1f} (median of {wcn})",
+        f"fetch_scale: {fscale:.4f}",
+        f"write_scale: {wscale:.4f}",
+        f"traffic_bytes_per_launch: {traffic:.0f}",
+        f"algorithmic_bytes_per_launch: {alg:.0f}",
+        f"traffic_over_algorithmic: {traffic / alg:.3f}",
+    ]
+    text = "\n".join(lines) + "\n"
+    if args.write_summary:
+        with open(traffic_file(name), "w") as fh:
+            fh.write(text)
+    print(text, end="")
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--algo", choices=["auto", "fused", "staged"], default="auto")
     ap.add_argument("--flags", type=lambda s: int(s, 0), default=None,
                     help="explicit wino_conv2d flags (overrides --algo)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of a HIP graph holding 10 steps (K a multiple of 10) "
+                         "instead of eager launches")
+    ap.add_argument("--eager", action="store_true", help="eager launches (the default)")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="capture no HIP graph at all (per-kernel timing from eager launches); "
+                         "for counter-collection runs")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU time budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc csv runs (no GPU needed)")
+    ap.add_argument("--kind", default="fused", help="kernel kind the --pmc-summary covers")
+    ap.add_argument("--write-summary", action="store_true",
+                    help="with --pmc-summary: also write it to profiles/traffic_<workload>.txt")
     args = ap.parse_args()
+
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -129,47 +272,68 @@ def main():
         else:
             pools.append(None)
 
-    stream = torch.cuda.current_stream()
-    sp = stream.cuda_stream
-
     def launches():
-        """The step as a list of (label, layer index, kind, thunk)."""
+        """The step as a list of (label, layer index, kind, fn(stream))."""
         out = []
         a = hx
         for i, L in enumerate(w.layers):
             relu = B.WINO_FLAG_RELU if L.relu else 0
             out.append((f"L{i}.filter", i, "filter",
-                        (lambda i=i, L=L: B.wino_filter_transform(hg[i], Us[i], L.C, L.K, L.m, sp))))
+                        (lambda sp, i=i, L=L: B.wino_filter_transform(hg[i], Us[i], L.C, L.K, L.m, sp))))
             if staged:
-                out.append((f"L{i}.input", i, "input", (lambda i=i, L=L, a=a: B.wino_input_transform(
+                out.append((f"L{i}.input", i, "input", (lambda sp, i=i, L=L, a=a: B.wino_input_transform(
                     a, Vs[i], N, L.C, L.H, L.W, L.pad, L.m, sp))))
-                out.append((f"L{i}.gemm", i, "gemm", (lambda i=i, L=L: B.wino_batched_gemm(
+                out.append((f"L{i}.gemm", i, "gemm", (lambda sp, i=i, L=L: B.wino_batched_gemm(
                     Us[i], Vs[i], Ms[i], N, L.C, L.H, L.W, L.K, L.pad, L.m, sp))))
-                out.append((f"L{i}.output", i, "output", (lambda i=i, L=L, relu=relu: B.wino_output_transform(
+                out.append((f"L{i}.output", i, "output", (lambda sp, i=i, L=L, relu=relu: B.wino_output_transform(
                     Ms[i], ys[i], N, L.K, L.H, L.W, L.pad, L.m, relu, sp))))
             else:
                 ws, wsb = wss[i]
-                out.append((f"L{i}.conv", i, "fused", (lambda i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                out.append((f"L{i}.conv", i, "fused", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                      L.pad, L.m, flags | relu,
                                                                      ws if wsb else None, wsb, sp))))
             a = ys[i]
             if L.pool:
-                out.append((f"L{i}.pool", i, "maxpool", (lambda i=i, L=L, a=a: B.wino_maxpool2x2(
+                out.append((f"L{i}.pool", i, "maxpool", (lambda sp, i=i, L=L, a=a: B.wino_maxpool2x2(
                     a, pools[i], N, L.K, nums[i]["Ho"], nums[i]["Wo"], sp))))
                 a = pools[i]
         return out
 
     step = launches()
 
-    def run_step():
-        for label, _, _, fn in step:
-            st = fn()
+    def run(fns):
+        sp = torch.cuda.current_stream().cuda_stream
+        for label, fn in fns:
+            st = fn(sp)
             if st != 0:
                 raise RuntimeError(f"{label}: {B.wino_status_string(st)}")
 
+    step_fns = [(label, fn) for label, _, _, fn in step]
+
+    def capture(fns, reps=1):
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            run(fns)                 # one eager pass on the capture stream first
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                run(fns)
+        torch.cuda.synchronize()
+        return g
+
+    stream = torch.cuda.current_stream()
+    GS = 10
+    use_graph = args.graph and not args.eager and not args.no_graphs
+    if use_graph and args.steps % GS:
+        raise SystemExit(f"--graph needs --steps to be a multiple of {GS}")
+    graph = capture(step_fns, reps=GS) if use_graph else None
+
     for _ in range(args.warmup):
-        run_step()
+        run(step_fns)
     torch.cuda.synchronize()
 
     # Timed region: exactly K steps, synchronised on both sides.
@@ -177,32 +341,93 @@ def main():
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     e0.record(stream)
-    for _ in range(args.steps):
-        run_step()
+    if graph is None:
+        for _ in range(args.steps):
+            run(step_fns)
+    else:
+        for _ in range(args.steps // GS):
+            graph.replay()
     e1.record(stream)
     torch.cuda.synchronize()
     wall1 = time.perf_counter()
     ms_step = e0.elapsed_time(e1) / args.steps
 
-    # Per-kernel durations: the same K steps again with an event pair around
-    # every launch, on the launch stream.
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in step]
-           for _ in range(args.steps)]
+    # The other launch mode of the same step, for reference (outside the timed region).
+    ref_steps = 20 * GS
     torch.cuda.synchronize()
-    for s in range(args.steps):
-        for j, (label, _, _, fn) in enumerate(step):
-            evs[s][j][0].record(stream)
-            fn()
-            evs[s][j][1].record(stream)
+    if args.no_graphs:
+        eager_ms, graph_ms = ms_step, None
+    elif graph is None:
+        g_ref = capture(step_fns, reps=GS)
+        e0.record(stream)
+        for _ in range(ref_steps // GS):
+            g_ref.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        eager_ms, graph_ms = ms_step, e0.elapsed_time(e1) / ref_steps
+        g_ref = None
+    else:
+        e0.record(stream)
+        for _ in range(ref_steps):
+            run(step_fns)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        eager_ms, graph_ms = e0.elapsed_time(e1) / ref_steps, ms_step
+
+    # Per-kernel average launch durations: for each launch of the step, a graph
+    # of R back-to-back launches of it alone (no host launch gaps), timed under
+    # HIP events on the stream the kernels run on.
+    R = 20
+    reps = max(1, min(args.steps // 10, 50))
+    per_launch = []
+    for label, _, _, fn in step:
+        if args.no_graphs:
+            g = None
+            def launch_r(fn=fn, label=label):
+                run([(label, fn)] * R)
+        else:
+            g = capture([(label, fn)], reps=R)
+            launch_r = g.replay
+        launch_r()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0.record(stream)
+            launch_r()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / R)
+        per_launch.append(float(np.median(ts)))
+        launch_r = g = None
+    # restore the step's outputs (the per-kernel graphs rewrote them)
+    run(step_fns)
     torch.cuda.synchronize()
-    per_launch = [float(np.mean([evs[s][j][0].elapsed_time(evs[s][j][1]) for s in range(args.steps)]))
-                  for j in range(len(step))]
+
+    total_by = {}
+    for (label, li, kind, _), t in zip(step, per_launch):
+        total_by[kind] = total_by.get(kind, 0.0) + t
     dom = int(np.argmax(per_launch))
     dlabel, dlayer, dkind, _ = step[dom]
-    dsec = per_launch[dom] / 1e3
-    roof = roofline(dkind, nums[dlayer], dsec)
-    roof["kernel"] = dlabel
+    roof = roofline(dkind, nums[dlayer], per_launch[dom] / 1e3)
+    roof["kernel"] = f"{dlabel} ({KERNEL_NAMES[dkind][5:]})"
     roof["avg_us"] = round(per_launch[dom] * 1e3, 3)
+    traffic, src = read_traffic(name, dkind) if len(w.layers) == 1 else (None, "multi-layer workload")
+    roof["traffic"] = traffic
+    roof["traffic_source"] = os.path.relpath(src, HERE) if traffic is not None else src
+
+    # Plain streaming kernel of known size (reads COPY_BYTES, writes COPY_BYTES:
+    # torch's elementwise negation): calibrates the HBM byte counters of the
+    # rocprofv3 PMC runs of this script.  It runs outside every timed region.
+    cs = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).uniform_()
+    cd = torch.empty_like(cs)
+    for _ in range(3):
+        torch.neg(cs, out=cd)
+    e0.record(stream)
+    torch.neg(cs, out=cd)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * COPY_BYTES / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del cs, cd
 
     direct = sum(f["direct_flops"] for f in nums)
     value = direct / (ms_step / 1e3) / 1e9
@@ -222,10 +447,17 @@ def main():
         "data": "synthetic",
         "config": {"workload": name, "N": N, "layers": len(w.layers),
                    "C": w.first.C, "K": w.first.K, "H": w.first.H, "W": w.first.W,
-                   "m": w.first.m, "pad": w.first.pad, "flags": hex(flags), "parallelism": "none"},
+                   "m": w.first.m, "pad": w.first.pad, "flags": hex(flags),
+                   "launch": "eager" if graph is None else "hip_graph", "parallelism": "none"},
         "roofline": roof,
         "per_launch_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, per_launch)},
+        "per_kind_us": {k: round(t * 1e3, 3) for k, t in total_by.items()},
+        "conv_only_gflops": round(direct / (sum(t for (_, _, k, _), t in zip(step, per_launch)
+                                                 if k != "filter") / 1e3) / 1e9, 1),
+        "eager_ms_per_step": round(eager_ms, 6),
+        "graph_ms_per_step": round(graph_ms, 6) if graph_ms is not None else None,
         "wall_ms_per_step": round((wall1 - wall0) * 1e3 / args.steps, 6),
+        "copy_calibration_gbs": round(copy_gbs, 1),
     }
 
     # CPU baseline: the fp64 oracle on this host, on a bounded sample (the first
@@ -234,19 +466,19 @@ def main():
         from oracle import direct as odirect
         L0, g0 = w.first, gs[0]
         y_gpu = ys[0].detach().cpu().numpy()      # holds the last step's output (ReLU applied)
-        reps, t_cpu, ref = 0, 0.0, None
-        while t_cpu < args.cpu_seconds and reps < 1000:
+        reps_cpu, t_cpu, ref = 0, 0.0, None
+        while t_cpu < args.cpu_seconds and reps_cpu < 100000:
             t0 = time.perf_counter()
             ref = odirect.conv2d(x, g0, L0.pad)
             t_cpu += time.perf_counter() - t0
-            reps += 1
+            reps_cpu += 1
         if L0.relu:
             ref = np.maximum(ref, 0.0)
         err = float(np.abs(y_gpu - ref).max() / max(np.abs(ref).max(), 1e-300))
         result["cpu_baseline"] = {
-            "value": round(nums[0]["direct_flops"] * reps / t_cpu / 1e9, 3),
+            "value": round(nums[0]["direct_flops"] * reps_cpu / t_cpu / 1e9, 3),
             "unit": "GFLOP/s", "cores": odirect.num_threads(), "kind": "oracle",
-            "sample": f"layer 0 of {name} (whole layer, N={N}), {reps} run(s), {t_cpu:.1f} s"}
+            "sample": f"layer 0 of {name} (whole layer, N={N}), {reps_cpu} run(s), {t_cpu:.1f} s"}
         result["max_rel_err_layer0"] = err
     print(json.dumps(result), flush=True)
 

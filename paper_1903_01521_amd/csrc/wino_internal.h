@@ -30,6 +30,7 @@ struct FusedTiling {
     int nkg;        // filter groups (each 16 * 8/(row groups * csplit) filters)
     int per;        // work items per XCD, ceil(nt * nkg / 8)
     int nsteps;     // channel steps, ceil(CQ / csplit)
+    int kfast;      // item order: 1 = filter group fastest (tile major), 0 = group major
 };
 
 size_t filter_elems(int C, int K, int m);                // T*Cp*Kp

@@ -160,15 +160,21 @@ __device__ __forceinline__ void store_t4(float* __restrict__ blk, int lane, cons
 }
 
 // ------------------------------------------------------------------ filter
-// One wave per (16-filter block, 4-channel quad); lane = (c%4)*16 + k%16.
+// One single-wave workgroup per (16-filter block, 4-channel quad, group of four
+// transform positions); lane = (c%4)*16 + k%16, so the wave writes one
+// contiguous 1 KiB run of U with a 16-byte store per lane.  Each lane redoes the
+// whole (cheap, fp64) transform of its filter and keeps its four positions: the
+// grid is T/4 times wider than one wave per filter pair, which keeps the
+// latency of this small kernel down.
 template <int MT>
-__global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, float* __restrict__ U,
-                                                int C, int K, int CQ, int KB) {
-    constexpr int T = (MT + 2) * (MT + 2);
-    const int lane = threadIdx.x & 63;
-    const long w = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= (long)KB * CQ) return;
-    const int kb = (int)(w / CQ), cq = (int)(w % CQ);
+__global__ __launch_bounds__(64) void k_filter(const float* __restrict__ gw, float* __restrict__ U,
+                                               int C, int K, int CQ) {
+    constexpr int T = (MT + 2) * (MT + 2), TG = T / 4;
+    const int lane = threadIdx.x;
+    const long w = blockIdx.x;                   // (kb * CQ + cq) * TG + tg
+    const int tg = (int)(w % TG);
+    const long pair = w / TG;
+    const int kb = (int)(pair / CQ), cq = (int)(pair % CQ);
     const int k = kb * 16 + (lane & 15), c = cq * 4 + (lane >> 4);
     float gg[3][3];
     const bool ok = k < K && c < C;
@@ -179,7 +185,11 @@ __global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, fl
         for (int s = 0; s < 3; ++s) gg[r][s] = ok ? src[r * 3 + s] : 0.0f;
     float u[T];
     filter_tf<MT>(gg, u);
-    store_t4<T>(U + (size_t)w * T * 64, lane, u);
+    float4 o = make_float4(u[0], u[1], u[2], u[3]);
+#pragma unroll
+    for (int g4 = 1; g4 < TG; ++g4)
+        if (g4 == tg) o = make_float4(u[4 * g4], u[4 * g4 + 1], u[4 * g4 + 2], u[4 * g4 + 3]);
+    *(float4*)(U + ((size_t)w * 64 + lane) * 4) = o;
 }
 
 // ------------------------------------------------------------------ input
@@ -448,23 +458,30 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
     f32x4 ua[NG], ub[NG];
     if constexpr (!S::SHARE) {
         // Step s: transform quad cs of step s (patch landed two steps ago), one
-        // quad of MFMAs; filters one step ahead.
+        // quad of MFMAs.  Filters also come two steps ahead, into a ring of three
+        // register sets that follows the three patch stages.
         constexpr int WAITN = S::JX + NG;     // loads issued in the previous step
+        f32x4 uc[NG];
+        auto uring = [&](auto rc) -> f32x4 (&)[NG] {
+            constexpr int R = decltype(rc)::value % 3;
+            if constexpr (R == 0) return ua;
+            else if constexpr (R == 1) return ub;
+            else return uc;
+        };
         issue_x(IC<0>{}, 0);
-        issue_x(IC<1>{}, 1);
         load_u(0, cs, ua);
+        issue_x(IC<1>{}, 1);
+        load_u(1, cs, ub);
         auto step = [&](auto rc, int s) {  // s % 3 == R
             constexpr int R = decltype(rc)::value;
-            wait_vm_lds<WAITN>();          // patch of step s has landed (for this wave)
+            wait_vm_lds<WAITN>();          // patch and filters of step s have landed (for this wave)
             wg_barrier();                  // ... for every wave; step s-1 is fully consumed
             issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
-            load_u(s + 1, cs, ub);
+            load_u(s + 2, cs, uring(IC<(R + 2) % 3>{}));
             __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's work
             float v[TH];
             transform(IC<R>{}, v);
-            mfma_quad(v, ua);
-#pragma unroll
-            for (int i = 0; i < NG; ++i) ua[i] = ub[i];
+            mfma_quad(v, uring(IC<R>{}));
         };
         int s = 0;
         for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
@@ -572,12 +589,15 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     __shared__ float4 vs[S::VSN / 4 > 0 ? S::VSN / 4 : 1];                 // transforms, then reduction
 
     // Work item, XCD-aware: workgroups go round-robin to the 8 XCDs, so XCD
-    // (b % 8) gets the contiguous run [xcd*per, (xcd+1)*per) of the filter-group-
-    // major order; its L2 then holds the filters of one or two groups.
+    // (b % 8) gets the contiguous run [xcd*per, (xcd+1)*per) of the item order.
+    // Filter-group-major order keeps one or two groups' filters in an XCD's L2;
+    // tile-major order (kfast) keeps the XCD's input patches there instead, and
+    // every filter group of a patch reads it from L2.
     const int b = blockIdx.x;
     const int item = (b & 7) * ft.per + (b >> 3);
     if (item >= ft.nt * ft.nkg) return;
-    const int kgi = item / ft.nt, tb = item - kgi * ft.nt;
+    const int kgi = ft.kfast ? item % ft.nkg : item / ft.nt;
+    const int tb = ft.kfast ? item / ft.nkg : item - kgi * ft.nt;
     const int per_img = ft.nbh * ft.nbw;
     const int n = tb / per_img, r2 = tb - n * per_img;
     const int ti0 = (r2 / ft.nbw) * S::BH, tj0 = (r2 % ft.nbw) * BW;
@@ -691,12 +711,13 @@ static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) 
 
 hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int m, hipStream_t s) {
     const int CQ = (C + 3) / 4, KB = (K + 15) / 16;
-    const long waves = (long)KB * CQ;
-    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    const long waves = (long)KB * CQ * ((m + 2) * (m + 2) / 4);
+    if (waves > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)waves), block(64);
     if (m == 2)
-        hipLaunchKernelGGL(k_filter<2>, grid, block, 0, s, gw, U, C, K, CQ, KB);
+        hipLaunchKernelGGL(k_filter<2>, grid, block, 0, s, gw, U, C, K, CQ);
     else
-        hipLaunchKernelGGL(k_filter<4>, grid, block, 0, s, gw, U, C, K, CQ, KB);
+        hipLaunchKernelGGL(k_filter<4>, grid, block, 0, s, gw, U, C, K, CQ);
     return hipGetLastError();
 }
 
@@ -739,6 +760,17 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
     ft.nkg = (g.KB + S::KGW - 1) / S::KGW;
     ft.per = (int)(((long)ft.nt * ft.nkg + 7) / 8);
     ft.nsteps = (g.CQ + S::QS - 1) / S::QS;
+    // Item order: estimate the bytes an XCD fetches past its L2 for each order,
+    // with one workgroup per CU (32 per XCD) resident at a time.  Filter-group
+    // major: every group re-reads the whole input; tile major: every resident
+    // set of 32 items re-reads the filters of all its groups.
+    {
+        const double xb = 4.0 * g.N * g.C * g.H * g.W, ub = 4.0 * g.T * g.CQ * 4 * g.KB * 16;
+        const double sets = (double)ft.nt * ft.nkg / 32.0;
+        const double group_major = xb * ft.nkg + ub * sets / ft.nkg;
+        const double tile_major = xb + ub * sets * (ft.nkg < 32 ? 1.0 : 32.0 / ft.nkg);
+        ft.kfast = tile_major < group_major ? 1 : 0;
+    }
     const dim3 grid((unsigned)(8 * ft.per)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
     hipLaunchKernelGGL((k_fused<MT, TS, CS, BW>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok);
