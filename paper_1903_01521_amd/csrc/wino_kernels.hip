@@ -353,9 +353,10 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 // record and read as 0.  Filters go straight to registers, one quad ahead (no
 // other wave uses them), one 16-byte load per 4 positions.  The region's input
 // transform gives exactly the B operand of v_mfma_f32_16x16x4_f32.  At the end
-// each wave applies its share of A^T M A (linear in M) and the TS*CS shares of
-// a filter block are summed through LDS in a fixed binary tree.
-template <int MT, int TS, int CS, int BW>
+// each wave applies its share of A^T M A (linear in M); the TS*CS shares of a
+// filter block are exchanged once through LDS, and every wave sums and stores
+// its own slice of the outputs, in a fixed order.
+template <int MT, int TS, int CS, int BW, int VEC>
 struct FusedShape {
     static constexpr int A = MT + 2, T = A * A, RN = A / TS, TH = RN * A;
     static constexpr int PARTS = TS * CS, KGW = 8 / PARTS, BH = 16 / BW;
@@ -363,17 +364,27 @@ struct FusedShape {
     static constexpr bool SHARE = KGW > 1;                 // transforms exchanged through LDS
     static constexpr int PR = BH * MT + 2;                 // patch rows
     static constexpr int PC = BW * MT + 2;                 // patch columns
-    static constexpr int PCP = (PC + 3) / 4 * 4;           // padded: 16-byte aligned rows
+    // VEC: the patch rows come as 16-byte chunks starting at the 4-aligned column
+    // at or before the patch (up to 3 columns early); else one float per load.
+    static constexpr int EW = VEC ? 4 : 1;                 // floats per load
+    static constexpr int PCP = VEC ? (PC + 6) / 4 * 4 : (PC + 3) / 4 * 4;   // row pitch, 16-byte aligned
+    static constexpr int NE = PCP / EW;                    // loads per patch row
     static constexpr int XS = 4 * QS * PR * PCP;           // patch floats per step
-    static constexpr int JX = (XS + 511) / 512;            // patch loads per thread per step
-    static constexpr int XSP = JX * 512;
+    static constexpr int JX = (XS / EW + 511) / 512;       // patch loads per thread per step
+    static constexpr int XSP = JX * 512 * EW;
     static constexpr int VSZ = TS * QS * TH * 64;          // floats of one transform stage
     static constexpr int NV = 4 * MT * MT;                 // output values per lane
-    static constexpr int REDT = (PARTS / 2) * KGW * NV * 64;   // first reduction round
-    static constexpr int VSN = (SHARE ? 2 * VSZ : 0) > REDT ? (SHARE ? 2 * VSZ : 0) : REDT;
+    // Output exchange: NB blocks of BS floats, placed in vs first, then in the
+    // three patch stages (CAPX blocks each); vs holds what the stages cannot.
+    static constexpr int NB = KGW * PARTS * (PARTS - 1), BS = NV / PARTS * 64;
+    static constexpr int CAPX = XSP / BS;
+    static constexpr int EXV = NB > 3 * CAPX ? (NB - 3 * CAPX) * BS : 0;
+    static constexpr int VSN0 = SHARE ? 2 * VSZ : 0;
+    static constexpr int VSN = (VSN0 > EXV ? VSN0 : EXV) > 4 ? (VSN0 > EXV ? VSN0 : EXV) : 4;
+    static constexpr int LDS_BYTES = 4 * (3 * (XSP + 4 * VEC) + VSN);
     static_assert(KGW * PARTS == 8, "8 waves per workgroup");
     static_assert(T % 4 == 0, "positions come in groups of 4");
-    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4 || PARTS == 8, "binary reduction tree");
+    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4 || PARTS == 8, "runs of whole output rows");
 };
 
 // s_waitcnt immediate: vmcnt <= n, lgkmcnt = 0, expcnt unconstrained.
@@ -392,14 +403,14 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 
 template <int R> using IC = std::integral_constant<int, R>;
 
-template <int MT, int TS, int CS, int BW, int H>
+template <int MT, int TS, int CS, int BW, int VEC, int H>
 __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
-                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW>::JX],
+                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW, VEC>::JX],
                                             uint32_t step_b, const float* __restrict__ U, const Geom& g,
                                             const FusedTiling& ft, int kb, int wave, int lane, int kw, int cs,
                                             int bi, int bj, float* xs0, float* xs1, float* xs2, float* vs,
-                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW>::TH]) {
-    using S = FusedShape<MT, TS, CS, BW>;
+                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC>::TH], int xlo) {
+    using S = FusedShape<MT, TS, CS, BW, VEC>;
     constexpr int A = S::A, RN = S::RN, X0 = H * RN, TH = S::TH, T = S::T, QS = S::QS, KGW = S::KGW;
     constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;   // this row group's position groups
     const int cl = lane >> 4;
@@ -418,7 +429,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         const uint32_t cbase = (uint32_t)j * step_b;
 #pragma unroll
         for (int i = 0; i < S::JX; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + i * 512 + wave * 64, 4, xoff[i] + cbase, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + xlo + (i * 512 + wave * 64) * S::EW, 4 * S::EW,
+                                                     xoff[i] + cbase, 0, 0, 0);
     };
     // Filters of (step j, quad slot q): a quad past CQ repeats a valid block (it
     // meets zero regions); past the last step it repeats the last step.
@@ -430,7 +442,9 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         for (int i = 0; i < NG; ++i) ug[i] = *(const f32x4*)(p + i * 256);
     };
     auto transform = [&](auto rc, float (&v)[TH]) {
-        const float* wp = xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT;
+        // VEC: the patch's first column sits 4 floats in (or at 0 when the
+        // chunks start on it), so region rows stay 16-byte aligned.
+        const float* wp = xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT + (xlo ? 4 : 0);
         float d[A][A];
 #pragma unroll
         for (int u = 0; u < A; ++u) {
@@ -566,10 +580,10 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
 }
 
 // o[r] = this wave's share of the m x m output of (tile, filter 16*kb + 4*cl + r)
-template <int MT, int TS, int CS, int BW, int H>
-__device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS, CS, BW>::TH],
+template <int MT, int TS, int CS, int BW, int VEC, int H>
+__device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC>::TH],
                                             float (&o)[4][MT][MT]) {
-    using S = FusedShape<MT, TS, CS, BW>;
+    using S = FusedShape<MT, TS, CS, BW, VEC>;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         float m1[S::TH];
@@ -579,14 +593,14 @@ __device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS
     }
 }
 
-template <int MT, int TS, int CS, int BW>
+template <int MT, int TS, int CS, int BW, int VEC>
 __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, const float* __restrict__ U,
                                                float* __restrict__ y, Geom g, FusedTiling ft, int relu,
                                                int vec_ok) {
-    using S = FusedShape<MT, TS, CS, BW>;
+    using S = FusedShape<MT, TS, CS, BW, VEC>;
     constexpr int PARTS = S::PARTS, KGW = S::KGW, NV = S::NV;
-    __shared__ float4 xs0[S::XSP / 4], xs1[S::XSP / 4], xs2[S::XSP / 4];   // patch stages
-    __shared__ float4 vs[S::VSN / 4 > 0 ? S::VSN / 4 : 1];                 // transforms, then reduction
+    __shared__ float4 xs0[S::XSP / 4 + VEC], xs1[S::XSP / 4 + VEC], xs2[S::XSP / 4 + VEC];  // patch stages
+    __shared__ float4 vs[S::VSN / 4];                      // transforms, then the output exchange
 
     // Work item, XCD-aware: workgroups go round-robin to the 8 XCDs, so XCD
     // (b % 8) gets the contiguous run [xcd*per, (xcd+1)*per) of the item order.
@@ -613,22 +627,31 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     tc.tj = tj0 + bj;
     tc.valid = tc.ti < g.th && tc.tj < g.tw;
 
-    // Patch element e = j*512 + tid of [4*QS channels][PR][PCP]: its byte offset
-    // in image n for step 0 (kInvalid outside the image or past the row).
+    // Patch load e = j*512 + tid of [4*QS channels][PR][NE loads]: its byte
+    // offset in image n for step 0 (kInvalid outside the image or past the
+    // row).  VEC: loads are 16-byte chunks from column col0, which is the patch's
+    // first column moved back by xsh to a multiple of 4; with W % 4 == 0 every
+    // chunk lies wholly inside or wholly outside the row.
     const size_t img = (size_t)g.C * g.H * g.W;
     const size_t img_b = img * 4;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(x + (size_t)n * img), (short)0, (int)(img_b < kInvalid ? img_b : kInvalid), kRsrcWord3);
     const uint32_t plane_b = (uint32_t)g.H * g.W * 4;
+    // In LDS the chunks start xlo floats past the stage base, which puts the
+    // patch's first column (xsh floats into its chunk) on a 16-byte boundary.
+    const int xsh = VEC ? (4 - g.pad % 4) % 4 : 0, xlo = (4 - xsh) % 4;
+    const int row0 = ti0 * MT - g.pad, col0 = tj0 * MT - g.pad - xsh;
     uint32_t xoff[S::JX];
 #pragma unroll
     for (int j = 0; j < S::JX; ++j) {
         const int e = j * 512 + tid;
-        const int ch = e / (S::PR * S::PCP), rem = e % (S::PR * S::PCP);
-        const int r = rem / S::PCP, c = rem % S::PCP;
-        const int row = ti0 * MT - g.pad + r, col = tj0 * MT - g.pad + c;
-        const bool ok = e < S::XS && c < S::PC && row >= 0 && row < g.H && col >= 0 && col < g.W;
-        xoff[j] = ok ? (uint32_t)ch * plane_b + ((uint32_t)row * g.W + col) * 4 : kInvalid;
+        const int ch = e / (S::PR * S::NE), rem = e - ch * (S::PR * S::NE);
+        const int r = rem / S::NE, c = (rem - r * S::NE) * S::EW;
+        const int row = row0 + r, col = col0 + c;
+        const bool ok = (e * S::EW < S::XS) & (VEC || c < S::PC) & ((unsigned)row < (unsigned)g.H) &
+                        ((unsigned)col < (unsigned)g.W);
+        const uint32_t off = (uint32_t)ch * plane_b + ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u;
+        xoff[j] = ok ? off : kInvalid;
     }
     const uint32_t step_b = 4u * S::QS * plane_b;
 
@@ -641,55 +664,100 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     float* xs2f = (float*)xs2;
     float* vsf = (float*)vs;
     if constexpr (TS == 1) {
-        fused_steps<MT, TS, CS, BW, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
-                                       xs2f, vsf, acc);
-        fused_share<MT, TS, CS, BW, 0>(acc, o);
+        fused_steps<MT, TS, CS, BW, VEC, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
+                                       xs2f, vsf, acc, xlo);
+        fused_share<MT, TS, CS, BW, VEC, 0>(acc, o);
     } else {
         if (h == 0) {
-            fused_steps<MT, TS, CS, BW, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
-                                           xs1f, xs2f, vsf, acc);
-            fused_share<MT, TS, CS, BW, 0>(acc, o);
+            fused_steps<MT, TS, CS, BW, VEC, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
+                                           xs1f, xs2f, vsf, acc, xlo);
+            fused_share<MT, TS, CS, BW, VEC, 0>(acc, o);
         } else {
-            fused_steps<MT, TS, CS, BW, 1>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
-                                           xs1f, xs2f, vsf, acc);
-            fused_share<MT, TS, CS, BW, 1>(acc, o);
+            fused_steps<MT, TS, CS, BW, VEC, 1>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f,
+                                           xs1f, xs2f, vsf, acc, xlo);
+            fused_share<MT, TS, CS, BW, VEC, 1>(acc, o);
         }
     }
 
     const int kbase = (kgi * KGW + kw) * 16 + 4 * cl;   // filters of this lane's slots r = 0..3
-    if constexpr (PARTS > 1) {
-        // Binary tree over the parts of each filter block: in the round with
-        // stride half, part p in [half, 2*half) publishes its share and part
-        // p - half adds it.  Slot layout red[kw][p - half][v][lane],
-        // v = (r*MT + i)*MT + j.
-        float* red = vsf;
+    const bool rl = relu != 0, vo = vec_ok != 0;
+    if constexpr (PARTS == 1) {
 #pragma unroll
-        for (int half = PARTS / 2; half >= 1; half /= 2) {
-            __syncthreads();
-            if (part >= half && part < 2 * half) {
-                float* slot = red + ((size_t)(kw * (PARTS / 2) + part - half) * NV) * 64 + lane;
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-#pragma unroll
-                    for (int i = 0; i < MT; ++i)
-#pragma unroll
-                        for (int j = 0; j < MT; ++j) slot[((r * MT + i) * MT + j) * 64] = o[r][i][j];
+        for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[r], rl, vo);
+    } else {
+        // One exchange through LDS.  A lane's NV output values (v = (r*MT + i)*MT
+        // + j) are cut into PARTS runs of NVS; part p adds run p of every part of
+        // its filter block, in a fixed order, and stores it.  Block (kw, j, p),
+        // j != p, carries run j of part p to part j as [NVS/VW][64][VW] floats;
+        // blocks fill vs, then xs0, xs1, xs2 (the patch stages are idle now).
+        constexpr int NVS = NV / PARTS, VW = NVS >= 4 ? 4 : NVS, BS = S::BS;
+        constexpr int CAPV = S::VSN / BS, CAPX = S::CAPX;
+        static_assert(NVS % MT == 0, "runs are whole output rows");
+        static_assert(CAPV + 3 * CAPX >= S::NB, "exchange blocks fit in LDS");
+        // Apply f to block bi.  Each branch names its LDS array, so every access
+        // stays an LDS access (a runtime choice of array would become a generic
+        // pointer).  bi is uniform across the wave.
+        auto with_block = [&](int bi, auto&& f) {
+            if (bi < CAPV || CAPX == 0) {
+                f(vsf + bi * BS + lane * VW);
+            } else {
+                const int k = bi - CAPV, a = k / (CAPX > 0 ? CAPX : 1), off = (k - a * CAPX) * BS + lane * VW;
+                if (a == 0) f(xs0f + off);
+                else if (a == 1) f(xs1f + off);
+                else f(xs2f + off);
             }
-            __syncthreads();
-            if (part < half) {
-                const float* slot = red + ((size_t)(kw * (PARTS / 2) + part) * NV) * 64 + lane;
+        };
+#define WINO_OVAL(v) o[(v) / (MT * MT)][((v) / MT) % MT][(v) % MT]
+        __syncthreads();                     // every wave is done with the patch stages and V
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
+        for (int j = 0; j < PARTS; ++j) {
+            if (j == part) continue;
+            with_block((kw * PARTS + j) * (PARTS - 1) + (part < j ? part : part - 1), [&](float* blk) {
 #pragma unroll
-                    for (int i = 0; i < MT; ++i)
-#pragma unroll
-                        for (int j = 0; j < MT; ++j) o[r][i][j] += slot[((r * MT + i) * MT + j) * 64];
-            }
+                for (int q = 0; q < NVS / VW; ++q) {
+                    const int v = j * NVS + q * VW;
+                    if constexpr (VW == 4)
+                        *(float4*)(blk + q * 64 * VW) =
+                            make_float4(WINO_OVAL(v), WINO_OVAL(v + 1), WINO_OVAL(v + 2), WINO_OVAL(v + 3));
+                    else
+                        *(float2*)(blk + q * 64 * VW) = make_float2(WINO_OVAL(v), WINO_OVAL(v + 1));
+                }
+            });
         }
-        if (part != 0) return;
-    }
+        __syncthreads();
+        float sum[NVS];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[r], relu != 0, vec_ok != 0);
+        for (int j = 0; j < PARTS; ++j)
+            if (j == part) {
+#pragma unroll
+                for (int i = 0; i < NVS; ++i) sum[i] = WINO_OVAL(j * NVS + i);
+            }
+        const int b0 = (kw * PARTS + part) * (PARTS - 1);
+#pragma unroll
+        for (int i = 0; i < PARTS - 1; ++i) {
+            with_block(b0 + i, [&](const float* blk) {
+#pragma unroll
+                for (int q = 0; q < NVS / VW; ++q) {
+                    if constexpr (VW == 4) {
+                        const float4 a4 = *(const float4*)(blk + q * 64 * VW);
+                        sum[q * 4] += a4.x; sum[q * 4 + 1] += a4.y; sum[q * 4 + 2] += a4.z; sum[q * 4 + 3] += a4.w;
+                    } else {
+                        const float2 a2 = *(const float2*)(blk + q * 64 * VW);
+                        sum[q * 2] += a2.x; sum[q * 2 + 1] += a2.y;
+                    }
+                }
+            });
+        }
+#pragma unroll
+        for (int rr = 0; rr < NVS / MT; ++rr) {
+            const int v0 = part * NVS + rr * MT;
+            float row[MT];
+#pragma unroll
+            for (int jj = 0; jj < MT; ++jj) row[jj] = sum[rr * MT + jj];
+            store_row<MT>(y, g, tc, kbase + v0 / (MT * MT), (v0 / MT) % MT, row, rl, vo);
+        }
+#undef WINO_OVAL
+    }
 }
 
 // ------------------------------------------------------------------ maxpool
@@ -749,10 +817,12 @@ hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool
     return hipGetLastError();
 }
 
+constexpr int kMaxLdsBytes = 160 * 1024;
+
 template <int MT, int TS, int CS, int BW>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
                                  hipStream_t s) {
-    using S = FusedShape<MT, TS, CS, BW>;
+    using S = FusedShape<MT, TS, CS, BW, 0>;
     FusedTiling ft;
     ft.nbh = (g.th + S::BH - 1) / S::BH;
     ft.nbw = (g.tw + BW - 1) / BW;
@@ -773,7 +843,15 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
     }
     const dim3 grid((unsigned)(8 * ft.per)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
-    hipLaunchKernelGGL((k_fused<MT, TS, CS, BW>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok);
+    // 16-byte patch loads need rows of whole chunks and an aligned image base,
+    // and the variant's larger stages must fit in LDS.
+    if constexpr (FusedShape<MT, TS, CS, BW, 1>::LDS_BYTES <= kMaxLdsBytes) {
+        if (g.W % 4 == 0 && aligned(x, 16)) {
+            hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 1>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 0>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok);
     return hipGetLastError();
 }
 

@@ -38,7 +38,25 @@ SHAPES = [
     (1, 4, 3, 3, 4, 0),
     (1, 24, 57, 57, 48, 1),
     (2, 64, 30, 30, 64, 1),
+    # widths that are multiples of 4 (16-byte patch loads), every padding phase
+    (1, 8, 16, 16, 20, 0),
+    (2, 12, 12, 20, 17, 1),
+    (1, 8, 9, 8, 16, 2),
+    (1, 4, 7, 12, 8, 3),
+    (1, 40, 24, 72, 32, 1),
 ]
+
+
+def tile_bound(bound, m):
+    """Max of |x|*|g| over each m x m output tile, broadcast to the tile's outputs.
+    Winograd rounding error is tile-local: an output whose own window sees only
+    padding is still a cancellation of its tile's nonzero terms."""
+    N, K, Ho, Wo = bound.shape
+    th, tw = -(-Ho // m), -(-Wo // m)
+    b = np.zeros((N, K, th * m, tw * m))
+    b[:, :, :Ho, :Wo] = bound
+    t = b.reshape(N, K, th, m, tw, m).max(axis=(3, 5))
+    return np.repeat(np.repeat(t, m, axis=2), m, axis=3)[:, :, :Ho, :Wo]
 
 
 def _run_case(shape, m, flags, kind="normal", seed=0):
@@ -57,7 +75,7 @@ def test_conv2d_all_variants(m, shape):
     rng = np.random.default_rng(sum(shape) + m)
     x, g = wl.random_layer(rng, N, C, H, W, K)
     ref = direct.conv2d(x, g, pad)
-    bound = direct.conv2d(x, g, pad, absval=True)
+    bound = tile_bound(direct.conv2d(x, g, pad, absval=True), m)
     U = h.filter_transform(g, m)
     for name, flags in VARIANTS[m]:
         print(f"conv2d m={m} shape={shape} variant={name}", flush=True)
@@ -65,7 +83,7 @@ def test_conv2d_all_variants(m, shape):
         assert np.all(np.isfinite(y)), name
         err = h.normwise_err(y, ref)
         assert err <= TOL[m], (name, err)
-        # elementwise, scaled by |x|*|g|: catches a wrong value hidden by a large max
+        # elementwise, scaled by the tile's |x|*|g|: catches a wrong value hidden by a large max
         assert np.all(np.abs(y - ref) <= ELEM[m] * (bound + 1e-30)), name
 
 
@@ -100,7 +118,8 @@ def _exact_bound(x, g, pad, m):
 
 
 @pytest.mark.parametrize("m,scale", [(2, 4), (4, 576)])
-@pytest.mark.parametrize("shape", [(2, 8, 13, 11, 20, 1), (1, 20, 9, 9, 16, 0), (1, 24, 30, 30, 40, 1)])
+@pytest.mark.parametrize("shape", [(2, 8, 13, 11, 20, 1), (1, 20, 9, 9, 16, 0), (1, 24, 30, 30, 40, 1),
+                                   (1, 20, 9, 12, 16, 1), (2, 8, 12, 16, 20, 2)])
 def test_exact_on_integers(m, scale, shape):
     # Integer x and g with g a multiple of S^2 (S*G is an integer matrix), so U,
     # V, M and every partial sum are integers below 2^24: each variant must
@@ -155,3 +174,25 @@ def test_batch_independence_and_pad_invariance(m):
         xp = np.pad(x, ((0, 0), (0, 0), (1, 1), (1, 1)))
         y0 = h.host(h.conv2d(xp, U, K, 0, m, flags))
         assert np.array_equal(yb, y0), name
+
+
+@pytest.mark.parametrize("m", [2, 4])
+@pytest.mark.parametrize("shape", [(1, 12, 16, 16, 20, 1), (2, 8, 10, 24, 16, 2), (1, 20, 9, 12, 24, 0)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_patch_load_paths_agree(m, shape):
+    # With W % 4 == 0 and a 16-byte aligned input the fused kernel loads its
+    # patches in 16-byte chunks; an input one float off that alignment takes the
+    # one-float path.  Both feed the same arithmetic: bit-identical outputs.
+    N, C, H, W, K, pad = shape
+    rng = np.random.default_rng(sum(shape) + 17 * m)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    ref = direct.conv2d(x, g, pad)
+    U = h.filter_transform(g, m)
+    buf = torch.zeros(x.size + 1, dtype=torch.float32, device=h.DEV)
+    xs = buf[1:].view(N, C, H, W)                 # 4-byte aligned, not 16-byte aligned
+    xs.copy_(h.dev(x))
+    for name, flags in VARIANTS[m]:
+        ya = h.host(h.conv2d(x, U, K, pad, m, flags))
+        yu = h.host(h.conv2d(xs, U, K, pad, m, flags))
+        assert np.array_equal(ya, yu), name
+        assert h.normwise_err(ya, ref) <= TOL[m], name
