@@ -75,6 +75,9 @@ extern "C" {
 #define WINO_ALGO_AUTO     0x000u   /* let the planner choose (default) */
 #define WINO_ALGO_FUSED    0x100u   /* one kernel: input transform -> GEMMs -> output transform */
 #define WINO_ALGO_STAGED   0x200u   /* three kernels through the workspace (V, then M) */
+#define WINO_ALGO_SPLIT    0x300u   /* two kernels: input transform into a tile-blocked
+                                       workspace, then the GEMMs with the output
+                                       transform in their epilogue (large layers) */
 #define WINO_ALGO_MASK     0xF00u
 /* Optional overrides of the fused kernel's variant (0 = planner's choice):
  *   WINO_BLOCK_1x16 / WINO_BLOCK_4x4: a workgroup's 16 tiles are one row of 16
@@ -124,8 +127,11 @@ int wino_filter_transform(const float* g, float* U, int C, int K, int m, void* s
  *   flags : WINO_FLAG_RELU and/or one WINO_ALGO_* value.
  *   workspace / workspace_bytes : device scratch of at least
  *       wino_workspace_bytes(N,C,H,W,K,pad,m,flags) bytes (V and M of the staged
- *       algorithm); may be NULL/0 when that is 0.  Contents on return are
- *       unspecified; calls sharing one workspace must not overlap in time.
+ *       algorithm, the tile-blocked V of the split one); may be NULL/0 when that
+ *       is 0.  With WINO_ALGO_AUTO the planner uses the split algorithm only if
+ *       the workspace given is large enough, else the fused one.  Contents on
+ *       return are unspecified; calls sharing one workspace must not overlap in
+ *       time.
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */
 int wino_conv2d(const float* x, const float* U, float* y,
                 int N, int C, int H, int W, int K, int pad, int m,

@@ -28,6 +28,7 @@ WINO_FLAG_RELU = 0x001
 WINO_ALGO_AUTO = 0x000
 WINO_ALGO_FUSED = 0x100
 WINO_ALGO_STAGED = 0x200
+WINO_ALGO_SPLIT = 0x300
 WINO_ALGO_MASK = 0xF00
 
 

@@ -54,7 +54,8 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Plan: which algorithm, and which fused-kernel variant.
 struct Plan {
-    unsigned algo;        // WINO_ALGO_FUSED or WINO_ALGO_STAGED
+    unsigned algo;        // WINO_ALGO_FUSED, WINO_ALGO_SPLIT or WINO_ALGO_STAGED
+    bool automatic;       // chosen by the planner (split falls back to fused without workspace)
     FusedCfg cfg;
 };
 
@@ -76,15 +77,25 @@ long fused_workgroups(const Geom& g, FusedCfg c) {
     return nt * ((g.KB + kgw - 1) / kgw);
 }
 
+constexpr long kSplitMinItems = 1024;
+
+long split_items(const Geom& g, int bw) {
+    const int kgw = g.m == 4 ? 4 : 8;
+    return (split_blocks(g, bw) + 1) / 2 * ((g.KB + kgw - 1) / kgw);
+}
+
+size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeof(float); }
+
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
     if (flags & ~kKnownFlags) return WINO_ERR_UNSUPPORTED;
     const unsigned algo = flags & WINO_ALGO_MASK;
-    if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED)
+    if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED && algo != WINO_ALGO_SPLIT)
         return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
-    p->algo = (algo == WINO_ALGO_STAGED) ? WINO_ALGO_STAGED : WINO_ALGO_FUSED;
+    p->algo = algo == WINO_ALGO_AUTO ? WINO_ALGO_FUSED : algo;
+    p->automatic = algo == WINO_ALGO_AUTO;
     // Fused variant.  Tile blocks: a row of 16 tiles when the tile grid is at
     // least 12 wide, else 4 x 4.  Channel split: the smallest that gives the
     // 256 CUs a workgroup each (more filter blocks per workgroup share the
@@ -99,7 +110,12 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
         while (c.csplit < max_cs && fused_workgroups(g, c) < 240) c.csplit *= 2;
     }
     if (p->algo == WINO_ALGO_FUSED && !valid_cfg(g.m, c)) return WINO_ERR_UNSUPPORTED;
+    // The fused and split kernels address U through a 32-bit buffer range.
+    if (p->algo != WINO_ALGO_STAGED && (int64_t)g.KB * g.CQ * g.T * 256 > 0x7fffffffLL) return WINO_ERR_UNSUPPORTED;
     p->cfg = c;
+    // Split path for layers with enough work items (tile-block pairs x filter
+    // groups) to fill the chip several times over.
+    if (p->automatic && !cs_req && split_items(g, c.bw) >= kSplitMinItems) p->algo = WINO_ALGO_SPLIT;
     return WINO_OK;
 }
 
@@ -148,6 +164,7 @@ size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, u
     if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
     if (p.algo == WINO_ALGO_FUSED) return 0;
+    if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
 
@@ -175,6 +192,17 @@ int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, i
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
     const bool relu = (flags & WINO_FLAG_RELU) != 0;
     hipStream_t s = (hipStream_t)stream;
+    if (p.algo == WINO_ALGO_SPLIT) {
+        const size_t need = split_workspace(g, p.cfg.bw);
+        if (!workspace || workspace_bytes < need) {
+            if (!p.automatic) return WINO_ERR_WORKSPACE;
+            p.algo = WINO_ALGO_FUSED;
+        } else {
+            if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+                return WINO_ERR_INVALID_ARG;
+            return hip_status(launch_split(x, U, y, (float*)workspace, g, p.cfg.bw, relu, s));
+        }
+    }
     if (p.algo == WINO_ALGO_FUSED) return hip_status(launch_fused(x, U, y, g, p.cfg, relu, s));
 
     const size_t vb = round_up(v_elems(g) * sizeof(float), 256);

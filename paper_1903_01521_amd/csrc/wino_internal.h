@@ -31,6 +31,7 @@ struct FusedTiling {
     int per;        // work items per XCD, ceil(nt * nkg / 8)
     int nsteps;     // channel steps, ceil(CQ / csplit)
     int kfast;      // item order: 1 = filter group fastest (tile major), 0 = group major
+    int bw;         // split path: tile-block width (16 or 4)
 };
 
 size_t filter_elems(int C, int K, int m);                // T*Cp*Kp
@@ -43,6 +44,12 @@ hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const G
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s);
 hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg cfg,
                         bool relu, hipStream_t s);
+// Split path: input transform into a tile-blocked workspace, then the GEMMs
+// with the output transform in their epilogue.
+long split_blocks(const Geom& g, int bw);
+size_t vblk_elems(const Geom& g, int bw);
+hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
+                        hipStream_t s);
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s);
 
 }  // namespace wino

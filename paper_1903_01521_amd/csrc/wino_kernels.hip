@@ -62,6 +62,19 @@ __device__ __forceinline__ TileCoord decode_tile(int p, const Geom& g) {
 constexpr uint32_t kInvalid = 1u << 30;
 constexpr int kRsrcWord3 = 0x00020000;   // raw (unformatted) 32-bit buffer
 
+// Transformed filters as a raw buffer (the host keeps U below 2 GiB for the
+// fused kernels).  A lane's 16-byte word of a U group sits at the constant
+// per-lane offset lane*16 plus a wave-uniform group offset, so filter loads
+// need no per-load address registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t u_rsrc(const float* U, const Geom& g) {
+    const size_t ub = (size_t)g.KB * g.CQ * g.T * 256;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)U, (short)0, (int)(ub < 0x7fffffffu ? ub : 0x7fffffffu),
+                                             kRsrcWord3);
+}
+__device__ __forceinline__ f32x4 u_load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t group_off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)group_off, 0));
+}
+
 template <int MT>
 struct RegionPlan {
     __amdgpu_buffer_rsrc_t rsrc;     // wave-uniform
@@ -434,12 +447,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
     };
     // Filters of (step j, quad slot q): a quad past CQ repeats a valid block (it
     // meets zero regions); past the last step it repeats the last step.
-    const float* ubase = U + ((size_t)kb * g.CQ * (T / 4) + G0) * 256 + lane * 4;
+    const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
+    const uint32_t ulane = (uint32_t)lane * 16u;
     auto load_u = [&](int j, int q, f32x4 (&ug)[NG]) {
         const int cq = min(min(j, ft.nsteps - 1) * QS + q, g.CQ - 1);
-        const float* p = ubase + (size_t)cq * (T / 4) * 256;
+        const uint32_t go = __builtin_amdgcn_readfirstlane((uint32_t)(((kb * g.CQ + cq) * (T / 4) + G0) * 1024));
 #pragma unroll
-        for (int i = 0; i < NG; ++i) ug[i] = *(const f32x4*)(p + i * 256);
+        for (int i = 0; i < NG; ++i) ug[i] = u_load(ur, ulane, go + i * 1024u);
     };
     auto transform = [&](auto rc, float (&v)[TH]) {
         // VEC: the patch's first column sits 4 floats in (or at 0 when the
@@ -760,6 +774,362 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     }
 }
 
+// ------------------------------------------------------------------ split
+// The split path, for layers with many tiles: k_vblk writes the input
+// transform to a tile-blocked workspace, then k_gemm_out runs the T GEMMs with
+// the output transform in their epilogue.  The transform's adds then run once
+// per (tile, channel) instead of once per filter group, and the GEMM loop is
+// MFMAs and LDS reads only -- on gfx950 vector ALU work does not overlap the
+// MFMAs of its SIMD, so it costs its full time inside a GEMM loop.
+//
+// Tile-blocked V: Vb[tb][CQ4][T/4][64][4], tb = (n*nbh + bh)*nbw + bw a spatial
+// block of 16 tiles (BH x BW), CQ4 = CQ rounded up to a multiple of 4 (the
+// padding quads hold zeros); element (t, c, tile (bh*BH + bi, bw*BW + bj)) at
+// lane (c%4)*16 + bi*BW + bj, slot t%4 of group t/4.
+
+// Patch byte offsets of one image for load e = j*NT + tid of
+// [4*NQ channels][PR rows][NE loads] (kInvalid outside the image or past the
+// row); VEC loads are 16-byte chunks from a 4-aligned column xsh floats before
+// the patch.
+template <int MT, int NT, int NQ, int PR, int PC, int PCP, int VEC, int JX>
+__device__ __forceinline__ void patch_offsets(uint32_t (&xoff)[JX], const Geom& g, int tid, int ti0, int tj0,
+                                              int xsh) {
+    constexpr int EW = VEC ? 4 : 1, NE = PCP / EW, XS = 4 * NQ * PR * PCP;
+    const uint32_t plane_b = (uint32_t)g.H * g.W * 4;
+    const int row0 = ti0 * MT - g.pad, col0 = tj0 * MT - g.pad - xsh;
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+        const int e = j * NT + tid;
+        const int ch = e / (PR * NE), rem = e - ch * (PR * NE);
+        const int r = rem / NE, c = (rem - r * NE) * EW;
+        const int row = row0 + r, col = col0 + c;
+        const bool ok = (e * EW < XS) & (VEC || c < PC) & ((unsigned)row < (unsigned)g.H) &
+                        ((unsigned)col < (unsigned)g.W);
+        const uint32_t off = (uint32_t)ch * plane_b + ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u;
+        xoff[j] = ok ? off : kInvalid;
+    }
+}
+
+// One direct-to-LDS buffer load of BYTES per lane (a device function: the
+// host pass rejects the 16-byte form written directly in a kernel body).
+template <int BYTES>
+__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, uint32_t off) {
+    static_assert(BYTES == 4 || BYTES == 16, "dword or 16-byte loads");
+    if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 4, off, 0, 0, 0);
+}
+
+template <int MT, int BW, int VEC>
+struct VblkShape {
+    static constexpr int A = MT + 2, T = A * A, BH = 16 / BW;
+    static constexpr int NQ = 4;                          // channel quads per workgroup, one per wave
+    static constexpr int PR = BH * MT + 2, PC = BW * MT + 2;
+    static constexpr int EW = VEC ? 4 : 1;
+    static constexpr int PCP = VEC ? (PC + 6) / 4 * 4 : (PC + 3) / 4 * 4;
+    static constexpr int XS = 4 * NQ * PR * PCP;
+    static constexpr int JX = (XS / EW + 255) / 256;
+    static constexpr int XSP = JX * 256 * EW;
+};
+
+// One workgroup per (tile block, 4 channel quads): the halo'd patch comes into
+// LDS by DMA, each wave transforms one quad for the block's 16 tiles and
+// stores its 9 (m = 4) or 4 (m = 2) 1 KiB groups.
+template <int MT, int BW, int VEC>
+__global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
+                                              int nbh, int nbw, int ncq4) {
+    using S = VblkShape<MT, BW, VEC>;
+    constexpr int A = S::A, T = S::T;
+    __shared__ float4 xs[S::XSP / 4 + VEC];
+    const int b = blockIdx.x;
+    const int tb = b / ncq4, q4 = b - tb * ncq4;
+    const int per_img = nbh * nbw;
+    const int n = tb / per_img, r2 = tb - n * per_img;
+    const int ti0 = (r2 / nbw) * S::BH, tj0 = (r2 % nbw) * BW;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, bi = l16 / BW, bj = l16 % BW, cl = lane >> 4;
+
+    const size_t img = (size_t)g.C * g.H * g.W;
+    const size_t img_b = img * 4;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + (size_t)n * img), (short)0, (int)(img_b < kInvalid ? img_b : kInvalid), kRsrcWord3);
+    const int xsh = VEC ? (4 - g.pad % 4) % 4 : 0, xlo = (4 - xsh) % 4;
+    uint32_t xoff[S::JX];
+    patch_offsets<MT, 256, S::NQ, S::PR, S::PC, S::PCP, VEC, S::JX>(xoff, g, tid, ti0, tj0, xsh);
+    const uint32_t cbase = (uint32_t)q4 * 16u * ((uint32_t)g.H * g.W * 4);
+    float* xf = (float*)xs;
+#pragma unroll
+    for (int i = 0; i < S::JX; ++i) lds_dma<4 * S::EW>(xr, xf + xlo + (i * 256 + wave * 64) * S::EW, xoff[i] + cbase);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const int cq = q4 * 4 + wave;        // < CQ4; quads past CQ read zero patches and store zeros
+    const float* wp = xf + ((wave * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT + (xlo ? 4 : 0);
+    float d[A][A];
+#pragma unroll
+    for (int u = 0; u < A; ++u) {
+        const float* row = wp + u * S::PCP;
+        if constexpr (MT == 4) {
+            const float4 a4 = *(const float4*)row;
+            const float2 b2 = *(const float2*)(row + 4);
+            d[u][0] = a4.x; d[u][1] = a4.y; d[u][2] = a4.z; d[u][3] = a4.w; d[u][4] = b2.x; d[u][5] = b2.y;
+        } else {
+            const float2 a2 = *(const float2*)row;
+            const float2 b2 = *(const float2*)(row + 2);
+            d[u][0] = a2.x; d[u][1] = a2.y; d[u][2] = b2.x; d[u][3] = b2.y;
+        }
+    }
+    float v[T];
+    input_tf<MT>(d, v);
+    store_t4<T>(Vb + ((size_t)tb * (ncq4 * 4) + cq) * T * 64, lane, v);
+}
+
+// GEMMs + output transform from Vb.  A workgroup of 8 waves computes two tile
+// blocks for KGW = 8/TS filter blocks over all channels; wave (kw, h) owns
+// filter block kw and transform rows [h*A/TS, (h+1)*A/TS) of both tile blocks
+// (each filter operand it loads feeds two MFMAs).  Per step of NQ = 4 channel
+// quads the two blocks' V (one contiguous run each) come into LDS by DMA one
+// step ahead, in two stages; filters come one quad ahead into registers.  At
+// the end each wave applies its share of A^T M A and, for TS = 2, the two row
+// halves of a filter block are summed through LDS in a fixed order.
+template <int MT>
+struct GoShape {
+    static constexpr int A = MT + 2, T = A * A, TG = T / 4;
+    static constexpr int TS = MT == 4 ? 2 : 1, KGW = 8 / TS, RN = A / TS, TH = RN * A;
+    static constexpr int TBW = 2, NQ = 4;                 // tile blocks, channel quads per step
+    static constexpr int VST = TBW * NQ * T * 64;         // floats of one V stage
+    static constexpr int JV = VST / 4 / 512;              // 16-byte DMA loads per thread per step
+    static constexpr int NV = 4 * MT * MT;                // output values per lane per tile block
+    static_assert(JV * 512 * 4 == VST, "whole DMA rounds");
+};
+
+template <int MT, int H>
+__device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32_t vbase0, uint32_t vbase1,
+                                         const float* __restrict__ U, const Geom& g, int nsteps, int kb,
+                                         int wave, int lane, float* vs0, float* vs1,
+                                         f32x4 (&acc)[2][GoShape<MT>::TH]) {
+    using S = GoShape<MT>;
+    constexpr int A = S::A, RN = S::RN, X0 = H * RN, TH = S::TH, T = S::T, NQ = S::NQ;
+    constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;
+    // V stage layout [block b][quad q][T/4][64][4]: the DMA of a step copies run
+    // b (NQ quads of block b, contiguous in Vb) to [b]; load e = i*512 + tid.
+    auto stage = [&](auto rc) -> float* {
+        if constexpr (decltype(rc)::value == 0) return vs0;
+        else return vs1;
+    };
+    // DMA loads i0 .. i1-1 (of JV) of step j's V into stage rc.  Unit e =
+    // i*512 + tid of the stage is unit e of block 0's run or unit e - JV*256 of
+    // block 1's; the padding quads of Vb are zeros, so no unit needs a mask.
+    const uint32_t tid16 = ((uint32_t)wave * 64 + lane) * 16u;
+    auto issue_v = [&](auto rc, int j, auto i0c, auto i1c) {
+        float* vs = stage(rc);
+        const uint32_t qoff = (uint32_t)j * NQ * T * 256;       // bytes: NQ quads of T*64 floats
+#pragma unroll
+        for (int i = decltype(i0c)::value; i < decltype(i1c)::value; ++i) {
+            constexpr int RUN = S::JV * 256 * 16;                // bytes of one block's run
+            const uint32_t e16 = (uint32_t)i * 8192u + tid16;   // byte offset of the unit in the stage
+            const uint32_t off = e16 < (uint32_t)RUN ? vbase0 + e16 : vbase1 + (e16 - RUN);
+            lds_dma<16>(vr, vs + (i * 512 + wave * 64) * 4, off + qoff);
+        }
+    };
+    const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
+    const uint32_t ulane = (uint32_t)lane * 16u;
+    auto load_u = [&](int cq, f32x4 (&ug)[NG]) {
+        const int c = min(cq, g.CQ - 1);
+        const uint32_t go = __builtin_amdgcn_readfirstlane((uint32_t)(((kb * g.CQ + c) * (T / 4) + G0) * 1024));
+#pragma unroll
+        for (int i = 0; i < NG; ++i) ug[i] = u_load(ur, ulane, go + i * 1024u);
+    };
+    // quad q of the stage: 2 blocks x TH MFMAs, V read group by group; after
+    // group gi, between(gi) (the next step's V DMA is spread over quad 0)
+    auto quad = [&](const float* vs, int q, const f32x4 (&ug)[NG], auto&& between) {
+#pragma unroll
+        for (int gi = 0; gi < NG; ++gi) {
+            f32x4 vv[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) vv[b] = *(const f32x4*)(vs + (((b * NQ + q) * (T / 4) + G0 + gi) * 64 + lane) * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int t = (G0 + gi) * 4 + e - X0 * A;       // position within this wave's rows
+                if (t >= 0 && t < TH) {
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) acc[b][t] = mfma16x16x4(ug[gi][e], vv[b][e], acc[b][t]);
+                }
+            }
+            between(gi);
+        }
+    };
+    f32x4 ua[NG], ub[NG];
+    // Loads of quad q of step s, in order: the filters of the next quad, then
+    // (q < 3) part q of the next step's V DMA, JP loads -- spread so that no
+    // wave stalls behind the whole burst.  Waiting for a quad's filters only
+    // forces DMA parts issued two quads earlier; at the start of step s+1 all of
+    // its V must have landed: the NG filter loads of quad 3 came after it.
+    constexpr int WAITN = NG;
+    constexpr int JV = S::JV, JP = (JV + 2) / 3;
+    issue_v(IC<0>{}, 0, IC<0>{}, IC<JV>{});
+    load_u(0, ua);
+    wait_vm_lds<NG>();                // V of step 0 has landed (for this wave)
+    auto step = [&](auto rc, int s) {  // s % 2 == R
+        constexpr int R = decltype(rc)::value;
+        wait_vm_lds<WAITN>();          // V of step s has landed (this wave)
+        wg_barrier();                  // ... every wave's; stage R^1 (step s-1) is consumed
+        const float* vs = stage(IC<R>{});
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            f32x4 (&cur)[NG] = (q & 1) ? ub : ua;
+            f32x4 (&nxt)[NG] = (q & 1) ? ua : ub;
+            load_u(s * NQ + q + 1, nxt);
+            auto part = [&](auto pc) {
+                constexpr int P = decltype(pc)::value;
+                constexpr int A0 = P * JP < JV ? P * JP : JV, A1 = (P + 1) * JP < JV ? (P + 1) * JP : JV;
+                if (q == P) issue_v(IC<R ^ 1>{}, s + 1, IC<A0>{}, IC<A1>{});
+            };
+            part(IC<0>{});
+            part(IC<1>{});
+            part(IC<2>{});
+            __builtin_amdgcn_sched_barrier(0);
+            quad(vs, q, cur, [](int) {});
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    int s = 0;
+    for (; s + 2 <= nsteps; s += 2) {      // straight-line body: exact wait analysis
+        step(IC<0>{}, s);
+        step(IC<1>{}, s + 1);
+    }
+    if (s < nsteps) step(IC<0>{}, s);
+    __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
+}
+
+template <int MT>
+__global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, const float* __restrict__ U,
+                                                  float* __restrict__ y, Geom g, FusedTiling ft, int ntb,
+                                                  int relu, int vec_ok) {
+    using S = GoShape<MT>;
+    constexpr int TS = S::TS, KGW = S::KGW, TH = S::TH, NV = S::NV;
+    __shared__ float4 vs0[S::VST / 4], vs1[S::VST / 4];
+
+    // item = (tile-block pair, filter group), XCD-aware as in k_fused
+    const int b = blockIdx.x;
+    const int item = (b & 7) * ft.per + (b >> 3);
+    if (item >= ft.nt * ft.nkg) return;
+    const int kgi = ft.kfast ? item % ft.nkg : item / ft.nt;
+    const int tp = ft.kfast ? item / ft.nkg : item - kgi * ft.nt;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kw = wave / TS, h = wave % TS;
+    const int kb = min(kgi * KGW + kw, g.KB - 1);
+    const int cl = lane >> 4;
+
+    // Vb as a buffer: a block past the last reads zeros
+    const size_t blk_b = (size_t)((g.CQ + 3) / 4 * 4) * g.T * 256;   // bytes of one tile block
+    const size_t tot_b = (size_t)ntb * blk_b;
+    const size_t first = (size_t)(2 * tp) * blk_b;
+    const size_t left = tot_b - first;
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)((const char*)Vb + first), (short)0, (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
+
+    f32x4 acc[2][TH];
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int t = 0; t < TH; ++t) acc[bb][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float* v0 = (float*)vs0;
+    float* v1 = (float*)vs1;
+    if constexpr (TS == 1) {
+        go_steps<MT, 0>(vr, 0u, (uint32_t)blk_b, U, g, ft.nsteps, kb, wave, lane, v0, v1, acc);
+    } else {
+        if (h == 0) go_steps<MT, 0>(vr, 0u, (uint32_t)blk_b, U, g, ft.nsteps, kb, wave, lane, v0, v1, acc);
+        else go_steps<MT, 1>(vr, 0u, (uint32_t)blk_b, U, g, ft.nsteps, kb, wave, lane, v0, v1, acc);
+    }
+
+    // This wave's share of A^T M A for both tile blocks.
+    float o[2][4][MT][MT];
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb) {
+        f32x4 a1[TH];
+#pragma unroll
+        for (int t = 0; t < TH; ++t) a1[t] = acc[bb][t];
+        if constexpr (TS == 1) {
+            fused_share<MT, 1, 8, 16, 0, 0>(a1, o[bb]);
+        } else {
+            if (h == 0) fused_share<MT, 2, 1, 16, 0, 0>(a1, o[bb]);
+            else fused_share<MT, 2, 1, 16, 0, 1>(a1, o[bb]);
+        }
+    }
+    const int kbase = (kgi * KGW + kw) * 16 + 4 * cl;
+    const int per_img = ft.nbh * ft.nbw;
+    auto tile_of = [&](int bb) {
+        const int tb = 2 * tp + bb;
+        const int n = tb / per_img, r2 = tb - n * per_img;
+        const int bh = 16 / ft.bw;
+        const int l16 = lane & 15;
+        TileCoord tc;
+        tc.n = n;
+        tc.ti = (r2 / ft.nbw) * bh + l16 / ft.bw;
+        tc.tj = (r2 % ft.nbw) * ft.bw + l16 % ft.bw;
+        tc.valid = tb < ntb && tc.ti < g.th && tc.tj < g.tw;
+        return tc;
+    };
+    const bool rl = relu != 0, vo = vec_ok != 0;
+    if constexpr (TS == 1) {
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) {
+            const TileCoord tc = tile_of(bb);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+        }
+    } else {
+        // Row half h of filter block kw sums tile block h (its own share plus
+        // the other half's, written to LDS) and stores it.  Slot (kw, bb) of
+        // NV*64 floats: kw < 2 in vs0, else vs1 (each branch names its array,
+        // so the accesses stay LDS accesses).
+        static_assert(4 * NV * 64 <= S::VST, "two exchange slots per filter block per stage");
+        auto with_slot = [&](int bb, auto&& f) {
+            const int k = (kw & 1) * 2 + bb;
+            if (kw < 2) f((float*)vs0 + (size_t)k * NV * 64 + lane);
+            else f((float*)vs1 + (size_t)k * NV * 64 + lane);
+        };
+        __syncthreads();                       // every wave is done with the V stages
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) {
+            if (bb == h) continue;
+            with_slot(bb, [&](float* slot) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < MT; ++j) slot[((r * MT + i) * MT + j) * 64] = o[bb][r][i][j];
+            });
+        }
+        __syncthreads();
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) {
+            if (bb != h) continue;
+            float sl[4][MT][MT];
+            with_slot(bb, [&](float* slot) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < MT; ++j) sl[r][i][j] = slot[((r * MT + i) * MT + j) * 64];
+            });
+            const TileCoord tc = tile_of(bb);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float ob[MT][MT];
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                    for (int j = 0; j < MT; ++j) ob[i][j] = o[bb][r][i][j] + sl[r][i][j];
+                store_block<MT>(y, g, tc, kbase + r, ob, rl, vo);
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------------ maxpool
 __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x, float* __restrict__ y,
                                                     long total, int H, int W, int Ho, int Wo) {
@@ -876,6 +1246,57 @@ hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g,
     WINO_FUSED_CASE(4, 2, 4, 4)
 #undef WINO_FUSED_CASE
     return hipErrorInvalidValue;
+}
+
+// Tile blocks of the split path's workspace for block width bw.
+long split_blocks(const Geom& g, int bw) {
+    const int bh = 16 / bw;
+    return (long)g.N * ((g.th + bh - 1) / bh) * ((g.tw + bw - 1) / bw);
+}
+size_t vblk_elems(const Geom& g, int bw) { return (size_t)split_blocks(g, bw) * ((g.CQ + 3) / 4 * 4) * g.T * 64; }
+
+template <int MT, int BW>
+static hipError_t split_instance(const float* x, const float* U, float* y, float* Vb, const Geom& g, bool relu,
+                                 hipStream_t s) {
+    using GS = GoShape<MT>;
+    FusedTiling ft;
+    ft.bw = BW;
+    ft.nbh = (g.th + 16 / BW - 1) / (16 / BW);
+    ft.nbw = (g.tw + BW - 1) / BW;
+    const int ntb = g.N * ft.nbh * ft.nbw;
+    const int ncq4 = (g.CQ + 3) / 4;
+    {
+        const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
+        if (g.W % 4 == 0 && aligned(x, 16)) {
+            hipLaunchKernelGGL((k_vblk<MT, BW, 1>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
+        } else {
+            hipLaunchKernelGGL((k_vblk<MT, BW, 0>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    ft.nt = (ntb + 1) / 2;
+    ft.nkg = (g.KB + GS::KGW - 1) / GS::KGW;
+    ft.per = (int)(((long)ft.nt * ft.nkg + 7) / 8);
+    ft.nsteps = (g.CQ + GS::NQ - 1) / GS::NQ;
+    {   // item order: V of a tile pair is read by every filter group
+        const double vb = 4.0 * vblk_elems(g, BW), ub = 4.0 * g.T * g.CQ * 4 * g.KB * 16;
+        const double sets = (double)ft.nt * ft.nkg / 32.0;
+        const double group_major = vb * ft.nkg + ub * sets / ft.nkg;
+        const double tile_major = vb + ub * sets * (ft.nkg < 32 ? 1.0 : 32.0 / ft.nkg);
+        ft.kfast = tile_major < group_major ? 1 : 0;
+    }
+    const dim3 grid((unsigned)(8 * ft.per)), block(512);
+    const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
+    hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, ntb, (int)relu, vec_ok);
+    return hipGetLastError();
+}
+
+hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
+                        hipStream_t s) {
+    if (g.m == 2) return bw == 16 ? split_instance<2, 16>(x, U, y, Vb, g, relu, s)
+                                  : split_instance<2, 4>(x, U, y, Vb, g, relu, s);
+    return bw == 16 ? split_instance<4, 16>(x, U, y, Vb, g, relu, s) : split_instance<4, 4>(x, U, y, Vb, g, relu, s);
 }
 
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s) {

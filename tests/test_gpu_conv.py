@@ -17,11 +17,14 @@ TOL = {2: 1e-4, 4: 1e-3}   # normwise max relative error gate per tile size
 ELEM = {2: 2e-5, 4: 2e-4}
 
 F = B.WINO_ALGO_FUSED
+BLOCKS = (("16", B.WINO_BLOCK_1x16), ("4x4", B.WINO_BLOCK_4x4))
 VARIANTS = {
     2: [("auto", 0), ("staged", B.WINO_ALGO_STAGED)]
+       + [(f"split_b{bn}", B.WINO_ALGO_SPLIT | bf) for bn, bf in BLOCKS]
        + [(f"f_b{bn}c{c}", F | bf | B.WINO_CSPLIT(c))
           for bn, bf in (("16", B.WINO_BLOCK_1x16), ("4x4", B.WINO_BLOCK_4x4)) for c in (1, 2, 4, 8)],
     4: [("auto", 0), ("staged", B.WINO_ALGO_STAGED)]
+       + [(f"split_b{bn}", B.WINO_ALGO_SPLIT | bf) for bn, bf in BLOCKS]
        + [(f"f_b{bn}c{c}", F | bf | B.WINO_CSPLIT(c))
           for bn, bf in (("16", B.WINO_BLOCK_1x16), ("4x4", B.WINO_BLOCK_4x4)) for c in (1, 2, 4)],
 }
