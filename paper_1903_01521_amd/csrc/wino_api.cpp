@@ -77,11 +77,34 @@ long fused_workgroups(const Geom& g, FusedCfg c) {
     return nt * ((g.KB + kgw - 1) / kgw);
 }
 
-constexpr long kSplitMinItems = 1024;
-
 long split_items(const Geom& g, int bw) {
     const int kgw = g.m == 4 ? 4 : 8;
     return (split_blocks(g, bw) + 1) / 2 * ((g.KB + kgw - 1) / kgw);
+}
+
+// Estimated time (ns) of the fused and split algorithms: both kernels run one
+// workgroup per CU, so a launch takes ceil(items/256) rounds of one
+// workgroup's MFMA work at an efficiency measured for each kernel family on
+// MI355X (fused: by filter blocks per workgroup), plus, for split, the
+// HBM-bound input transform (patches read with halo, tile-blocked V written).
+constexpr double kCus = 256.0, kFlopPerClk = 256.0, kClkGHz = 2.2, kHbmBytesPerNs = 7000.0;
+
+double rounds(long items) { return (double)((items + (long)kCus - 1) / (long)kCus); }
+
+double fused_ns(const Geom& g, FusedCfg c) {
+    const int kgw = 8 / (row_groups(g.m) * c.csplit);
+    const double eff = kgw >= 4 ? 0.58 : kgw == 2 ? 0.42 : 0.33;
+    const double work = 2.0 * 16 * kgw * 16 * (4.0 * g.CQ) * g.T;      // FLOP per workgroup
+    return rounds(fused_workgroups(g, c)) * work / (kFlopPerClk * eff) / kClkGHz;
+}
+
+double split_ns(const Geom& g, int bw) {
+    const int kgw = g.m == 4 ? 4 : 8;
+    const double cq4 = (g.CQ + 3) / 4 * 4;
+    const double work = 2.0 * 2 * 16 * kgw * 16 * (4.0 * cq4) * g.T;    // FLOP per workgroup
+    const double gemm = rounds(split_items(g, bw)) * work / (kFlopPerClk * 0.74) / kClkGHz;
+    const double bytes = 1.5 * 4.0 * g.N * g.C * g.H * g.W + 4.0 * (double)split_blocks(g, bw) * cq4 * g.T * 64;
+    return gemm + bytes / kHbmBytesPerNs;
 }
 
 size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeof(float); }
@@ -113,9 +136,10 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
     // The fused and split kernels address U through a 32-bit buffer range.
     if (p->algo != WINO_ALGO_STAGED && (int64_t)g.KB * g.CQ * g.T * 256 > 0x7fffffffLL) return WINO_ERR_UNSUPPORTED;
     p->cfg = c;
-    // Split path for layers with enough work items (tile-block pairs x filter
-    // groups) to fill the chip several times over.
-    if (p->automatic && !cs_req && split_items(g, c.bw) >= kSplitMinItems) p->algo = WINO_ALGO_SPLIT;
+    // Split path where the estimates favour it (layers with at least a full
+    // round of its workgroups).
+    if (p->automatic && !cs_req && split_items(g, c.bw) >= (long)kCus && split_ns(g, c.bw) < fused_ns(g, c))
+        p->algo = WINO_ALGO_SPLIT;
     return WINO_OK;
 }
 
