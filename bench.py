@@ -45,7 +45,7 @@ CSRC = os.path.join(HERE, "paper_1903_01521_amd", "csrc")
 PROFILES = os.path.join(HERE, "profiles")
 
 # Kernel-name prefixes as rocprofv3 reports them, per kind of launch.
-KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused",
+KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2"}
 
@@ -79,6 +79,7 @@ def layer_numbers(N, L):
     f["bytes"] = {
         "filter": 4 * L.K * L.C * 9 + u_b,
         "fused": x_b + u_b + y_b,
+        "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
         "gemm": v_b + u_b + m_b,
         "output": m_b + y_b,
@@ -289,7 +290,9 @@ def main():
                     Ms[i], ys[i], N, L.K, L.H, L.W, L.pad, L.m, relu, sp))))
             else:
                 ws, wsb = wss[i]
-                out.append((f"L{i}.conv", i, "fused", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                algo = flags & B.WINO_ALGO_MASK
+                lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4)
+                out.append((f"L{i}.conv", i, "lowc" if lowc else "fused", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                      L.pad, L.m, flags | relu,
                                                                      ws if wsb else None, wsb, sp))))

@@ -78,6 +78,8 @@ extern "C" {
 #define WINO_ALGO_SPLIT    0x300u   /* two kernels: input transform into a tile-blocked
                                        workspace, then the GEMMs with the output
                                        transform in their epilogue (large layers) */
+#define WINO_ALGO_LOWC     0x400u   /* one kernel for C <= 4 (a network's first layer): a
+                                       lane per tile, vector FMAs over the channels */
 #define WINO_ALGO_MASK     0xF00u
 /* Optional overrides of the fused kernel's variant (0 = planner's choice):
  *   WINO_BLOCK_1x16 / WINO_BLOCK_4x4: a workgroup's 16 tiles are one row of 16

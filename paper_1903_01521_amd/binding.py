@@ -29,6 +29,7 @@ WINO_ALGO_AUTO = 0x000
 WINO_ALGO_FUSED = 0x100
 WINO_ALGO_STAGED = 0x200
 WINO_ALGO_SPLIT = 0x300
+WINO_ALGO_LOWC = 0x400
 WINO_ALGO_MASK = 0xF00
 
 

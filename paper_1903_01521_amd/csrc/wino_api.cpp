@@ -112,8 +112,10 @@ size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeo
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
     if (flags & ~kKnownFlags) return WINO_ERR_UNSUPPORTED;
     const unsigned algo = flags & WINO_ALGO_MASK;
-    if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED && algo != WINO_ALGO_SPLIT)
+    if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED && algo != WINO_ALGO_SPLIT &&
+        algo != WINO_ALGO_LOWC)
         return WINO_ERR_UNSUPPORTED;
+    if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
@@ -136,6 +138,11 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
     // The fused and split kernels address U through a 32-bit buffer range.
     if (p->algo != WINO_ALGO_STAGED && (int64_t)g.KB * g.CQ * g.T * 256 > 0x7fffffffLL) return WINO_ERR_UNSUPPORTED;
     p->cfg = c;
+    // Layers with at most 4 channels: the low-C kernel.
+    if (p->automatic && g.C <= 4 && !cs_req && !blk) {
+        p->algo = WINO_ALGO_LOWC;
+        return WINO_OK;
+    }
     // Split path where the estimates favour it (layers with at least a full
     // round of its workgroups).
     if (p->automatic && !cs_req && split_items(g, c.bw) >= (long)kCus && split_ns(g, c.bw) < fused_ns(g, c))
@@ -187,7 +194,7 @@ size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, u
     Plan p;
     if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
-    if (p.algo == WINO_ALGO_FUSED) return 0;
+    if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
     if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
@@ -228,6 +235,7 @@ int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, i
         }
     }
     if (p.algo == WINO_ALGO_FUSED) return hip_status(launch_fused(x, U, y, g, p.cfg, relu, s));
+    if (p.algo == WINO_ALGO_LOWC) return hip_status(launch_lowc(x, U, y, g, relu, s));
 
     const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
     const size_t need = vb + m_elems(g) * sizeof(float);

@@ -50,6 +50,8 @@ long split_blocks(const Geom& g, int bw);
 size_t vblk_elems(const Geom& g, int bw);
 hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
                         hipStream_t s);
+// Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.
+hipError_t launch_lowc(const float* x, const float* U, float* y, const Geom& g, bool relu, hipStream_t s);
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s);
 
 }  // namespace wino

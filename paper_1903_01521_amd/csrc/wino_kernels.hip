@@ -129,6 +129,18 @@ __device__ __forceinline__ void load_region(const RegionPlan<MT>& rp, const Geom
     }
 }
 
+// Output rows leave through streaming (non-temporal) stores: y is written once
+// and not read back by the kernel, so it need not displace cached inputs.
+__device__ __forceinline__ void store_out(float* p, float a, float b, float c, float d) {
+    const f32x4 q = {a, b, c, d};
+    __builtin_nontemporal_store(q, (f32x4*)p);
+}
+__device__ __forceinline__ void store_out(float* p, float a, float b) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 q = {a, b};
+    __builtin_nontemporal_store(q, (f32x2*)p);
+}
+
 // Write output row i (MT values) of the block of (tile tc, output channel k),
 // cropped to Ho x Wo.
 template <int MT>
@@ -142,14 +154,14 @@ __device__ __forceinline__ void store_row(float* __restrict__ y, const Geom& g, 
     for (int j = 0; j < MT; ++j) v[j] = relu ? fmaxf(o[j], 0.0f) : o[j];
     if (vec_ok && oj0 + MT <= g.Wo) {
         if constexpr (MT == 4) {
-            *(float4*)row = make_float4(v[0], v[1], v[2], v[3]);
+            store_out(row, v[0], v[1], v[2], v[3]);
         } else {
-            *(float2*)row = make_float2(v[0], v[1]);
+            store_out(row, v[0], v[1]);
         }
     } else {
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-            if (oj0 + j < g.Wo) row[j] = v[j];
+            if (oj0 + j < g.Wo) __builtin_nontemporal_store(v[j], row + j);
     }
 }
 
@@ -173,36 +185,78 @@ __device__ __forceinline__ void store_t4(float* __restrict__ blk, int lane, cons
 }
 
 // ------------------------------------------------------------------ filter
-// One single-wave workgroup per (16-filter block, 4-channel quad, group of four
-// transform positions); lane = (c%4)*16 + k%16, so the wave writes one
-// contiguous 1 KiB run of U with a 16-byte store per lane.  Each lane redoes the
-// whole (cheap, fp64) transform of its filter and keeps its four positions: the
-// grid is T/4 times wider than one wave per filter pair, which keeps the
-// latency of this small kernel down.
-template <int MT>
-__global__ __launch_bounds__(64) void k_filter(const float* __restrict__ gw, float* __restrict__ U,
-                                               int C, int K, int CQ) {
+// Filter pairs (16 filters x 4 channels) from which one wave per pair computes
+// all positions.
+constexpr long kFilterAllPairs = 256;
+
+// The 4-position group tg (wave-uniform) of a lane's filter transform: a
+// branch per group, each computing only its own positions.
+template <int MT, int... G>
+__device__ __forceinline__ float4 filter_pick(int tg, const float (&g)[3][3], std::integer_sequence<int, G...>) {
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    ((tg == G ? (void)(o = filter_tf4<MT, 4 * G>(g)) : (void)0), ...);
+    return o;
+}
+
+// All position groups of a lane's filter transform, group G to U + G*256.
+template <int MT, int... G>
+__device__ __forceinline__ void filter_all(const float (&g)[3][3], float* __restrict__ u,
+                                           std::integer_sequence<int, G...>) {
+    ((*(float4*)(u + G * 256) = filter_tf4<MT, 4 * G>(g)), ...);
+}
+
+// One wave per (16-filter block, 4-channel quad) -- or, for layers with few
+// filter pairs, per (block, quad, group of four positions), which widens the
+// grid T/4 times and keeps the latency of the small case down.  Lane =
+// (c%4)*16 + k%16, so each group the wave writes is one contiguous 1 KiB run of
+// U with a 16-byte store per lane.  Four waves per workgroup.  With STAGE (one
+// wave per pair and CQ % 4 == 0) the workgroup's four quads are 16 consecutive
+// channels of the same 16 filters: it reads their 16 x 576 contiguous bytes of
+// g with coalesced loads into LDS first.
+template <int MT, bool ALL, bool STAGE>
+__global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, float* __restrict__ U,
+                                                int C, int K, int CQ, long nw) {
     constexpr int T = (MT + 2) * (MT + 2), TG = T / 4;
-    const int lane = threadIdx.x;
-    const long w = blockIdx.x;                   // (kb * CQ + cq) * TG + tg
-    const int tg = (int)(w % TG);
-    const long pair = w / TG;
-    const int kb = (int)(pair / CQ), cq = (int)(pair % CQ);
-    const int k = kb * 16 + (lane & 15), c = cq * 4 + (lane >> 4);
+    static_assert(ALL || !STAGE, "staging needs one wave per pair");
+    const int lane = threadIdx.x & 63;
+    const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     float gg[3][3];
-    const bool ok = k < K && c < C;
-    const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c : 0)) * 9;
+    long pair;
+    if constexpr (STAGE) {
+        __shared__ float gs[16 * 144];                // [filter][16 channels x 9]
+        const long p0 = (long)blockIdx.x * 4;         // nw % 4 == 0: every wave is valid
+        const int kb = (int)(p0 / CQ), c0 = (int)(p0 % CQ) * 4;
 #pragma unroll
-    for (int r = 0; r < 3; ++r)
+        for (int i = 0; i < 9; ++i) {
+            const int e = (int)threadIdx.x + 256 * i, row = e / 144, off = e - row * 144;
+            const int k = kb * 16 + row, c = c0 + off / 9;
+            gs[e] = (k < K && c < C) ? gw[((size_t)k * C + c0) * 9 + off] : 0.0f;
+        }
+        __syncthreads();
+        pair = w;
+        const float* src = gs + (lane & 15) * 144 + ((int)(w - p0) * 4 + (lane >> 4)) * 9;
 #pragma unroll
-        for (int s = 0; s < 3; ++s) gg[r][s] = ok ? src[r * 3 + s] : 0.0f;
-    float u[T];
-    filter_tf<MT>(gg, u);
-    float4 o = make_float4(u[0], u[1], u[2], u[3]);
+        for (int r = 0; r < 3; ++r)
 #pragma unroll
-    for (int g4 = 1; g4 < TG; ++g4)
-        if (g4 == tg) o = make_float4(u[4 * g4], u[4 * g4 + 1], u[4 * g4 + 2], u[4 * g4 + 3]);
-    *(float4*)(U + ((size_t)w * 64 + lane) * 4) = o;
+            for (int s = 0; s < 3; ++s) gg[r][s] = src[r * 3 + s];
+    } else {
+        if (w >= nw) return;
+        pair = ALL ? w : w / TG;                      // kb * CQ + cq
+        const int kb = (int)(pair / CQ), cq = (int)(pair % CQ);
+        const int k = kb * 16 + (lane & 15), c = cq * 4 + (lane >> 4);
+        const bool ok = k < K && c < C;
+        const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c : 0)) * 9;
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+            for (int s = 0; s < 3; ++s) gg[r][s] = ok ? src[r * 3 + s] : 0.0f;
+    }
+    if constexpr (ALL) {
+        filter_all<MT>(gg, U + ((size_t)pair * TG * 64 + lane) * 4, std::make_integer_sequence<int, TG>{});
+    } else {
+        *(float4*)(U + ((size_t)w * 64 + lane) * 4) =
+            filter_pick<MT>((int)(w % TG), gg, std::make_integer_sequence<int, TG>{});
+    }
 }
 
 // ------------------------------------------------------------------ input
@@ -1130,6 +1184,102 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
     }
 }
 
+// ------------------------------------------------------------------ low C
+// Layers with at most 4 input channels (a network's first layer).  The GEMMs
+// contract over NC <= 4 channels, so the layer is bound by writing y; the
+// fused kernels' per-workgroup phases (load, transform, MFMA, exchange,
+// store) would run one after another on each CU.  Here a lane owns one tile:
+// it keeps the transforms of its NC regions in registers and, filter by
+// filter, forms M_t = sum_c U_t[c][k] V_t[c] with vector FMAs (U broadcast
+// from LDS), applies A^T M A and stores the m x m block -- the stores of one
+// filter drain while the next is computed.  A workgroup of 4 waves covers 256
+// consecutive tiles and a range of KPW filters.
+template <int MT, int NC, bool RELU>
+__global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const float* __restrict__ U,
+                                              float* __restrict__ y, Geom g, int ntg, int kpw, int vec_ok) {
+    constexpr int A = MT + 2, T = A * A, TG = T / 4;
+    extern __shared__ float4 us4[];                   // [kpw][NC][T]
+    float* us = (float*)us4;
+    const int tg = blockIdx.x % ntg, kf = blockIdx.x / ntg;
+    const int k0 = kf * kpw, nk = min(kpw, g.K - k0);
+    const int tid = threadIdx.x;
+    // this workgroup's filters into LDS: element (t, c, k) of U is at lane
+    // c*16 + k%16, slot t%4 of group ((k/16)*CQ*TG + t/4) (CQ = 1 here)
+    for (int e = tid; e < nk * NC * T; e += 256) {
+        const int kk = e / (NC * T), rem = e - kk * (NC * T), c = rem / T, t = rem - c * T;
+        const int k = k0 + kk;
+        us[e] = U[((size_t)(k / 16) * TG + t / 4) * 256 + (c * 16 + k % 16) * 4 + t % 4];
+    }
+    const int p = tg * 256 + tid;
+    const TileCoord tc = decode_tile(p, g);
+    float v[NC][T];
+    {
+        const int r0 = tc.ti * MT - g.pad, c0 = tc.tj * MT - g.pad;
+        const float* xi = x + (size_t)tc.n * g.C * g.H * g.W;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            float d[A][A];
+#pragma unroll
+            for (int u = 0; u < A; ++u)
+#pragma unroll
+                for (int w = 0; w < A; ++w) {
+                    const int r = r0 + u, cc = c0 + w;
+                    const bool ok = tc.valid && (unsigned)r < (unsigned)g.H && (unsigned)cc < (unsigned)g.W;
+                    d[u][w] = ok ? xi[((size_t)c * g.H + r) * g.W + cc] : 0.0f;
+                }
+            input_tf<MT>(d, v[c]);
+        }
+    }
+    __syncthreads();
+    // A tile whose m x m block lies inside the image (all but the last tile row
+    // and column) stores whole rows with vector stores, no per-row checks.
+    const bool vo = vec_ok != 0;
+    const bool inner = vo && tc.valid && tc.ti * MT + MT <= g.Ho && tc.tj * MT + MT <= g.Wo;
+    const size_t plane = (size_t)g.Ho * g.Wo;
+    float* yb = y + ((size_t)tc.n * g.K + k0) * plane + (size_t)(tc.ti * MT) * g.Wo + tc.tj * MT;
+    for (int kk = 0; kk < nk; ++kk) {
+        const float4* uk = (const float4*)(us + (size_t)kk * NC * T);
+        float mv[T];
+#pragma unroll
+        for (int t4 = 0; t4 < TG; ++t4) {
+            const float4 u0 = uk[t4];
+            mv[4 * t4] = u0.x * v[0][4 * t4];
+            mv[4 * t4 + 1] = u0.y * v[0][4 * t4 + 1];
+            mv[4 * t4 + 2] = u0.z * v[0][4 * t4 + 2];
+            mv[4 * t4 + 3] = u0.w * v[0][4 * t4 + 3];
+#pragma unroll
+            for (int c = 1; c < NC; ++c) {
+                const float4 uc = uk[c * TG + t4];
+                mv[4 * t4] = __builtin_fmaf(uc.x, v[c][4 * t4], mv[4 * t4]);
+                mv[4 * t4 + 1] = __builtin_fmaf(uc.y, v[c][4 * t4 + 1], mv[4 * t4 + 1]);
+                mv[4 * t4 + 2] = __builtin_fmaf(uc.z, v[c][4 * t4 + 2], mv[4 * t4 + 2]);
+                mv[4 * t4 + 3] = __builtin_fmaf(uc.w, v[c][4 * t4 + 3], mv[4 * t4 + 3]);
+            }
+        }
+        float o[MT][MT];
+        output_tf<MT>(mv, o);
+        if (RELU) {
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int j = 0; j < MT; ++j) o[i][j] = fmaxf(o[i][j], 0.0f);
+        }
+        if (inner) {
+            float* r = yb + kk * plane;
+#pragma unroll
+            for (int i = 0; i < MT; ++i) {
+                if constexpr (MT == 4) {
+                    store_out(r + (size_t)i * g.Wo, o[i][0], o[i][1], o[i][2], o[i][3]);
+                } else {
+                    store_out(r + (size_t)i * g.Wo, o[i][0], o[i][1]);
+                }
+            }
+        } else {
+            store_block<MT>(y, g, tc, k0 + kk, o, false, vo);
+        }
+    }
+}
+
 // ------------------------------------------------------------------ maxpool
 __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x, float* __restrict__ y,
                                                     long total, int H, int W, int Ho, int Wo) {
@@ -1148,14 +1298,23 @@ __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x,
 static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int m, hipStream_t s) {
-    const int CQ = (C + 3) / 4, KB = (K + 15) / 16;
-    const long waves = (long)KB * CQ * ((m + 2) * (m + 2) / 4);
-    if (waves > 0x7fffffffL) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)waves), block(64);
-    if (m == 2)
-        hipLaunchKernelGGL(k_filter<2>, grid, block, 0, s, gw, U, C, K, CQ);
-    else
-        hipLaunchKernelGGL(k_filter<4>, grid, block, 0, s, gw, U, C, K, CQ);
+    const int CQ = (C + 3) / 4, KB = (K + 15) / 16, TG = (m + 2) * (m + 2) / 4;
+    const long pairs = (long)KB * CQ;
+    const bool all = pairs >= kFilterAllPairs;     // enough waves without splitting the positions
+    const bool stage = all && CQ % 4 == 0;         // a workgroup's quads share their filters
+    const long waves = all ? pairs : pairs * TG;
+    if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+#define WINO_FILTER_LAUNCH(MT)                                                                        \
+    if (stage) hipLaunchKernelGGL((k_filter<MT, true, true>), grid, block, 0, s, gw, U, C, K, CQ, waves); \
+    else if (all) hipLaunchKernelGGL((k_filter<MT, true, false>), grid, block, 0, s, gw, U, C, K, CQ, waves); \
+    else hipLaunchKernelGGL((k_filter<MT, false, false>), grid, block, 0, s, gw, U, C, K, CQ, waves);
+    if (m == 2) {
+        WINO_FILTER_LAUNCH(2)
+    } else {
+        WINO_FILTER_LAUNCH(4)
+    }
+#undef WINO_FILTER_LAUNCH
     return hipGetLastError();
 }
 
@@ -1297,6 +1456,30 @@ hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, con
     if (g.m == 2) return bw == 16 ? split_instance<2, 16>(x, U, y, Vb, g, relu, s)
                                   : split_instance<2, 4>(x, U, y, Vb, g, relu, s);
     return bw == 16 ? split_instance<4, 16>(x, U, y, Vb, g, relu, s) : split_instance<4, 4>(x, U, y, Vb, g, relu, s);
+}
+
+// Low-C path: tile groups of 256 x filter ranges; the filters are split so the
+// launch has at least ~512 workgroups when the layer has few tiles.
+hipError_t launch_lowc(const float* x, const float* U, float* y, const Geom& g, bool relu, hipStream_t s) {
+    const int ntg = (g.P + 255) / 256;
+    int ks = 1;
+    while (ks * 2 <= (g.K + 3) / 4 && (long)ntg * ks < 512) ks *= 2;
+    int kpw = (g.K + ks - 1) / ks;
+    if (kpw > 64) kpw = 64;                            // LDS: kpw*NC*T floats
+    ks = (g.K + kpw - 1) / kpw;
+    const dim3 grid((unsigned)((long)ntg * ks)), block(256);
+    const int vec_ok = (g.Wo % g.m == 0) && aligned(y, 4 * g.m);
+    const size_t lds = (size_t)kpw * g.C * g.T * sizeof(float);
+#define WINO_LOWC_CASE(MT, NC) \
+    if (g.m == MT && g.C == NC) { \
+        if (relu) hipLaunchKernelGGL((k_lowc<MT, NC, true>), grid, block, lds, s, x, U, y, g, ntg, kpw, vec_ok); \
+        else hipLaunchKernelGGL((k_lowc<MT, NC, false>), grid, block, lds, s, x, U, y, g, ntg, kpw, vec_ok); \
+        return hipGetLastError(); \
+    }
+    WINO_LOWC_CASE(2, 1) WINO_LOWC_CASE(2, 2) WINO_LOWC_CASE(2, 3) WINO_LOWC_CASE(2, 4)
+    WINO_LOWC_CASE(4, 1) WINO_LOWC_CASE(4, 2) WINO_LOWC_CASE(4, 3) WINO_LOWC_CASE(4, 4)
+#undef WINO_LOWC_CASE
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s) {

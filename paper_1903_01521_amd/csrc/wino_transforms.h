@@ -233,27 +233,28 @@ template <> struct GScaled<4> {
     }
 };
 
-// u[xi*A + nu] = (G g G^T)[xi][nu], fp64 inside, rounded to fp32
-template <int MT>
-__device__ __forceinline__ void filter_tf(const float (&g)[3][3], float (&u)[(MT + 2) * (MT + 2)]) {
+// Positions T0 .. T0+3 of U = G g G^T (t = xi*A + nu), fp64 inside, each
+// rounded once to fp32.  Only the rows of (S G) g that these positions need are
+// live after unrolling; the rest is dead code.
+template <int MT, int T0>
+__device__ __forceinline__ float4 filter_tf4(const float (&g)[3][3]) {
     constexpr int A = MT + 2;
-    double s[A][3];
+    double cs[3][A];                       // (S G) g, column c, every row
 #pragma unroll
-    for (int j = 0; j < 3; ++j) {          // (S G) g: column j
-        double col[3] = {(double)g[0][j], (double)g[1][j], (double)g[2][j]};
-        double r[A];
-        GScaled<MT>::rows(col, r);
-#pragma unroll
-        for (int i = 0; i < A; ++i) s[i][j] = r[i];
+    for (int c = 0; c < 3; ++c) {
+        const double col[3] = {(double)g[0][c], (double)g[1][c], (double)g[2][c]};
+        GScaled<MT>::rows(col, cs[c]);
     }
+    float o[4];
 #pragma unroll
-    for (int i = 0; i < A; ++i) {          // ((S G) g) (S G)^T: row i
-        double row[3] = {s[i][0], s[i][1], s[i][2]};
+    for (int e = 0; e < 4; ++e) {          // ((S G) g) (S G)^T at row xi, column nu
+        const int t = T0 + e, xi = t / A, nu = t % A;
+        const double row[3] = {cs[0][xi], cs[1][xi], cs[2][xi]};
         double r[A];
         GScaled<MT>::rows(row, r);
-#pragma unroll
-        for (int j = 0; j < A; ++j) u[i * A + j] = (float)(r[j] * GScaled<MT>::INV_S2);
+        o[e] = (float)(r[nu] * GScaled<MT>::INV_S2);
     }
+    return make_float4(o[0], o[1], o[2], o[3]);
 }
 
 }  // namespace wino

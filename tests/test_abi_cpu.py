@@ -50,7 +50,9 @@ def test_workspace_bytes():
     assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 3, 0) == 2**64 - 1
     # split: the tile-blocked V, 16-tile blocks (1 x 16 here: 28 x 28 tiles -> 28 x 2 blocks)
     assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_SPLIT) == 4 * 56 * 16 * 36 * 64
-    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, 0x400) == 2**64 - 1
+    assert B.wino_workspace_bytes(1, 3, 112, 112, 64, 1, 4, B.WINO_ALGO_LOWC) == 0
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_LOWC) == 2**64 - 1   # C > 4
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, 0x500) == 2**64 - 1
 
 
 GOOD = dict(N=1, C=4, H=8, W=8, K=4, pad=1, m=4)
@@ -77,7 +79,8 @@ def _conv(x=FAKE, U=FAKE, y=FAKE + 0x100000, flags=0, ws=None, wsb=0, **kw):
     (dict(m=3), B.WINO_ERR_UNSUPPORTED),
     (dict(m=6), B.WINO_ERR_UNSUPPORTED),
     (dict(flags=0x80000000), B.WINO_ERR_UNSUPPORTED),        # unknown flag bit
-    (dict(flags=0x400), B.WINO_ERR_UNSUPPORTED),             # unknown algorithm
+    (dict(flags=0x500), B.WINO_ERR_UNSUPPORTED),             # unknown algorithm
+    (dict(flags=B.WINO_ALGO_LOWC, C=5), B.WINO_ERR_UNSUPPORTED),   # low-C kernel needs C <= 4
     (dict(flags=B.WINO_ALGO_SPLIT), B.WINO_ERR_WORKSPACE),   # split needs its workspace
     (dict(flags=B.WINO_ALGO_FUSED | B.WINO_CSPLIT(3)), B.WINO_ERR_UNSUPPORTED),
     (dict(flags=B.WINO_ALGO_FUSED | B.WINO_CSPLIT(8)), B.WINO_ERR_UNSUPPORTED),  # m=4: 2 x 8 > 8 waves

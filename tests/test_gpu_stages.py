@@ -14,7 +14,10 @@ U32 = 2.0 ** -24          # unit roundoff of fp32
 
 
 @pytest.mark.parametrize("m", [2, 4])
-@pytest.mark.parametrize("C,K", [(3, 20), (16, 16), (37, 5), (64, 64)])
+# small layers take one wave per (filter pair, position group); from 512 filter
+# pairs on (the last three shapes) one wave per pair computes every position,
+# reading g through LDS when the channel quads come in fours (the last two)
+@pytest.mark.parametrize("C,K", [(3, 20), (16, 16), (37, 5), (64, 64), (130, 250), (126, 120), (512, 512)])
 def test_filter_transform(m, C, K):
     rng = np.random.default_rng(100 + C + K + m)
     _, g = wl.random_layer(rng, 1, C, 4, 4, K)
