@@ -105,14 +105,18 @@ def roofline(kind, nums, seconds):
             "algorithmic_flops": fl, "algorithmic_bytes": b}
 
 
-def traffic_file(workload: str) -> str:
-    return os.path.join(PROFILES, f"traffic_{workload}.txt")
+def traffic_file(workload: str, kind: str) -> str:
+    """Counter summary of a workload's convolution kernel (fused, low-C), or of
+    one stage of its staged path (input, gemm, output)."""
+    if kind in ("fused", "lowc"):
+        return os.path.join(PROFILES, f"traffic_{workload}.txt")
+    return os.path.join(PROFILES, f"traffic_{workload}_{kind}.txt")
 
 
 def read_traffic(workload: str, kind: str):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary, or None if there is none or it was taken on other sources."""
-    path = traffic_file(workload)
+    path = traffic_file(workload, kind)
     if not os.path.exists(path):
         return None, "no counter summary"
     kv = {}
@@ -162,16 +166,17 @@ def pmc_summary(args):
     wscale = wc * 1024 / COPY_BYTES
     traffic = fk * 1024 / fscale + wk * 1024 / wscale
     alg = sum(f["bytes"][kind] for f in nums) / len(nums)
+    fl = f" --flags {args.flags:#x}" if args.flags is not None else ""
     lines = [
         f"# HBM traffic per launch of the {kind} kernel on workload {name}",
         "# from two rocprofv3 PMC runs of bench.py on one MI355X (commands below), each",
         f"# counter scaled by what it reads for a plain streaming kernel over {COPY_BYTES} bytes.",
         "#   cd /tmp && export TMPDIR=/tmp",
         f"#   timeout -s KILL 60 rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/fetch -o run -- "
-        f"python3 <repo>/bench.py --workload {name} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
+        f"python3 <repo>/bench.py --workload {name}{fl} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
         f"#   timeout -s KILL 60 rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/write -o run -- "
-        f"python3 <repo>/bench.py --workload {name} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
-        f"#   python3 bench.py --workload {name} --kind {kind} --pmc-summary <out>/fetch <out>/write",
+        f"python3 <repo>/bench.py --workload {name}{fl} --steps 20 --warmup 2 --cpu-seconds 0 --no-graphs",
+        f"#   python3 bench.py --workload {name}{fl} --kind {kind} --pmc-summary <out>/fetch <out>/write",
         f"workload: {name}",
         f"kind: {kind}",
         f"kernels: {' | '.join(names)}",
@@ -191,9 +196,23 @@ def pmc_summary(args):
     ]
     text = "\n".join(lines) + "\n"
     if args.write_summary:
-        with open(traffic_file(name), "w") as fh:
+        with open(traffic_file(name, kind), "w") as fh:
             fh.write(text)
     print(text, end="")
+
+
+def sleep_calibration(stream) -> float:
+    """GPU cycles per millisecond of torch's spin kernel (torch.cuda._sleep)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(1000)
+    torch.cuda.synchronize()
+    n = 2_000_000
+    e0.record(stream)
+    torch.cuda._sleep(n)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return n / max(e0.elapsed_time(e1), 1e-3)
 
 
 def main():
@@ -379,7 +398,9 @@ def main():
 
     # Per-kernel average launch durations: for each launch of the step, a graph
     # of R back-to-back launches of it alone (no host launch gaps), timed under
-    # HIP events on the stream the kernels run on.
+    # HIP events on the stream the kernels run on.  Repeating a kernel alone lets
+    # inputs that fit the 256 MB last-level cache stay there; the in-sequence
+    # durations below show what each kernel takes after its real predecessors.
     R = 20
     reps = max(1, min(args.steps // 10, 50))
     per_launch = []
@@ -402,8 +423,38 @@ def main():
             ts.append(e0.elapsed_time(e1) / R)
         per_launch.append(float(np.median(ts)))
         launch_r = g = None
-    # restore the step's outputs (the per-kernel graphs rewrote them)
-    run(step_fns)
+
+    # In-sequence durations: HIP events around every launch of KP more eager
+    # steps.  The GPU is first held in a spin kernel while the host enqueues all
+    # KP steps, so the launches then run back to back with no host gaps, each
+    # after its real predecessors (cache state as in the timed region).  Each
+    # figure includes the launch's dispatch latency (~3 us), which back-to-back
+    # launches of one kernel hide.
+    cyc_per_ms = sleep_calibration(stream)
+    KP = max(1, min(args.steps, 300 // len(step)))
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in step] for _ in range(KP)]
+    sp = stream.cuda_stream
+    hold_ms = 20.0
+    for _ in range(3):
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(hold_ms * cyc_per_ms))
+        h0 = time.perf_counter()
+        for k in range(KP):
+            for (label, _, _, fn), (a0, a1) in zip(step, evs[k]):
+                a0.record(stream)
+                st = fn(sp)
+                a1.record(stream)
+                if st != 0:
+                    raise RuntimeError(f"{label}: {B.wino_status_string(st)}")
+        enqueue_ms = (time.perf_counter() - h0) * 1e3
+        torch.cuda.synchronize()
+        gapless = enqueue_ms < 0.8 * hold_ms
+        if gapless:
+            break
+        hold_ms = 2.5 * enqueue_ms
+    in_seq = [float(np.mean([evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(KP)]))
+              for i in range(len(step))]
     torch.cuda.synchronize()
 
     total_by = {}
@@ -455,6 +506,11 @@ def main():
         "roofline": roof,
         "per_launch_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, per_launch)},
         "per_kind_us": {k: round(t * 1e3, 3) for k, t in total_by.items()},
+        "per_launch_in_sequence_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, in_seq)},
+        "in_sequence_timing": {"steps": KP, "host_gaps": not gapless},
+        # every launch against the roof that bounds it (algorithmic work / duration)
+        "per_launch_roofline": {lbl: (lambda r: f"{r['bound']} {r['frac']:.3f}")(
+            roofline(kind, nums[li], t / 1e3)) for (lbl, li, kind, _), t in zip(step, per_launch)},
         "conv_only_gflops": round(direct / (sum(t for (_, _, k, _), t in zip(step, per_launch)
                                                  if k != "filter") / 1e3) / 1e9, 1),
         "eager_ms_per_step": round(eager_ms, 6),

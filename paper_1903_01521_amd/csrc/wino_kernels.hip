@@ -129,21 +129,29 @@ __device__ __forceinline__ void load_region(const RegionPlan<MT>& rp, const Geom
     }
 }
 
-// Output rows leave through streaming (non-temporal) stores: y is written once
-// and not read back by the kernel, so it need not displace cached inputs.
+// Output rows leave through streaming (non-temporal) stores where a kernel
+// writes whole cache lines: y is not read back, so it need not displace cached
+// inputs.  Where the lines of a row are completed by several store
+// instructions (rows narrower than a line run, or not line-aligned), plain
+// stores let L2 merge the pieces before they go to HBM; streaming stores of
+// such pieces run at half the bandwidth or less.
+template <bool NT>
 __device__ __forceinline__ void store_out(float* p, float a, float b, float c, float d) {
     const f32x4 q = {a, b, c, d};
-    __builtin_nontemporal_store(q, (f32x4*)p);
+    if constexpr (NT) __builtin_nontemporal_store(q, (f32x4*)p);
+    else *(f32x4*)p = q;
 }
+template <bool NT>
 __device__ __forceinline__ void store_out(float* p, float a, float b) {
     typedef float f32x2 __attribute__((ext_vector_type(2)));
     const f32x2 q = {a, b};
-    __builtin_nontemporal_store(q, (f32x2*)p);
+    if constexpr (NT) __builtin_nontemporal_store(q, (f32x2*)p);
+    else *(f32x2*)p = q;
 }
 
 // Write output row i (MT values) of the block of (tile tc, output channel k),
 // cropped to Ho x Wo.
-template <int MT>
+template <int MT, bool NT = true>
 __device__ __forceinline__ void store_row(float* __restrict__ y, const Geom& g, const TileCoord& tc, int k,
                                           int i, const float (&o)[MT], bool relu, bool vec_ok) {
     const int oi = tc.ti * MT + i, oj0 = tc.tj * MT;
@@ -154,34 +162,38 @@ __device__ __forceinline__ void store_row(float* __restrict__ y, const Geom& g, 
     for (int j = 0; j < MT; ++j) v[j] = relu ? fmaxf(o[j], 0.0f) : o[j];
     if (vec_ok && oj0 + MT <= g.Wo) {
         if constexpr (MT == 4) {
-            store_out(row, v[0], v[1], v[2], v[3]);
+            store_out<NT>(row, v[0], v[1], v[2], v[3]);
         } else {
-            store_out(row, v[0], v[1]);
+            store_out<NT>(row, v[0], v[1]);
         }
     } else {
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-            if (oj0 + j < g.Wo) __builtin_nontemporal_store(v[j], row + j);
+            if (oj0 + j < g.Wo) {
+                if constexpr (NT) __builtin_nontemporal_store(v[j], row + j);
+                else row[j] = v[j];
+            }
     }
 }
 
 // Write the m x m output block of (tile tc, output channel k), cropped to Ho x Wo.
-template <int MT>
+template <int MT, bool NT = true>
 __device__ __forceinline__ void store_block(float* __restrict__ y, const Geom& g,
                                             const TileCoord& tc, int k,
                                             const float (&o)[MT][MT], bool relu, bool vec_ok) {
 #pragma unroll
-    for (int i = 0; i < MT; ++i) store_row<MT>(y, g, tc, k, i, o[i], relu, vec_ok);
+    for (int i = 0; i < MT; ++i) store_row<MT, NT>(y, g, tc, k, i, o[i], relu, vec_ok);
 }
 
 // Store a lane's T transform-domain values into one (block, quad) group of the
-// U/V layout [T/4][64][4]: one 16-byte store per group of four positions.
-template <int T>
+// U/V layout [T/4][64][4]: one 16-byte store per group of four positions, the
+// wave writing whole 1 KiB runs.  NT: streaming stores (measured: faster for
+// the staged input transform, slower for the split path's).
+template <int T, bool NT>
 __device__ __forceinline__ void store_t4(float* __restrict__ blk, int lane, const float (&v)[T]) {
 #pragma unroll
     for (int g4 = 0; g4 < T / 4; ++g4)
-        *(float4*)(blk + ((size_t)g4 * 64 + lane) * 4) =
-            make_float4(v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
+        store_out<NT>(blk + ((size_t)g4 * 64 + lane) * 4, v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
 }
 
 // ------------------------------------------------------------------ filter
@@ -261,12 +273,17 @@ __global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, fl
 
 // ------------------------------------------------------------------ input
 // One wave per (16-tile block, 4-channel quad); neighbouring waves take
-// neighbouring tile blocks so their overlapping regions share cache lines.
+// neighbouring tile blocks so their overlapping regions share cache lines, and
+// each XCD takes one contiguous run of workgroups (workgroup b runs item
+// (b % 8) * per + b / 8), so those neighbours meet in the same L2.
 template <int MT>
-__global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, float* __restrict__ V, Geom g) {
+__global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, float* __restrict__ V, Geom g,
+                                               long nwg) {
     constexpr int A = MT + 2, T = A * A;
     const int lane = threadIdx.x & 63;
-    const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nwg) return;
+    const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (w >= (long)g.PB * g.CQ) return;
     const int cq = (int)(w / g.PB), pb = (int)(w % g.PB);
     const int cl = lane >> 4;
@@ -276,7 +293,7 @@ __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, floa
     load_region<MT>(rp, g, cq, cl, d);
     float v[T];
     input_tf<MT>(d, v);
-    store_t4<T>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, v);
+    store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, v);
 }
 
 // ------------------------------------------------------------------ GEMM
@@ -371,22 +388,36 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
 }
 
 // ------------------------------------------------------------------ output
-// One wave per (16-tile block, 16-filter block): each lane gathers the T
-// accumulators of its four (tile, output channel) pairs and writes four m x m
-// blocks.
+// A workgroup owns whole rows of tiles of one image (R rows of tw <= 64 tiles,
+// or a 64-tile piece of one row) for one 16-filter block: wave = filter quad,
+// lane = tile.  Each lane gathers the T values of its four (tile, filter) pairs
+// from the blocked M and writes four m x m blocks, so the workgroup writes, per
+// filter, output rows that together cover whole rows of y -- the pieces of a
+// cache line come from the same wave, moments apart, and merge in L2.
 template <int MT>
 __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, float* __restrict__ y, Geom g,
-                                                int relu, int vec_ok) {
+                                                int relu, int vec_ok, int R, int segs, int ipi, int nitems) {
     constexpr int T = (MT + 2) * (MT + 2);
-    const int lane = threadIdx.x & 63;
-    const long w = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= (long)g.PB * g.KB) return;
-    const int pb = (int)(w / g.KB), kb = (int)(w % g.KB);
-    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
-    const float* src = M + ((size_t)w * T) * 256 + lane * 4;
+    const int lane = threadIdx.x & 63, kq = threadIdx.x >> 6;
+    const int item = (int)(blockIdx.x % (unsigned)nitems), kb = (int)(blockIdx.x / (unsigned)nitems);
+    const int n = item / ipi, it = item - n * ipi;
+    TileCoord tc;
+    tc.n = n;
+    if (segs == 0) {                        // R whole rows of tw tiles
+        tc.ti = it * R + lane / g.tw;
+        tc.tj = lane % g.tw;
+        tc.valid = lane < R * g.tw && tc.ti < g.th;
+    } else {                                // piece it % segs of row it / segs
+        tc.ti = it / segs;
+        tc.tj = (it % segs) * 64 + lane;
+        tc.valid = tc.tj < g.tw;
+    }
+    const int p = tc.valid ? (n * g.th + tc.ti) * g.tw + tc.tj : 0;
+    // element (t, k, p) of M: lane 16*((k%16)/4) + p%16, slot k%4 of block (p/16, k/16, t)
+    const float* src = M + (((size_t)(p / 16) * g.KB + kb) * T) * 256 + (16 * kq + p % 16) * 4;
     f32x4 mv[T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) mv[t] = *(const f32x4*)(src + t * 256);
+    for (int t = 0; t < T; ++t) mv[t] = tc.valid ? *(const f32x4*)(src + t * 256) : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         float m1[T];
@@ -394,7 +425,7 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
         for (int t = 0; t < T; ++t) m1[t] = mv[t][r];
         float o[MT][MT];
         output_tf<MT>(m1, o);
-        store_block<MT>(y, g, tc, kb * 16 + 4 * (lane >> 4) + r, o, relu != 0, vec_ok != 0);
+        store_block<MT, false>(y, g, tc, kb * 16 + 4 * kq + r, o, relu != 0, vec_ok != 0);
     }
 }
 
@@ -934,7 +965,7 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
     }
     float v[T];
     input_tf<MT>(d, v);
-    store_t4<T>(Vb + ((size_t)tb * (ncq4 * 4) + cq) * T * 64, lane, v);
+    store_t4<T, false>(Vb + ((size_t)tb * (ncq4 * 4) + cq) * T * 64, lane, v);
 }
 
 // GEMMs + output transform from Vb.  A workgroup of 8 waves computes two tile
@@ -1269,9 +1300,9 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
                 if constexpr (MT == 4) {
-                    store_out(r + (size_t)i * g.Wo, o[i][0], o[i][1], o[i][2], o[i][3]);
+                    store_out<true>(r + (size_t)i * g.Wo, o[i][0], o[i][1], o[i][2], o[i][3]);
                 } else {
-                    store_out(r + (size_t)i * g.Wo, o[i][0], o[i][1]);
+                    store_out<true>(r + (size_t)i * g.Wo, o[i][0], o[i][1]);
                 }
             }
         } else {
@@ -1319,12 +1350,13 @@ hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int 
 }
 
 hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s) {
-    const long waves = (long)g.PB * g.CQ;
-    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
+    if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
     if (g.m == 2)
-        hipLaunchKernelGGL(k_input<2>, grid, block, 0, s, x, V, g);
+        hipLaunchKernelGGL(k_input<2>, grid, block, 0, s, x, V, g, nwg);
     else
-        hipLaunchKernelGGL(k_input<4>, grid, block, 0, s, x, V, g);
+        hipLaunchKernelGGL(k_input<4>, grid, block, 0, s, x, V, g, nwg);
     return hipGetLastError();
 }
 
@@ -1336,13 +1368,22 @@ hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const G
 }
 
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s) {
-    const long waves = (long)g.PB * g.KB;
-    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
     const int vec_ok = (g.Wo % g.m == 0) && aligned(y, 4 * g.m);
+    int R = 0, segs = 0, ipi;                      // items per image
+    if (g.tw <= 64) {
+        R = 64 / g.tw;
+        ipi = (g.th + R - 1) / R;
+    } else {
+        segs = (g.tw + 63) / 64;
+        ipi = g.th * segs;
+    }
+    const long nitems = (long)g.N * ipi, wgs = nitems * g.KB;
+    if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)wgs), block(256);
     if (g.m == 2)
-        hipLaunchKernelGGL(k_output<2>, grid, block, 0, s, M, y, g, (int)relu, vec_ok);
+        hipLaunchKernelGGL(k_output<2>, grid, block, 0, s, M, y, g, (int)relu, vec_ok, R, segs, ipi, (int)nitems);
     else
-        hipLaunchKernelGGL(k_output<4>, grid, block, 0, s, M, y, g, (int)relu, vec_ok);
+        hipLaunchKernelGGL(k_output<4>, grid, block, 0, s, M, y, g, (int)relu, vec_ok, R, segs, ipi, (int)nitems);
     return hipGetLastError();
 }
 

@@ -94,7 +94,11 @@ def test_batched_gemm(m, shape):
 
 @pytest.mark.parametrize("m", [2, 4])
 @pytest.mark.parametrize("relu", [False, True])
-@pytest.mark.parametrize("shape", [(1, 16, 20, 20, 1), (2, 33, 9, 13, 1), (1, 5, 57, 57, 1), (1, 1, 3, 3, 0)])
+# (N, K, H, W, pad); the kernel takes whole rows of tiles (several rows per
+# workgroup up to 64 tiles, a ragged last group) or 64-tile pieces of rows
+# wider than that (the last two shapes)
+@pytest.mark.parametrize("shape", [(1, 16, 20, 20, 1), (2, 33, 9, 13, 1), (1, 5, 57, 57, 1), (1, 1, 3, 3, 0),
+                                   (3, 18, 37, 26, 2), (2, 20, 10, 300, 1), (1, 7, 6, 515, 0)])
 def test_output_transform(m, relu, shape):
     N, K, H, W, pad = shape
     Ho, Wo, th, tw, P = h.geometry(N, H, W, pad, m)
