@@ -141,6 +141,16 @@ def pmc_rows(d: str):
     return rows
 
 
+def kernel_is(name: str, prefix: str) -> bool:
+    """Whether a profiler kernel name is of the given kind: template instances
+    carry their return type ("void wino::k_fused<...>(...)"), plain functions
+    do not ("wino::k_gemm(...)")."""
+    strip = lambda n: n[5:] if n.startswith("void ") else n
+    base = strip(prefix)
+    n = strip(name)
+    return n.startswith(base) and n[len(base):len(base) + 1] in ("<", "(")
+
+
 def pmc_summary(args):
     """Summarise a FETCH_SIZE run and a WRITE_SIZE run of this script."""
     from paper_1903_01521_amd import workloads as wl
@@ -153,13 +163,13 @@ def pmc_summary(args):
     for counter, d in (("FETCH_SIZE", args.pmc_summary[0]), ("WRITE_SIZE", args.pmc_summary[1])):
         rows = [r for r in pmc_rows(d) if r["Counter_Name"] == counter]
         # the calibration launches: torch's elementwise negation over COPY_BYTES
-        kern = [float(r["Counter_Value"]) for r in rows if r["Kernel_Name"].startswith(prefix)]
+        kern = [float(r["Counter_Value"]) for r in rows if kernel_is(r["Kernel_Name"], prefix)]
         copy = [float(r["Counter_Value"]) for r in rows
                 if "neg" in r["Kernel_Name"].lower() and int(r["Grid_Size"]) * 16 >= COPY_BYTES // 4]
         if not kern or not copy:
             raise SystemExit(f"{counter}: {len(kern)} {kind} dispatches, {len(copy)} copy dispatches in {d}")
         out[counter] = (float(np.mean(kern)), len(kern), float(np.median(copy)), len(copy),
-                        sorted(set(r["Kernel_Name"] for r in rows if r["Kernel_Name"].startswith(prefix))))
+                        sorted(set(r["Kernel_Name"] for r in rows if kernel_is(r["Kernel_Name"], prefix))))
     fk, fn_, fc, fcn, names = out["FETCH_SIZE"]
     wk, wn, wc, wcn, _ = out["WRITE_SIZE"]
     fscale = fc * 1024 / COPY_BYTES

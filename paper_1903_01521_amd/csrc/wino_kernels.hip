@@ -308,11 +308,19 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
                                               float* __restrict__ M, Geom g) {
     __shared__ float4 As[2][4][4][64];   // [buf][quad][k-block][lane] -> 4 positions
     __shared__ float4 Bs[2][4][4][64];   // [buf][quad][p-block][lane]
-    const int tg = blockIdx.y;           // positions 4*tg .. 4*tg+3
     const int T = g.T, TG = g.T / 4;
-    const int KB4 = (g.KB + 3) >> 2;
-    const int pb0 = (int)(blockIdx.x / KB4) * 4;
-    const int kb0 = (int)(blockIdx.x % KB4) * 4;
+    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
+    // Items (position group, p-tile, k-tile), k-tile fastest; each XCD runs one
+    // contiguous range of items (workgroup b takes item (b % 8) * per + b / 8),
+    // so the k-tiles that share a p-tile's V run together and V comes from HBM
+    // into that XCD's L2 once.
+    const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
+    const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nitems) return;
+    const int kb0 = (int)(item % KB4) * 4;
+    const long rest = item / KB4;
+    const int pb0 = (int)(rest % PB4) * 4;
+    const int tg = (int)(rest / PB4);     // positions 4*tg .. 4*tg+3
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wk = wave >> 1, wp = wave & 1;
     const int nchunks = (g.CQ + 3) >> 2;
@@ -1361,8 +1369,10 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
 }
 
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s) {
-    const long tiles = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4);
-    const dim3 grid((unsigned)tiles, (unsigned)(g.T / 4)), block(256);
+    const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
+    const long wgs = (nitems + 7) / 8 * 8;
+    if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)wgs), block(256);
     hipLaunchKernelGGL(k_gemm, grid, block, 0, s, U, V, M, g);
     return hipGetLastError();
 }
