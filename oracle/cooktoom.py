@@ -6,12 +6,14 @@ independently of anything here.
 
 Contents, each in the paper's notation where it has one (Sec. 2):
 
-* :func:`cook_toom` -- the exact rational matrices of F(m x m, 3 x 3): the output
+* :func:`cook_toom` -- the exact rational matrices of F(m x m, r x r): the output
   (inverse) transform A^T (the paper's Z^T), the filter transform G (its W) and
   the input transform B^T (its X^T), derived from interpolation points.  Only
   the F(2x2,3x3) input matrix is printed in the paper (Sec. 2.1.1); the rest
   follows from the construction below, and the m=2 signs are chosen so that
-  B^T equals the printed matrix.
+  B^T equals the printed matrix.  r = 3 is the method's filter size; r = 5 is
+  F(2x2,5x5) for the 5x5 layers of the paper's Table 2 (same region size, 6x6,
+  as F(4x4,3x3)).
 * :func:`winograd_conv_exact` -- Eq. 1 evaluated over the rationals, region by
   region, in the loop order of Listing 1 (per output channel, per output region,
   sum over the input channels in the transform domain, one inverse transform
@@ -25,8 +27,8 @@ Contents, each in the paper's notation where it has one (Sec. 2):
   pass combining rows, then the same pass combining columns.
 
 Transform-domain index: t = xi * alpha + nu for the (xi, nu) element of an
-alpha x alpha region, alpha = m + 2, T = alpha^2.  Tile index p = (n*th + ti)*tw
-+ tj with th = ceil(Ho/m), tw = ceil(Wo/m).  Tile (ti, tj) produces output rows
+alpha x alpha region, alpha = m + r - 1 (m + 2 for 3x3 filters), T = alpha^2.
+Tile index p = (n*th + ti)*tw + tj with th = ceil(Ho/m), tw = ceil(Wo/m).  Tile (ti, tj) produces output rows
 ti*m .. ti*m+m-1 and reads the input region starting at (ti*m - pad, tj*m - pad);
 values outside the input (padding and the ragged overhang) are zero, and outputs
 beyond Ho x Wo are discarded.
@@ -40,25 +42,24 @@ from math import prod
 import numpy as np
 
 R_FILTER = 3  # the method's filter size for this path (3x3 layers)
+SUPPORTED = ((2, 3), (4, 3), (2, 5))   # (m, r): F(2x2,3x3), F(4x4,3x3), F(2x2,5x5)
 
 
 # ----------------------------------------------------------------------------
 # Exact matrices
 # ----------------------------------------------------------------------------
 
-def interpolation_points(m: int) -> list[int]:
-    """Finite interpolation points of F(m, 3); the point at infinity is implied.
+def interpolation_points(m: int, r: int = R_FILTER) -> list[int]:
+    """Finite interpolation points of F(m, r); the point at infinity is implied.
 
     The paper names the Cook-Toom class but not its points.  Reading taken: the
-    smallest-magnitude integer points, {0, 1, -1} for m=2 and {0, 1, -1, 2, -2}
-    for m=4.  Any distinct points give an exact algorithm; the choice only changes
-    fp32 rounding.
+    smallest-magnitude integer points, alpha - 1 = m + r - 2 of them: {0, 1, -1}
+    for F(2,3) and {0, 1, -1, 2, -2} for F(4,3) and F(2,5).  Any distinct points
+    give an exact algorithm; the choice only changes fp32 rounding.
     """
-    if m == 2:
-        return [0, 1, -1]
-    if m == 4:
-        return [0, 1, -1, 2, -2]
-    raise ValueError("m must be 2 or 4")
+    if (m, r) not in SUPPORTED:
+        raise ValueError("(m, r) must be one of %s" % (SUPPORTED,))
+    return [0, 1, -1, 2, -2][:m + r - 2]
 
 
 def _solve_consistent(rows: list[list[Q]], rhs: list[Q]) -> list[Q]:
@@ -88,10 +89,9 @@ def _solve_consistent(rows: list[list[Q]], rhs: list[Q]) -> list[Q]:
 
 
 @lru_cache(maxsize=None)
-def _raw_cook_toom(m: int):
-    r = R_FILTER
+def _raw_cook_toom(m: int, r: int = R_FILTER):
     a = m + r - 1
-    pts = [Q(p) for p in interpolation_points(m)]
+    pts = [Q(p) for p in interpolation_points(m, r)]
     nf = a - 1  # finite points; the last row/column is the point at infinity
     # Output transform: evaluate the length-m output polynomial's basis at each
     # point; the infinity column picks the leading coefficient.
@@ -116,20 +116,21 @@ def _raw_cook_toom(m: int):
     return AT, G, BT
 
 
-def cook_toom(m: int):
-    """Exact (A^T, G, B^T) of F(m x m, 3 x 3) as lists of Fractions.
+def cook_toom(m: int, r: int = R_FILTER):
+    """Exact (A^T, G, B^T) of F(m x m, r x r) as lists of Fractions.
 
     Sign normalisation: scaling row j of G by s and row j of B^T by 1/s (or
     column j of A^T by s and row j of B^T by 1/s) leaves the algorithm exact.
-    For m=2 the paper prints B^T; the raw derivation differs from it by the sign
-    of rows 0 and 3, so row 0 is flipped through G and row 3 (the infinity row)
-    through A^T.  For m=4 nothing is printed and the raw derivation is kept.
+    For F(2,3) the paper prints B^T; the raw derivation differs from it by the
+    sign of rows 0 and 3, so row 0 is flipped through G and row 3 (the infinity
+    row) through A^T.  For F(4,3) and F(2,5) nothing is printed and the raw
+    derivation is kept (their B^T coincide: same points).
     """
-    AT, G, BT = _raw_cook_toom(m)
-    AT = [list(r) for r in AT]
-    G = [list(r) for r in G]
-    BT = [list(r) for r in BT]
-    if m == 2:
+    AT, G, BT = _raw_cook_toom(m, r)
+    AT = [list(row) for row in AT]
+    G = [list(row) for row in G]
+    BT = [list(row) for row in BT]
+    if (m, r) == (2, 3):
         G[0] = [-v for v in G[0]]
         BT[0] = [-v for v in BT[0]]
         for i in range(len(AT)):
@@ -138,9 +139,9 @@ def cook_toom(m: int):
     return AT, G, BT
 
 
-def matrices_f64(m: int):
+def matrices_f64(m: int, r: int = R_FILTER):
     """(A^T, G, B^T) as fp64 numpy arrays (G's thirds are rounded to fp64)."""
-    AT, G, BT = cook_toom(m)
+    AT, G, BT = cook_toom(m, r)
     f = lambda M: np.array([[float(v) for v in row] for row in M], dtype=np.float64)
     return f(AT), f(G), f(BT)
 
@@ -149,9 +150,9 @@ def matrices_f64(m: int):
 # Geometry
 # ----------------------------------------------------------------------------
 
-def geometry(N: int, H: int, W: int, pad: int, m: int):
-    """(Ho, Wo, th, tw, P) of a 3x3 stride-1 layer tiled into m x m output regions."""
-    Ho, Wo = H + 2 * pad - 2, W + 2 * pad - 2
+def geometry(N: int, H: int, W: int, pad: int, m: int, r: int = R_FILTER):
+    """(Ho, Wo, th, tw, P) of an r x r stride-1 layer tiled into m x m output regions."""
+    Ho, Wo = H + 2 * pad - (r - 1), W + 2 * pad - (r - 1)
     th, tw = -(-Ho // m), -(-Wo // m)
     return Ho, Wo, th, tw, N * th * tw
 
@@ -172,17 +173,18 @@ def _tr(A):
 def winograd_conv_exact(x, g, pad: int, m: int):
     """Region-wise multi-channel Winograd convolution over the rationals.
 
-    x: integer/rational array [N][C][H][W]; g: [K][C][3][3].  Returns a nested
-    list [N][K][Ho][Wo] of Fractions.  Pure Python: tiny inputs only.
+    x: integer/rational array [N][C][H][W]; g: [K][C][r][r] (r = 3, or 5 with
+    m = 2).  Returns a nested list [N][K][Ho][Wo] of Fractions.  Pure Python:
+    tiny inputs only.
     """
     x = np.asarray(x, dtype=object)
     g = np.asarray(g, dtype=object)
     N, C, H, W = x.shape
-    K = g.shape[0]
-    AT, G, BT = cook_toom(m)
+    K, r = g.shape[0], g.shape[2]
+    AT, G, BT = cook_toom(m, r)
     A, GT, B = _tr(AT), _tr(G), _tr(BT)
-    a = m + 2
-    Ho, Wo, th, tw, _ = geometry(N, H, W, pad, m)
+    a = m + r - 1
+    Ho, Wo, th, tw, _ = geometry(N, H, W, pad, m, r)
 
     def pix(n, c, u, v):
         if 0 <= u < H and 0 <= v < W:
@@ -190,7 +192,7 @@ def winograd_conv_exact(x, g, pad: int, m: int):
         return Q(0)
 
     # Offline weight transform W w W^T per (output channel, input channel).
-    U = [[_mm(_mm(G, [[Q(g[k, c, r, s]) for s in range(3)] for r in range(3)]), GT)
+    U = [[_mm(_mm(G, [[Q(g[k, c, u, v]) for v in range(r)] for u in range(r)]), GT)
           for c in range(C)] for k in range(K)]
     # Input transform X^T x X of every (image, channel, region).
     V = {}
@@ -226,22 +228,22 @@ def winograd_conv_exact(x, g, pad: int, m: int):
 # ----------------------------------------------------------------------------
 
 def filter_transform(g: np.ndarray, m: int) -> np.ndarray:
-    """U[t][c][k] = (G g[k,c] G^T)[xi, nu], t = xi*alpha + nu, in fp64."""
-    _, G, _ = matrices_f64(m)
+    """U[t][c][k] = (G g[k,c] G^T)[xi, nu], t = xi*alpha + nu, in fp64 (r from g)."""
     g = np.asarray(g, dtype=np.float64)
-    K, C = g.shape[:2]
-    a = m + 2
+    K, C, r = g.shape[:3]
+    _, G, _ = matrices_f64(m, r)
+    a = m + r - 1
     U = np.einsum("ar,kcrs,bs->abck", G, g, G)
     return np.ascontiguousarray(U.reshape(a * a, C, K))
 
 
-def extract_regions(x: np.ndarray, pad: int, m: int) -> np.ndarray:
+def extract_regions(x: np.ndarray, pad: int, m: int, r: int = R_FILTER) -> np.ndarray:
     """d[n, c, ti, tj, u, v] = zero-extended x[n, c, ti*m - pad + u, tj*m - pad + v]."""
     x = np.asarray(x)
     N, C, H, W = x.shape
-    a = m + 2
-    _, _, th, tw, _ = geometry(N, H, W, pad, m)
-    Hx, Wx = th * m + 2, tw * m + 2
+    a = m + r - 1
+    _, _, th, tw, _ = geometry(N, H, W, pad, m, r)
+    Hx, Wx = th * m + r - 1, tw * m + r - 1
     xe = np.zeros((N, C, Hx, Wx), dtype=x.dtype)
     h1, w1 = min(H, Hx - pad), min(W, Wx - pad)
     xe[:, :, pad:pad + h1, pad:pad + w1] = x[:, :, :h1, :w1]
@@ -252,10 +254,10 @@ def extract_regions(x: np.ndarray, pad: int, m: int) -> np.ndarray:
     return d
 
 
-def input_transform(x: np.ndarray, pad: int, m: int) -> np.ndarray:
+def input_transform(x: np.ndarray, pad: int, m: int, r: int = R_FILTER) -> np.ndarray:
     """V[t][c][p] = (B^T d_{n,c,ti,tj} B)[xi, nu] in fp64, p = (n*th+ti)*tw+tj."""
-    _, _, BT = matrices_f64(m)
-    d = extract_regions(np.asarray(x, dtype=np.float64), pad, m)
+    _, _, BT = matrices_f64(m, r)
+    d = extract_regions(np.asarray(x, dtype=np.float64), pad, m, r)
     N, C, th, tw, a, _ = d.shape
     Vr = np.einsum("au,nctjuv,bv->abcntj", BT, d, BT)
     return np.ascontiguousarray(Vr.reshape(a * a, C, N * th * tw))
@@ -266,11 +268,11 @@ def batched_gemm(U: np.ndarray, V: np.ndarray) -> np.ndarray:
     return np.matmul(np.transpose(U, (0, 2, 1)), V)
 
 
-def output_transform(M: np.ndarray, N: int, Ho: int, Wo: int, m: int) -> np.ndarray:
+def output_transform(M: np.ndarray, N: int, Ho: int, Wo: int, m: int, r: int = R_FILTER) -> np.ndarray:
     """y[n,k,ti*m+i,tj*m+j] = (A^T M_{k,p} A)[i, j], cropped to Ho x Wo, in fp64."""
-    AT, _, _ = matrices_f64(m)
+    AT, _, _ = matrices_f64(m, r)
     T, K, P = M.shape
-    a = m + 2
+    a = m + r - 1
     th, tw = -(-Ho // m), -(-Wo // m)
     Mr = np.asarray(M, dtype=np.float64).reshape(a, a, K, N, th, tw)
     # labels: t = ti, w = tj; result axes n, k, ti, i, tj, j -> rows ti*m+i, cols tj*m+j
@@ -282,10 +284,11 @@ def output_transform(M: np.ndarray, N: int, Ho: int, Wo: int, m: int) -> np.ndar
 def winograd_conv_f64(x: np.ndarray, g: np.ndarray, pad: int, m: int) -> np.ndarray:
     """The three stages composed in fp64 (weights transformed first, offline)."""
     N, C, H, W = np.asarray(x).shape
-    Ho, Wo, _, _, _ = geometry(N, H, W, pad, m)
+    r = np.asarray(g).shape[2]
+    Ho, Wo, _, _, _ = geometry(N, H, W, pad, m, r)
     U = filter_transform(g, m)
-    V = input_transform(x, pad, m)
-    return output_transform(batched_gemm(U, V), N, Ho, Wo, m)
+    V = input_transform(x, pad, m, r)
+    return output_transform(batched_gemm(U, V), N, Ho, Wo, m, r)
 
 
 def input_transform_m2_paper_order_f32(x: np.ndarray, pad: int) -> np.ndarray:

@@ -44,22 +44,25 @@ def _load():
             dp = ctypes.POINTER(ctypes.c_double)
             lib.oracle_conv2d_f64.argtypes = [dp, dp, dp] + [ctypes.c_int] * 7
             lib.oracle_conv2d_f64.restype = ctypes.c_int
+            lib.oracle_conv2d_rs_f64.argtypes = [dp, dp, dp] + [ctypes.c_int] * 9
+            lib.oracle_conv2d_rs_f64.restype = ctypes.c_int
             lib.oracle_num_threads.argtypes = []
             lib.oracle_num_threads.restype = ctypes.c_int
             _lib = lib
     return _lib
 
 
-def out_hw(H: int, W: int, pad: int) -> tuple[int, int]:
-    """Output size of a 3x3 stride-1 layer with symmetric zero padding."""
-    return H + 2 * pad - 2, W + 2 * pad - 2
+def out_hw(H: int, W: int, pad: int, R: int = 3, S: int = 3) -> tuple[int, int]:
+    """Output size of an R x S stride-1 layer with symmetric zero padding."""
+    return H + 2 * pad - (R - 1), W + 2 * pad - (S - 1)
 
 
 def conv2d(x: np.ndarray, g: np.ndarray, pad: int, absval: bool = False) -> np.ndarray:
-    """y = x (*) g, 3x3 stride-1 cross-correlation with zero padding, in fp64.
+    """y = x (*) g, stride-1 cross-correlation with zero padding, in fp64.
 
     x: [N, C, H, W] (any real dtype; widened exactly to fp64)
-    g: [K, C, 3, 3]
+    g: [K, C, R, S]: 3 x 3 (the method's filters), or any other size (the 5 x 5
+       layers of the paper's Table 2)
     Returns y: [N, K, Ho, Wo] fp64.  absval=True evaluates the same sums on |x|
     and |g| (the elementwise magnitude bound used to scale rounding error).
     """
@@ -67,18 +70,23 @@ def conv2d(x: np.ndarray, g: np.ndarray, pad: int, absval: bool = False) -> np.n
     g = np.ascontiguousarray(g, dtype=np.float64)
     N, C, H, W = x.shape
     K, C2, R, S = g.shape
-    if C2 != C or (R, S) != (3, 3):
-        raise ValueError("filter must be [K, C, 3, 3] with C matching x")
-    Ho, Wo = out_hw(H, W, pad)
+    if C2 != C or R < 1 or S < 1:
+        raise ValueError("filter must be [K, C, R, S] with C matching x")
+    Ho, Wo = out_hw(H, W, pad, R, S)
     if pad < 0 or Ho < 1 or Wo < 1:
         raise ValueError("invalid padding / size")
     y = np.empty((N, K, Ho, Wo), dtype=np.float64)
     dp = ctypes.POINTER(ctypes.c_double)
-    rc = _load().oracle_conv2d_f64(x.ctypes.data_as(dp), g.ctypes.data_as(dp),
-                                   y.ctypes.data_as(dp), N, C, H, W, K, pad,
-                                   1 if absval else 0)
+    if (R, S) == (3, 3):
+        rc = _load().oracle_conv2d_f64(x.ctypes.data_as(dp), g.ctypes.data_as(dp),
+                                       y.ctypes.data_as(dp), N, C, H, W, K, pad,
+                                       1 if absval else 0)
+    else:
+        rc = _load().oracle_conv2d_rs_f64(x.ctypes.data_as(dp), g.ctypes.data_as(dp),
+                                          y.ctypes.data_as(dp), N, C, H, W, K, R, S, pad,
+                                          1 if absval else 0)
     if rc != 0:
-        raise RuntimeError("oracle_conv2d_f64 rejected its arguments")
+        raise RuntimeError("oracle direct convolution rejected its arguments")
     return y
 
 

@@ -71,6 +71,59 @@ int oracle_conv2d_f64(const double* x, const double* g, double* y,
     return 0;
 }
 
+/*
+ * The same definition for an R x S filter (the paper's layers also have 5x5
+ * filters, Table 2): g is [K][C][R][S],
+ *
+ *   y[n,k,i,j] = sum_{c<C} sum_{r<R} sum_{s<S} xt[n,c,i+r-pad,j+s-pad] * g[k,c,r,s]
+ *
+ * for 0 <= i < Ho = H+2pad-(R-1), 0 <= j < Wo = W+2pad-(S-1).  Same loops, same
+ * rules; kept apart from the 3x3 function above so that function stays exactly
+ * as pinned.
+ */
+int oracle_conv2d_rs_f64(const double* x, const double* g, double* y,
+                         int N, int C, int H, int W, int K, int R, int S, int pad, int absval)
+{
+    if (!x || !g || !y || N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || R <= 0 || S <= 0 || pad < 0)
+        return -1;
+    const long Ho = (long)H + 2L * pad - (R - 1);
+    const long Wo = (long)W + 2L * pad - (S - 1);
+    if (Ho < 1 || Wo < 1)
+        return -1;
+
+    long nk;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (nk = 0; nk < (long)N * K; ++nk) {
+        const long n = nk / K;
+        const long k = nk % K;
+        double* yo = y + ((n * K + k) * Ho) * Wo;
+        for (long p = 0; p < Ho * Wo; ++p)
+            yo[p] = 0.0;
+        for (long c = 0; c < C; ++c) {
+            const double* xi = x + ((n * C + c) * (long)H) * W;
+            const double* gk = g + ((k * C + c) * (long)R) * S;
+            for (long r = 0; r < R; ++r) {
+                for (long s = 0; s < S; ++s) {
+                    double w = gk[r * S + s];
+                    if (absval) w = fabs(w);
+                    for (long i = 0; i < Ho; ++i) {
+                        const long u = i + r - pad;
+                        if (u < 0 || u >= H) continue;       /* zero padding: row outside */
+                        for (long j = 0; j < Wo; ++j) {
+                            const long v = j + s - pad;
+                            if (v < 0 || v >= W) continue;   /* zero padding: column outside */
+                            double a = xi[u * W + v];
+                            if (absval) a = fabs(a);
+                            yo[i * Wo + j] += a * w;
+                        }
+                    }
+                }
+            }
+        }
+    }
+    return 0;
+}
+
 /* Number of OpenMP threads the oracle's parallel loop will use. */
 int oracle_num_threads(void)
 {

@@ -52,27 +52,44 @@ def test_printed_row_sequence_is_bt():
     assert rows == [[int(v) for v in r] for r in BT]
 
 
-@pytest.mark.parametrize("m", [2, 4])
-def test_bilinear_identity_1d(m):
-    # F(m, 3) computes y[i] = sum_k g[k] d[i+k] for every g, d: check on all basis pairs.
-    AT, G, BT = ct.cook_toom(m)
-    a = m + 2
-    for kk in range(3):
+@pytest.mark.parametrize("m,r", [(2, 3), (4, 3), (2, 5)])
+def test_bilinear_identity_1d(m, r):
+    # F(m, r) computes y[i] = sum_k g[k] d[i+k] for every g, d: check on all basis pairs.
+    AT, G, BT = ct.cook_toom(m, r)
+    a = m + r - 1
+    for kk in range(r):
         for aa in range(a):
             for i in range(m):
                 s = sum((AT[i][j] * G[j][kk] * BT[j][aa] for j in range(a)), Q(0))
-                assert s == (1 if aa == i + kk else 0), (m, i, kk, aa, s)
+                assert s == (1 if aa == i + kk else 0), (m, r, i, kk, aa, s)
 
 
-@pytest.mark.parametrize("m", [2, 4])
-def test_matrix_shapes_and_points(m):
-    AT, G, BT = ct.cook_toom(m)
-    a = m + 2
-    assert len(AT) == m and all(len(r) == a for r in AT)
-    assert len(G) == a and all(len(r) == 3 for r in G)
-    assert len(BT) == a and all(len(r) == a for r in BT)
+@pytest.mark.parametrize("m,r", [(2, 3), (4, 3), (2, 5)])
+def test_matrix_shapes_and_points(m, r):
+    AT, G, BT = ct.cook_toom(m, r)
+    a = m + r - 1
+    assert len(AT) == m and all(len(row) == a for row in AT)
+    assert len(G) == a and all(len(row) == r for row in G)
+    assert len(BT) == a and all(len(row) == a for row in BT)
     # A^T and B^T are integer matrices (the fractions sit in G, applied offline).
-    assert all(v.denominator == 1 for r in AT + BT for v in r)
+    assert all(v.denominator == 1 for row in AT + BT for v in row)
+
+
+def test_f2x2_5x5_shares_the_input_transform_of_f4x4_3x3():
+    # Both have alpha = 6 and the points {0, +-1, +-2, inf}: B^T depends only on
+    # the points, so the 5x5 variant reuses the 6x6 input transform.
+    assert ct.cook_toom(2, 5)[2] == ct.cook_toom(4, 3)[2]
+    # ... while A^T keeps the first two rows of F(4,3)'s except the point at
+    # infinity, which picks the leading output coefficient (row m - 1 = 1).
+    AT5, AT3 = ct.cook_toom(2, 5)[0], ct.cook_toom(4, 3)[0]
+    assert [row[:5] for row in AT5] == [row[:5] for row in AT3[:2]]
+    assert [row[5] for row in AT5] == [0, 1]
+
+
+def test_unsupported_pairs_are_rejected():
+    for m, r in [(3, 3), (4, 5), (2, 7)]:
+        with pytest.raises(ValueError):
+            ct.cook_toom(m, r)
 
 
 # Fig. 2's example: a 3 x 6 x 6 input, four filters, F(2x2,3x3) -> 2x2 regions of
@@ -86,12 +103,21 @@ EXACT_CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", EXACT_CASES)
-def test_listing1_over_rationals_equals_direct(case):
+# F(2x2,5x5): valid, padded (pad 2 keeps the size), ragged and one-pixel cases.
+EXACT_CASES_5 = [
+    (1, 2, 6, 6, 2, 0, 2),
+    (1, 2, 7, 9, 3, 2, 2),
+    (2, 1, 5, 8, 2, 1, 2),
+    (1, 3, 1, 1, 2, 2, 2),
+]
+
+
+@pytest.mark.parametrize("case,r", [(c, 3) for c in EXACT_CASES] + [(c, 5) for c in EXACT_CASES_5])
+def test_listing1_over_rationals_equals_direct(case, r):
     N, C, H, W, K, pad, m = case
-    rng = np.random.default_rng(sum(case))
+    rng = np.random.default_rng(sum(case) + r)
     x = rng.integers(-6, 7, (N, C, H, W))
-    g = rng.integers(-6, 7, (K, C, 3, 3))
+    g = rng.integers(-6, 7, (K, C, r, r))
     yq = ct.winograd_conv_exact(x, g, pad, m)
     yd = direct.conv2d(x.astype(np.float64), g.astype(np.float64), pad)
     assert np.array(yq, dtype=object).shape == yd.shape
@@ -99,14 +125,16 @@ def test_listing1_over_rationals_equals_direct(case):
     assert np.array_equal(np.array(yq, dtype=np.float64), yd)
 
 
-@pytest.mark.parametrize("m", [2, 4])
+@pytest.mark.parametrize("m,r", [(2, 3), (4, 3), (2, 5)])
 @pytest.mark.parametrize("shape", [(1, 3, 6, 6, 4, 0), (2, 5, 9, 7, 6, 1), (1, 4, 57, 57, 3, 1),
-                                   (3, 2, 1, 1, 2, 1), (1, 1, 3, 3, 1, 0)])
-def test_fp64_stages_compose_to_direct(m, shape):
+                                   (3, 2, 1, 1, 2, 1), (1, 1, 5, 5, 1, 0)])
+def test_fp64_stages_compose_to_direct(m, r, shape):
     N, C, H, W, K, pad = shape
-    rng = np.random.default_rng(N * 100 + C + H)
+    if r == 5:
+        pad += 1                     # keep Ho, Wo >= 1 for the one-pixel shape
+    rng = np.random.default_rng(N * 100 + C + H + r)
     x = rng.standard_normal((N, C, H, W))
-    g = rng.standard_normal((K, C, 3, 3))
+    g = rng.standard_normal((K, C, r, r))
     yw = ct.winograd_conv_f64(x, g, pad, m)
     yd = direct.conv2d(x, g, pad)
     bound = direct.conv2d(x, g, pad, absval=True)
@@ -170,3 +198,23 @@ def test_multiplication_reduction(m, ratio):
     direct_flops = 2 * N * K * C * 9 * Ho * Wo
     gemm_flops = 2 * a * a * P * C * K
     assert direct_flops / gemm_flops == ratio
+
+
+def test_stage_layouts_5x5():
+    N, C, H, W, K, pad, m, r = 2, 3, 10, 9, 5, 2, 2, 5
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((K, C, r, r))
+    Ho, Wo, th, tw, P = ct.geometry(N, H, W, pad, m, r)
+    assert (Ho, Wo) == (H, W)                     # pad 2 keeps the size of a 5x5 layer
+    U = ct.filter_transform(g, m)
+    V = ct.input_transform(x, pad, m, r)
+    assert U.shape == (36, C, K) and V.shape == (36, C, P)
+    _, G, BT = ct.matrices_f64(m, r)
+    k, c, xi, nu = 4, 1, 3, 5
+    assert np.isclose(U[xi * 6 + nu, c, k], (G @ g[k, c] @ G.T)[xi, nu], rtol=1e-15, atol=1e-15)
+    n, ti, tj = 1, 3, 2
+    p = (n * th + ti) * tw + tj
+    xe = np.pad(x[n, c], ((pad, 20), (pad, 20)))
+    d = xe[ti * m:ti * m + 6, tj * m:tj * m + 6]
+    assert np.isclose(V[xi * 6 + nu, c, p], (BT @ d @ BT.T)[xi, nu], rtol=1e-14, atol=1e-14)

@@ -3,11 +3,17 @@ import numpy as np
 import pytest
 
 import pins_direct
+import pins_direct_rs
 from oracle import direct
 
 
 @pytest.mark.parametrize("check", pins_direct.ALL_CHECKS, ids=lambda f: f.__name__)
 def test_pin(check):
+    check(direct.conv2d)
+
+
+@pytest.mark.parametrize("check", pins_direct_rs.ALL_CHECKS, ids=lambda f: f.__name__)
+def test_pin_rs(check):
     check(direct.conv2d)
 
 
@@ -27,3 +33,5 @@ def test_rejects_bad_shapes():
         direct.conv2d(x, np.zeros((1, 3, 3, 3)), 1)      # channel mismatch
     with pytest.raises(ValueError):
         direct.conv2d(np.zeros((1, 1, 1, 1)), np.zeros((1, 1, 3, 3)), 0)   # Ho < 1
+    with pytest.raises(ValueError):
+        direct.conv2d(np.zeros((1, 1, 4, 4)), np.zeros((1, 1, 5, 5)), 0)   # Ho < 1 (5x5)
