@@ -66,18 +66,18 @@ def sources_hash() -> str:
 
 def layer_numbers(N, L):
     """Sizes and algorithmic work of one layer (m x m tiles, alpha = m+2)."""
-    Ho, Wo = L.H + 2 * L.pad - 2, L.W + 2 * L.pad - 2
+    Ho, Wo = L.H + 2 * L.pad - (L.r - 1), L.W + 2 * L.pad - (L.r - 1)
     th, tw = -(-Ho // L.m), -(-Wo // L.m)
     P = N * th * tw
-    T = (L.m + 2) ** 2
+    T = (L.m + L.r - 1) ** 2
     f = dict(Ho=Ho, Wo=Wo, P=P, T=T)
-    f["direct_flops"] = 2 * N * L.K * L.C * 9 * Ho * Wo
+    f["direct_flops"] = 2 * N * L.K * L.C * L.r * L.r * Ho * Wo
     f["gemm_flops"] = 2 * T * P * L.C * L.K
     x_b, y_b, u_b = 4 * N * L.C * L.H * L.W, 4 * N * L.K * Ho * Wo, 4 * T * L.C * L.K
     v_b, m_b = 4 * T * P * L.C, 4 * T * P * L.K
     # minimum HBM bytes per kernel launch (what the method must move, padding excluded)
     f["bytes"] = {
-        "filter": 4 * L.K * L.C * 9 + u_b,
+        "filter": 4 * L.K * L.C * L.r * L.r + u_b,
         "fused": x_b + u_b + y_b,
         "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
@@ -286,15 +286,18 @@ def main():
     H, W = w.first.H, w.first.W
     for L, f in zip(w.layers, nums):
         assert (L.H, L.W) == (H, W)
-        Us.append(torch.empty(B.wino_filter_bytes(L.C, L.K, L.m) // 4, dtype=torch.float32, device=dev))
+        Us.append(torch.empty(B.wino_filter_bytes_r(L.C, L.K, L.m, L.r) // 4, dtype=torch.float32, device=dev))
         ys.append(torch.empty((N, L.K, f["Ho"], f["Wo"]), dtype=torch.float32, device=dev))
-        wsb = B.wino_workspace_bytes(N, L.C, L.H, L.W, L.K, L.pad, L.m, flags)
+        wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
         wss.append((torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev), wsb))
-        if staged:
-            Vs.append(torch.empty(B.wino_input_tf_bytes(N, L.C, L.H, L.W, L.pad, L.m) // 4,
+        if staged or L.r != 3:
+            Vs.append(torch.empty(B.wino_input_tf_bytes_r(N, L.C, L.H, L.W, L.pad, L.m, L.r) // 4,
                                   dtype=torch.float32, device=dev))
-            Ms.append(torch.empty(B.wino_gemm_out_bytes(N, L.K, L.H, L.W, L.pad, L.m) // 4,
+            Ms.append(torch.empty(B.wino_gemm_out_bytes_r(N, L.K, L.H, L.W, L.pad, L.m, L.r) // 4,
                                   dtype=torch.float32, device=dev))
+        else:
+            Vs.append(None)
+            Ms.append(None)
         H, W = f["Ho"], f["Wo"]
         if L.pool:
             pools.append(torch.empty((N, L.K, H // 2, W // 2), dtype=torch.float32, device=dev))
@@ -309,21 +312,21 @@ def main():
         for i, L in enumerate(w.layers):
             relu = B.WINO_FLAG_RELU if L.relu else 0
             out.append((f"L{i}.filter", i, "filter",
-                        (lambda sp, i=i, L=L: B.wino_filter_transform(hg[i], Us[i], L.C, L.K, L.m, sp))))
-            if staged:
-                out.append((f"L{i}.input", i, "input", (lambda sp, i=i, L=L, a=a: B.wino_input_transform(
-                    a, Vs[i], N, L.C, L.H, L.W, L.pad, L.m, sp))))
-                out.append((f"L{i}.gemm", i, "gemm", (lambda sp, i=i, L=L: B.wino_batched_gemm(
-                    Us[i], Vs[i], Ms[i], N, L.C, L.H, L.W, L.K, L.pad, L.m, sp))))
-                out.append((f"L{i}.output", i, "output", (lambda sp, i=i, L=L, relu=relu: B.wino_output_transform(
-                    Ms[i], ys[i], N, L.K, L.H, L.W, L.pad, L.m, relu, sp))))
+                        (lambda sp, i=i, L=L: B.wino_filter_transform_r(hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
+            if staged or L.r != 3:         # 5x5 layers run the three stages
+                out.append((f"L{i}.input", i, "input", (lambda sp, i=i, L=L, a=a: B.wino_input_transform_r(
+                    a, Vs[i], N, L.C, L.H, L.W, L.pad, L.m, L.r, sp))))
+                out.append((f"L{i}.gemm", i, "gemm", (lambda sp, i=i, L=L: B.wino_batched_gemm_r(
+                    Us[i], Vs[i], Ms[i], N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, sp))))
+                out.append((f"L{i}.output", i, "output", (lambda sp, i=i, L=L, relu=relu: B.wino_output_transform_r(
+                    Ms[i], ys[i], N, L.K, L.H, L.W, L.pad, L.m, L.r, relu, sp))))
             else:
                 ws, wsb = wss[i]
                 algo = flags & B.WINO_ALGO_MASK
                 lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4)
                 out.append((f"L{i}.conv", i, "lowc" if lowc else "fused", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
-                                                       B.wino_conv2d(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
-                                                                     L.pad, L.m, flags | relu,
+                                                       B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
+                                                                       L.pad, L.m, L.r, flags | relu,
                                                                      ws if wsb else None, wsb, sp))))
             a = ys[i]
             if L.pool:
@@ -511,7 +514,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": name, "N": N, "layers": len(w.layers),
                    "C": w.first.C, "K": w.first.K, "H": w.first.H, "W": w.first.W,
-                   "m": w.first.m, "pad": w.first.pad, "flags": hex(flags),
+                   "m": w.first.m, "r": w.first.r, "pad": w.first.pad, "flags": hex(flags),
                    "launch": "eager" if graph is None else "hip_graph", "parallelism": "none"},
         "roofline": roof,
         "per_launch_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, per_launch)},

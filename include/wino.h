@@ -161,6 +161,36 @@ int wino_batched_gemm(const float* U, const float* V, float* M,
 int wino_output_transform(const float* M, float* y, int N, int K, int H, int W,
                           int pad, int m, unsigned flags, void* stream);
 
+/* ---- 5x5 filters: F(2x2,5x5) ----------------------------------------------
+ * The same method for r x r filters (Eq. 1 with a 5x5 filter; the paper's
+ * Table 2 benchmarks 5x5 layers with its F(2x2,5x5,6x6) variant).  Supported
+ * (m, r): (2, 3), (4, 3) -- identical to the 3x3 calls above -- and (2, 5).
+ * For r = 5: alpha = m + r - 1 = 6, T = 36, Ho = H + 2*pad - 4, Wo = W + 2*pad - 4;
+ * points {0, 1, -1, 2, -2, inf} (the same B^T as F(4x4,3x3)):
+ *   G   = [1/4 0 0 0 0; -1/6 -1/6 -1/6 -1/6 -1/6; -1/6 1/6 -1/6 1/6 -1/6;
+ *          1/24 1/12 1/6 1/3 2/3; 1/24 -1/12 1/6 -1/3 2/3; 0 0 0 0 1]
+ *   A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 1]
+ *   y[n,k,i,j] = sum_c sum_{r,s<5} x[n,c,i+r-pad,j+s-pad] * g[k,c,r,s].
+ * Layouts of U, V and M are the ones above with T = 36.  g is [K][C][5][5].
+ * Only the three-stage algorithm runs 5x5 layers: flags may be WINO_ALGO_AUTO
+ * or WINO_ALGO_STAGED (plus WINO_FLAG_RELU); the workspace is always required.
+ * Errors as for the 3x3 calls; UNSUPPORTED for other (m, r) or algorithms. */
+size_t wino_filter_bytes_r(int C, int K, int m, int r);
+int wino_filter_transform_r(const float* g, float* U, int C, int K, int m, int r, void* stream);
+size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsigned flags);
+int wino_conv2d_r(const float* x, const float* U, float* y,
+                  int N, int C, int H, int W, int K, int pad, int m, int r,
+                  unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
+/* The three stages alone for r x r filters (the calls above with r = 3). */
+size_t wino_input_tf_bytes_r(int N, int C, int H, int W, int pad, int m, int r);
+size_t wino_gemm_out_bytes_r(int N, int K, int H, int W, int pad, int m, int r);
+int wino_input_transform_r(const float* x, float* V, int N, int C, int H, int W,
+                           int pad, int m, int r, void* stream);
+int wino_batched_gemm_r(const float* U, const float* V, float* M,
+                        int N, int C, int H, int W, int K, int pad, int m, int r, void* stream);
+int wino_output_transform_r(const float* M, float* y, int N, int K, int H, int W,
+                            int pad, int m, int r, unsigned flags, void* stream);
+
 /* Glue between the blocks of a VGG-style stack (not part of the method):
  * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);

@@ -63,6 +63,15 @@ _SIGS = {
     "wino_batched_gemm": ([_vp, _vp, _vp] + [_c_int] * 7 + [_vp], _c_int),
     "wino_output_transform": ([_vp, _vp] + [_c_int] * 6 + [_c_uint, _vp], _c_int),
     "wino_maxpool2x2": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
+    "wino_filter_bytes_r": ([_c_int] * 4, _c_size),
+    "wino_filter_transform_r": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
+    "wino_workspace_bytes_r": ([_c_int] * 8 + [_c_uint], _c_size),
+    "wino_conv2d_r": ([_vp, _vp, _vp] + [_c_int] * 8 + [_c_uint, _vp, _c_size, _vp], _c_int),
+    "wino_input_tf_bytes_r": ([_c_int] * 7, _c_size),
+    "wino_gemm_out_bytes_r": ([_c_int] * 7, _c_size),
+    "wino_input_transform_r": ([_vp, _vp] + [_c_int] * 7 + [_vp], _c_int),
+    "wino_batched_gemm_r": ([_vp, _vp, _vp] + [_c_int] * 8 + [_vp], _c_int),
+    "wino_output_transform_r": ([_vp, _vp] + [_c_int] * 7 + [_c_uint, _vp], _c_int),
 }
 
 
@@ -169,6 +178,44 @@ def wino_output_transform(M, y, N, K, H, W, pad, m, flags=0, stream=None) -> int
 
 def wino_maxpool2x2(x, y, N, C, H, W, stream=None) -> int:
     return lib().wino_maxpool2x2(_fptr(x), _fptr(y), N, C, H, W, _stream(stream))
+
+
+def wino_filter_bytes_r(C, K, m, r) -> int:
+    return lib().wino_filter_bytes_r(C, K, m, r)
+
+
+def wino_filter_transform_r(g, U, C, K, m, r, stream=None) -> int:
+    return lib().wino_filter_transform_r(_fptr(g), _fptr(U), C, K, m, r, _stream(stream))
+
+
+def wino_workspace_bytes_r(N, C, H, W, K, pad, m, r, flags=0) -> int:
+    return lib().wino_workspace_bytes_r(N, C, H, W, K, pad, m, r, flags)
+
+
+def wino_conv2d_r(x, U, y, N, C, H, W, K, pad, m, r, flags=0, workspace=None, workspace_bytes=0,
+                  stream=None) -> int:
+    return lib().wino_conv2d_r(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, r, flags,
+                               _ptr(workspace), workspace_bytes, _stream(stream))
+
+
+def wino_input_tf_bytes_r(N, C, H, W, pad, m, r) -> int:
+    return lib().wino_input_tf_bytes_r(N, C, H, W, pad, m, r)
+
+
+def wino_gemm_out_bytes_r(N, K, H, W, pad, m, r) -> int:
+    return lib().wino_gemm_out_bytes_r(N, K, H, W, pad, m, r)
+
+
+def wino_input_transform_r(x, V, N, C, H, W, pad, m, r, stream=None) -> int:
+    return lib().wino_input_transform_r(_fptr(x), _fptr(V), N, C, H, W, pad, m, r, _stream(stream))
+
+
+def wino_batched_gemm_r(U, V, M, N, C, H, W, K, pad, m, r, stream=None) -> int:
+    return lib().wino_batched_gemm_r(_fptr(U), _fptr(V), _fptr(M), N, C, H, W, K, pad, m, r, _stream(stream))
+
+
+def wino_output_transform_r(M, y, N, K, H, W, pad, m, r, flags=0, stream=None) -> int:
+    return lib().wino_output_transform_r(_fptr(M), _fptr(y), N, K, H, W, pad, m, r, flags, _stream(stream))
 
 
 def check(status: int, where: str = "wino") -> None:

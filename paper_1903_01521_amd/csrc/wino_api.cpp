@@ -23,26 +23,33 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
     return *out <= kMaxElems;
 }
 
-int make_geom(int N, int C, int H, int W, int K, int pad, int m, Geom* g) {
+// Supported (m, r): F(2x2,3x3), F(4x4,3x3), F(2x2,5x5).
+bool supported(int m, int r) { return (r == 3 && (m == 2 || m == 4)) || (r == 5 && m == 2); }
+
+int make_geom_r(int N, int C, int H, int W, int K, int pad, int m, int r, Geom* g) {
     if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || pad < 0) return WINO_ERR_INVALID_ARG;
-    if (m != 2 && m != 4) return WINO_ERR_UNSUPPORTED;
-    const int64_t Ho = (int64_t)H + 2 * (int64_t)pad - 2;
-    const int64_t Wo = (int64_t)W + 2 * (int64_t)pad - 2;
+    if (!supported(m, r)) return WINO_ERR_UNSUPPORTED;
+    const int64_t Ho = (int64_t)H + 2 * (int64_t)pad - (r - 1);
+    const int64_t Wo = (int64_t)W + 2 * (int64_t)pad - (r - 1);
     if (Ho < 1 || Wo < 1 || Ho > INT32_MAX / 2 || Wo > INT32_MAX / 2) return WINO_ERR_INVALID_ARG;
     const int64_t th = (Ho + m - 1) / m, tw = (Wo + m - 1) / m;
     int64_t t1, P, xin, xout;
     if (!mul_ok(th, tw, &t1) || !mul_ok(t1, N, &P) || P > kMaxTiles) return WINO_ERR_INVALID_ARG;
     if (!mul_ok((int64_t)N * C, (int64_t)H * W, &xin)) return WINO_ERR_INVALID_ARG;
     if (!mul_ok((int64_t)N * K, Ho * Wo, &xout)) return WINO_ERR_INVALID_ARG;
-    const int64_t A = m + 2, T = A * A;
+    const int64_t A = m + r - 1, T = A * A;
     const int64_t CQ = (C + 3) / 4, KB = (K + 15) / 16, PB = (P + 15) / 16;
     int64_t v, mm;
     if (!mul_ok(PB * CQ, T * 64, &v) || !mul_ok(PB * KB, T * 256, &mm)) return WINO_ERR_INVALID_ARG;
     g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
     g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
-    g->A = (int)A; g->T = (int)T;
+    g->A = (int)A; g->T = (int)T; g->r = r;
     g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
     return WINO_OK;
+}
+
+int make_geom(int N, int C, int H, int W, int K, int pad, int m, Geom* g) {
+    return make_geom_r(N, C, H, W, K, pad, m, 3, g);
 }
 
 bool overlap(const void* a, size_t na, const void* b, size_t nb) {
@@ -117,6 +124,16 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
         return WINO_ERR_UNSUPPORTED;
     if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
+    // 5x5 filters run the three stages (input transform, GEMMs, output
+    // transform); the one-kernel variants are written for 3x3 regions.
+    if (g.r != 3) {
+        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
+            return WINO_ERR_UNSUPPORTED;
+        p->algo = WINO_ALGO_STAGED;
+        p->automatic = algo == WINO_ALGO_AUTO;
+        p->cfg = FusedCfg{1, 16};
+        return WINO_OK;
+    }
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
     p->algo = algo == WINO_ALGO_AUTO ? WINO_ALGO_FUSED : algo;
@@ -169,57 +186,76 @@ const char* wino_status_string(int status) {
 
 int wino_version(void) { return 100; }
 
-size_t wino_filter_bytes(int C, int K, int m) {
-    if (C <= 0 || K <= 0 || (m != 2 && m != 4)) return 0;
+size_t wino_filter_bytes_r(int C, int K, int m, int r) {
+    if (C <= 0 || K <= 0 || !supported(m, r)) return 0;
     int64_t e;
-    if (!mul_ok((int64_t)(C + 3) / 4 * 4, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, (m + 2) * (m + 2), &e))
+    const int a = m + r - 1;
+    if (!mul_ok((int64_t)(C + 3) / 4 * 4, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, a * a, &e))
         return 0;
     return (size_t)e * sizeof(float);
 }
 
-size_t wino_input_tf_bytes(int N, int C, int H, int W, int pad, int m) {
+size_t wino_filter_bytes(int C, int K, int m) { return wino_filter_bytes_r(C, K, m, 3); }
+
+size_t wino_input_tf_bytes_r(int N, int C, int H, int W, int pad, int m, int r) {
     Geom g;
-    if (make_geom(N, C, H, W, 1, pad, m, &g) != WINO_OK) return 0;
+    if (make_geom_r(N, C, H, W, 1, pad, m, r, &g) != WINO_OK) return 0;
     return v_elems(g) * sizeof(float);
 }
 
-size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m) {
+size_t wino_gemm_out_bytes_r(int N, int K, int H, int W, int pad, int m, int r) {
     Geom g;
-    if (make_geom(N, 1, H, W, K, pad, m, &g) != WINO_OK) return 0;
+    if (make_geom_r(N, 1, H, W, K, pad, m, r, &g) != WINO_OK) return 0;
     return m_elems(g) * sizeof(float);
 }
 
-size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags) {
+size_t wino_input_tf_bytes(int N, int C, int H, int W, int pad, int m) {
+    return wino_input_tf_bytes_r(N, C, H, W, pad, m, 3);
+}
+
+size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m) {
+    return wino_gemm_out_bytes_r(N, K, H, W, pad, m, 3);
+}
+
+size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsigned flags) {
     Geom g;
     Plan p;
-    if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
+    if (make_geom_r(N, C, H, W, K, pad, m, r, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
     if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
     if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
 
-int wino_filter_transform(const float* gw, float* U, int C, int K, int m, void* stream) {
-    if (!gw || !U || C <= 0 || K <= 0) return WINO_ERR_INVALID_ARG;
-    if (m != 2 && m != 4) return WINO_ERR_UNSUPPORTED;
-    const size_t ub = wino_filter_bytes(C, K, m);
-    if (ub == 0) return WINO_ERR_INVALID_ARG;
-    if (overlap(gw, (size_t)K * C * 9 * sizeof(float), U, ub)) return WINO_ERR_INVALID_ARG;
-    return hip_status(launch_filter_transform(gw, U, C, K, m, (hipStream_t)stream));
+size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags) {
+    return wino_workspace_bytes_r(N, C, H, W, K, pad, m, 3, flags);
 }
 
-int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
-                unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
+int wino_filter_transform_r(const float* gw, float* U, int C, int K, int m, int r, void* stream) {
+    if (!gw || !U || C <= 0 || K <= 0) return WINO_ERR_INVALID_ARG;
+    if (!supported(m, r)) return WINO_ERR_UNSUPPORTED;
+    const size_t ub = wino_filter_bytes_r(C, K, m, r);
+    if (ub == 0) return WINO_ERR_INVALID_ARG;
+    if (overlap(gw, (size_t)K * C * r * r * sizeof(float), U, ub)) return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_filter_transform(gw, U, C, K, m, r, (hipStream_t)stream));
+}
+
+int wino_filter_transform(const float* gw, float* U, int C, int K, int m, void* stream) {
+    return wino_filter_transform_r(gw, U, C, K, m, 3, stream);
+}
+
+int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
+                  int r, unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
     if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
     Geom g;
-    int st = make_geom(N, C, H, W, K, pad, m, &g);
+    int st = make_geom_r(N, C, H, W, K, pad, m, r, &g);
     if (st != WINO_OK) return st;
     Plan p;
     st = make_plan(g, flags, &p);
     if (st != WINO_OK) return st;
     const size_t xb = (size_t)N * C * H * W * sizeof(float);
     const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
-    const size_t ub = wino_filter_bytes(C, K, m);
+    const size_t ub = wino_filter_bytes_r(C, K, m, r);
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
     const bool relu = (flags & WINO_FLAG_RELU) != 0;
     hipStream_t s = (hipStream_t)stream;
@@ -251,38 +287,58 @@ int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, i
     return hip_status(launch_output_transform(M, y, g, relu, s));
 }
 
-int wino_input_transform(const float* x, float* V, int N, int C, int H, int W, int pad, int m, void* stream) {
+int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
+                unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
+    return wino_conv2d_r(x, U, y, N, C, H, W, K, pad, m, 3, flags, workspace, workspace_bytes, stream);
+}
+
+int wino_input_transform_r(const float* x, float* V, int N, int C, int H, int W, int pad, int m, int r,
+                           void* stream) {
     if (!x || !V) return WINO_ERR_INVALID_ARG;
     Geom g;
-    const int st = make_geom(N, C, H, W, 1, pad, m, &g);
+    const int st = make_geom_r(N, C, H, W, 1, pad, m, r, &g);
     if (st != WINO_OK) return st;
     if (overlap(x, (size_t)N * C * H * W * sizeof(float), V, v_elems(g) * sizeof(float)))
         return WINO_ERR_INVALID_ARG;
     return hip_status(launch_input_transform(x, V, g, (hipStream_t)stream));
 }
 
-int wino_batched_gemm(const float* U, const float* V, float* M, int N, int C, int H, int W, int K, int pad, int m,
-                      void* stream) {
+int wino_input_transform(const float* x, float* V, int N, int C, int H, int W, int pad, int m, void* stream) {
+    return wino_input_transform_r(x, V, N, C, H, W, pad, m, 3, stream);
+}
+
+int wino_batched_gemm_r(const float* U, const float* V, float* M, int N, int C, int H, int W, int K, int pad,
+                        int m, int r, void* stream) {
     if (!U || !V || !M) return WINO_ERR_INVALID_ARG;
     Geom g;
-    const int st = make_geom(N, C, H, W, K, pad, m, &g);
+    const int st = make_geom_r(N, C, H, W, K, pad, m, r, &g);
     if (st != WINO_OK) return st;
     const size_t mb = m_elems(g) * sizeof(float);
-    if (overlap(M, mb, U, wino_filter_bytes(C, K, m)) || overlap(M, mb, V, v_elems(g) * sizeof(float)))
+    if (overlap(M, mb, U, wino_filter_bytes_r(C, K, m, r)) || overlap(M, mb, V, v_elems(g) * sizeof(float)))
         return WINO_ERR_INVALID_ARG;
     return hip_status(launch_batched_gemm(U, V, M, g, (hipStream_t)stream));
 }
 
-int wino_output_transform(const float* M, float* y, int N, int K, int H, int W, int pad, int m, unsigned flags,
-                          void* stream) {
+int wino_batched_gemm(const float* U, const float* V, float* M, int N, int C, int H, int W, int K, int pad, int m,
+                      void* stream) {
+    return wino_batched_gemm_r(U, V, M, N, C, H, W, K, pad, m, 3, stream);
+}
+
+int wino_output_transform_r(const float* M, float* y, int N, int K, int H, int W, int pad, int m, int r,
+                            unsigned flags, void* stream) {
     if (!M || !y) return WINO_ERR_INVALID_ARG;
     if (flags & ~WINO_FLAG_RELU) return WINO_ERR_UNSUPPORTED;
     Geom g;
-    const int st = make_geom(N, 1, H, W, K, pad, m, &g);
+    const int st = make_geom_r(N, 1, H, W, K, pad, m, r, &g);
     if (st != WINO_OK) return st;
     if (overlap(M, m_elems(g) * sizeof(float), y, (size_t)N * K * g.Ho * g.Wo * sizeof(float)))
         return WINO_ERR_INVALID_ARG;
     return hip_status(launch_output_transform(M, y, g, (flags & WINO_FLAG_RELU) != 0, (hipStream_t)stream));
+}
+
+int wino_output_transform(const float* M, float* y, int N, int K, int H, int W, int pad, int m, unsigned flags,
+                          void* stream) {
+    return wino_output_transform_r(M, y, N, K, H, W, pad, m, 3, flags, stream);
 }
 
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream) {

@@ -7,13 +7,15 @@
 
 namespace wino {
 
-// Geometry of a 3x3 stride-1 layer tiled into m x m output regions, and the
-// blocked transform-domain extents (see the layout notes in wino.h).
+// Geometry of an r x r (3x3, or 5x5 with m = 2) stride-1 layer tiled into
+// m x m output regions, and the blocked transform-domain extents (see the
+// layout notes in wino.h).
 struct Geom {
     int N, C, H, W, K, pad, m;
     int Ho, Wo, th, tw;
     int P;          // tiles, N*th*tw
-    int A, T;       // alpha = m + 2, T = alpha^2
+    int A, T;       // alpha = m + r - 1, T = alpha^2
+    int r;          // filter side
     int CQ, KB, PB; // 4-channel quads, 16-filter blocks, 16-tile blocks
 };
 
@@ -34,11 +36,11 @@ struct FusedTiling {
     int bw;         // split path: tile-block width (16 or 4)
 };
 
-size_t filter_elems(int C, int K, int m);                // T*Cp*Kp
+size_t filter_elems(int C, int K, int m, int r);         // T*Cp*Kp
 size_t v_elems(const Geom& g);                           // PB*CQ*T*64
 size_t m_elems(const Geom& g);                           // PB*KB*T*256
 
-hipError_t launch_filter_transform(const float* g, float* U, int C, int K, int m, hipStream_t s);
+hipError_t launch_filter_transform(const float* g, float* U, int C, int K, int m, int r, hipStream_t s);
 hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s);
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s);
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s);

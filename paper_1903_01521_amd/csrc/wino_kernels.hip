@@ -75,21 +75,21 @@ __device__ __forceinline__ f32x4 u_load(__amdgpu_buffer_rsrc_t r, uint32_t lane_
     return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)group_off, 0));
 }
 
-template <int MT>
+// Regions of side A (MT + 2 for 3x3 filters, MT + 4 for 5x5) stepping by MT.
+template <int MT, int A = MT + 2>
 struct RegionPlan {
     __amdgpu_buffer_rsrc_t rsrc;     // wave-uniform
-    uint32_t row[MT + 2];            // lane's channel-plane + row byte offset, or kInvalid
-    uint32_t col[MT + 2];            // column byte offset, or kInvalid
+    uint32_t row[A];                 // lane's channel-plane + row byte offset, or kInvalid
+    uint32_t col[A];                 // column byte offset, or kInvalid
     uint32_t plane_bytes;            // H*W*4: step between channels (soffset units)
 };
 
 // p0 = first tile of the wave's 16-tile block (wave-uniform); tc = lane's tile;
 // cl = lane's channel within a quad.
-template <int MT>
-__device__ __forceinline__ RegionPlan<MT> make_region_plan(const float* __restrict__ x, const Geom& g,
-                                                           int p0, const TileCoord& tc, int cl) {
-    constexpr int A = MT + 2;
-    RegionPlan<MT> rp;
+template <int MT, int A = MT + 2>
+__device__ __forceinline__ RegionPlan<MT, A> make_region_plan(const float* __restrict__ x, const Geom& g,
+                                                              int p0, const TileCoord& tc, int cl) {
+    RegionPlan<MT, A> rp;
     const int n0 = __builtin_amdgcn_readfirstlane(min(p0, g.P - 1) / (g.th * g.tw));
     const size_t img = (size_t)g.C * g.H * g.W;
     const size_t left = ((size_t)g.N - n0) * img * 4;
@@ -113,10 +113,9 @@ __device__ __forceinline__ RegionPlan<MT> make_region_plan(const float* __restri
 
 // d = the region of channel quad cq for this lane (channel cq*4 + cl), zero
 // outside the image, past the last channel, and for tiles past P.
-template <int MT>
-__device__ __forceinline__ void load_region(const RegionPlan<MT>& rp, const Geom& g, int cq, int cl,
-                                            float (&d)[MT + 2][MT + 2]) {
-    constexpr int A = MT + 2;
+template <int MT, int A = MT + 2>
+__device__ __forceinline__ void load_region(const RegionPlan<MT, A>& rp, const Geom& g, int cq, int cl,
+                                            float (&d)[A][A]) {
     const uint32_t chan = (cq * 4 + cl < g.C) ? 0u : kInvalid;
     const int soff = __builtin_amdgcn_readfirstlane(cq * 4 * (int)rp.plane_bytes);
 #pragma unroll
@@ -203,18 +202,18 @@ constexpr long kFilterAllPairs = 256;
 
 // The 4-position group tg (wave-uniform) of a lane's filter transform: a
 // branch per group, each computing only its own positions.
-template <int MT, int... G>
-__device__ __forceinline__ float4 filter_pick(int tg, const float (&g)[3][3], std::integer_sequence<int, G...>) {
+template <int MT, int R, int... G>
+__device__ __forceinline__ float4 filter_pick(int tg, const float (&g)[R][R], std::integer_sequence<int, G...>) {
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-    ((tg == G ? (void)(o = filter_tf4<MT, 4 * G>(g)) : (void)0), ...);
+    ((tg == G ? (void)(o = filter_tf4<MT, 4 * G, R>(g)) : (void)0), ...);
     return o;
 }
 
 // All position groups of a lane's filter transform, group G to U + G*256.
-template <int MT, int... G>
-__device__ __forceinline__ void filter_all(const float (&g)[3][3], float* __restrict__ u,
+template <int MT, int R, int... G>
+__device__ __forceinline__ void filter_all(const float (&g)[R][R], float* __restrict__ u,
                                            std::integer_sequence<int, G...>) {
-    ((*(float4*)(u + G * 256) = filter_tf4<MT, 4 * G>(g)), ...);
+    ((*(float4*)(u + G * 256) = filter_tf4<MT, 4 * G, R>(g)), ...);
 }
 
 // One wave per (16-filter block, 4-channel quad) -- or, for layers with few
@@ -223,51 +222,51 @@ __device__ __forceinline__ void filter_all(const float (&g)[3][3], float* __rest
 // (c%4)*16 + k%16, so each group the wave writes is one contiguous 1 KiB run of
 // U with a 16-byte store per lane.  Four waves per workgroup.  With STAGE (one
 // wave per pair and CQ % 4 == 0) the workgroup's four quads are 16 consecutive
-// channels of the same 16 filters: it reads their 16 x 576 contiguous bytes of
-// g with coalesced loads into LDS first.
-template <int MT, bool ALL, bool STAGE>
+// channels of the same 16 filters: it reads their 16 runs of 16*R*R contiguous
+// floats of g with coalesced loads into LDS first.  R: filter side (3 or 5).
+template <int MT, bool ALL, bool STAGE, int R = 3>
 __global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, float* __restrict__ U,
                                                 int C, int K, int CQ, long nw) {
-    constexpr int T = (MT + 2) * (MT + 2), TG = T / 4;
+    constexpr int A = MT + R - 1, T = A * A, TG = T / 4, RR = R * R, RUN = 16 * RR;
     static_assert(ALL || !STAGE, "staging needs one wave per pair");
     const int lane = threadIdx.x & 63;
     const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    float gg[3][3];
+    float gg[R][R];
     long pair;
     if constexpr (STAGE) {
-        __shared__ float gs[16 * 144];                // [filter][16 channels x 9]
+        __shared__ float gs[16 * RUN];                // [filter][16 channels x R*R]
         const long p0 = (long)blockIdx.x * 4;         // nw % 4 == 0: every wave is valid
         const int kb = (int)(p0 / CQ), c0 = (int)(p0 % CQ) * 4;
 #pragma unroll
-        for (int i = 0; i < 9; ++i) {
-            const int e = (int)threadIdx.x + 256 * i, row = e / 144, off = e - row * 144;
-            const int k = kb * 16 + row, c = c0 + off / 9;
-            gs[e] = (k < K && c < C) ? gw[((size_t)k * C + c0) * 9 + off] : 0.0f;
+        for (int i = 0; i < RR; ++i) {
+            const int e = (int)threadIdx.x + 256 * i, row = e / RUN, off = e - row * RUN;
+            const int k = kb * 16 + row, c = c0 + off / RR;
+            gs[e] = (k < K && c < C) ? gw[((size_t)k * C + c0) * RR + off] : 0.0f;
         }
         __syncthreads();
         pair = w;
-        const float* src = gs + (lane & 15) * 144 + ((int)(w - p0) * 4 + (lane >> 4)) * 9;
+        const float* src = gs + (lane & 15) * RUN + ((int)(w - p0) * 4 + (lane >> 4)) * RR;
 #pragma unroll
-        for (int r = 0; r < 3; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int s = 0; s < 3; ++s) gg[r][s] = src[r * 3 + s];
+            for (int s = 0; s < R; ++s) gg[r][s] = src[r * R + s];
     } else {
         if (w >= nw) return;
         pair = ALL ? w : w / TG;                      // kb * CQ + cq
         const int kb = (int)(pair / CQ), cq = (int)(pair % CQ);
         const int k = kb * 16 + (lane & 15), c = cq * 4 + (lane >> 4);
         const bool ok = k < K && c < C;
-        const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c : 0)) * 9;
+        const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c : 0)) * RR;
 #pragma unroll
-        for (int r = 0; r < 3; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int s = 0; s < 3; ++s) gg[r][s] = ok ? src[r * 3 + s] : 0.0f;
+            for (int s = 0; s < R; ++s) gg[r][s] = ok ? src[r * R + s] : 0.0f;
     }
     if constexpr (ALL) {
-        filter_all<MT>(gg, U + ((size_t)pair * TG * 64 + lane) * 4, std::make_integer_sequence<int, TG>{});
+        filter_all<MT, R>(gg, U + ((size_t)pair * TG * 64 + lane) * 4, std::make_integer_sequence<int, TG>{});
     } else {
         *(float4*)(U + ((size_t)w * 64 + lane) * 4) =
-            filter_pick<MT>((int)(w % TG), gg, std::make_integer_sequence<int, TG>{});
+            filter_pick<MT, R>((int)(w % TG), gg, std::make_integer_sequence<int, TG>{});
     }
 }
 
@@ -276,10 +275,10 @@ __global__ __launch_bounds__(256) void k_filter(const float* __restrict__ gw, fl
 // neighbouring tile blocks so their overlapping regions share cache lines, and
 // each XCD takes one contiguous run of workgroups (workgroup b runs item
 // (b % 8) * per + b / 8), so those neighbours meet in the same L2.
-template <int MT>
+template <int MT, int R = 3>
 __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, float* __restrict__ V, Geom g,
                                                long nwg) {
-    constexpr int A = MT + 2, T = A * A;
+    constexpr int A = MT + R - 1, T = A * A;
     const int lane = threadIdx.x & 63;
     const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (item >= nwg) return;
@@ -288,11 +287,11 @@ __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, floa
     const int cq = (int)(w / g.PB), pb = (int)(w % g.PB);
     const int cl = lane >> 4;
     const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
-    const RegionPlan<MT> rp = make_region_plan<MT>(x, g, pb * 16, tc, cl);
+    const RegionPlan<MT, A> rp = make_region_plan<MT, A>(x, g, pb * 16, tc, cl);
     float d[A][A];
-    load_region<MT>(rp, g, cq, cl, d);
+    load_region<MT, A>(rp, g, cq, cl, d);
     float v[T];
-    input_tf<MT>(d, v);
+    input_tf<A - 2>(d, v);                 // B^T depends only on the region side (the points)
     store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, v);
 }
 
@@ -402,10 +401,10 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
 // from the blocked M and writes four m x m blocks, so the workgroup writes, per
 // filter, output rows that together cover whole rows of y -- the pieces of a
 // cache line come from the same wave, moments apart, and merge in L2.
-template <int MT>
+template <int MT, int RF = 3>
 __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, float* __restrict__ y, Geom g,
                                                 int relu, int vec_ok, int R, int segs, int ipi, int nitems) {
-    constexpr int T = (MT + 2) * (MT + 2);
+    constexpr int T = (MT + RF - 1) * (MT + RF - 1);
     const int lane = threadIdx.x & 63, kq = threadIdx.x >> 6;
     const int item = (int)(blockIdx.x % (unsigned)nitems), kb = (int)(blockIdx.x / (unsigned)nitems);
     const int n = item / ipi, it = item - n * ipi;
@@ -432,7 +431,7 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 #pragma unroll
         for (int t = 0; t < T; ++t) m1[t] = mv[t][r];
         float o[MT][MT];
-        output_tf<MT>(m1, o);
+        output_tf<MT, RF>(m1, o);
         store_block<MT, false>(y, g, tc, kb * 16 + 4 * kq + r, o, relu != 0, vec_ok != 0);
     }
 }
@@ -1336,22 +1335,24 @@ __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x,
 
 static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int m, hipStream_t s) {
-    const int CQ = (C + 3) / 4, KB = (K + 15) / 16, TG = (m + 2) * (m + 2) / 4;
+hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int m, int r, hipStream_t s) {
+    const int CQ = (C + 3) / 4, KB = (K + 15) / 16, TG = (m + r - 1) * (m + r - 1) / 4;
     const long pairs = (long)KB * CQ;
     const bool all = pairs >= kFilterAllPairs;     // enough waves without splitting the positions
     const bool stage = all && CQ % 4 == 0;         // a workgroup's quads share their filters
     const long waves = all ? pairs : pairs * TG;
     if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
-#define WINO_FILTER_LAUNCH(MT)                                                                        \
-    if (stage) hipLaunchKernelGGL((k_filter<MT, true, true>), grid, block, 0, s, gw, U, C, K, CQ, waves); \
-    else if (all) hipLaunchKernelGGL((k_filter<MT, true, false>), grid, block, 0, s, gw, U, C, K, CQ, waves); \
-    else hipLaunchKernelGGL((k_filter<MT, false, false>), grid, block, 0, s, gw, U, C, K, CQ, waves);
-    if (m == 2) {
-        WINO_FILTER_LAUNCH(2)
+#define WINO_FILTER_LAUNCH(MT, R)                                                                         \
+    if (stage) hipLaunchKernelGGL((k_filter<MT, true, true, R>), grid, block, 0, s, gw, U, C, K, CQ, waves);  \
+    else if (all) hipLaunchKernelGGL((k_filter<MT, true, false, R>), grid, block, 0, s, gw, U, C, K, CQ, waves); \
+    else hipLaunchKernelGGL((k_filter<MT, false, false, R>), grid, block, 0, s, gw, U, C, K, CQ, waves);
+    if (r == 5) {
+        WINO_FILTER_LAUNCH(2, 5)
+    } else if (m == 2) {
+        WINO_FILTER_LAUNCH(2, 3)
     } else {
-        WINO_FILTER_LAUNCH(4)
+        WINO_FILTER_LAUNCH(4, 3)
     }
 #undef WINO_FILTER_LAUNCH
     return hipGetLastError();
@@ -1361,7 +1362,9 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
     const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
-    if (g.m == 2)
+    if (g.r == 5)
+        hipLaunchKernelGGL((k_input<2, 5>), grid, block, 0, s, x, V, g, nwg);
+    else if (g.m == 2)
         hipLaunchKernelGGL(k_input<2>, grid, block, 0, s, x, V, g, nwg);
     else
         hipLaunchKernelGGL(k_input<4>, grid, block, 0, s, x, V, g, nwg);
@@ -1390,7 +1393,10 @@ hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool
     const long nitems = (long)g.N * ipi, wgs = nitems * g.KB;
     if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)wgs), block(256);
-    if (g.m == 2)
+    if (g.r == 5)
+        hipLaunchKernelGGL((k_output<2, 5>), grid, block, 0, s, M, y, g, (int)relu, vec_ok, R, segs, ipi,
+                           (int)nitems);
+    else if (g.m == 2)
         hipLaunchKernelGGL(k_output<2>, grid, block, 0, s, M, y, g, (int)relu, vec_ok, R, segs, ipi, (int)nitems);
     else
         hipLaunchKernelGGL(k_output<4>, grid, block, 0, s, M, y, g, (int)relu, vec_ok, R, segs, ipi, (int)nitems);
@@ -1541,8 +1547,8 @@ hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int 
     return hipGetLastError();
 }
 
-size_t filter_elems(int C, int K, int m) {
-    const size_t T = (size_t)(m + 2) * (m + 2);
+size_t filter_elems(int C, int K, int m, int r) {
+    const size_t T = (size_t)(m + r - 1) * (m + r - 1);
     return T * (size_t)((C + 3) / 4) * 4 * (size_t)((K + 15) / 16) * 16;
 }
 size_t v_elems(const Geom& g) { return (size_t)g.PB * g.CQ * g.T * 64; }

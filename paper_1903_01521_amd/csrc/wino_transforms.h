@@ -1,4 +1,4 @@
-// Device-side Cook-Toom transforms for F(2x2,3x3) and F(4x4,3x3).
+// Device-side Cook-Toom transforms for F(2x2,3x3), F(4x4,3x3) and F(2x2,5x5).
 //
 // The matrices (Lavin's names; the paper writes X^T for B^T, W for G and Z^T
 // for A^T, Eq. 1):
@@ -16,7 +16,12 @@
 //            1/24 1/12 1/6; 1/24 -1/12 1/6; 0 0 1]
 //     A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 0; 0 1 1 4 4 0; 0 1 -1 8 -8 1]
 //
-// Both compute correlation: y[i] = sum_k g[k] d[i+k].  Every 2-D transform is
+//   F(2x2,5x5), alpha = 6, the same points as m = 4 (so the same B^T):
+//     G   = [1/4 0 0 0 0; -1/6 -1/6 -1/6 -1/6 -1/6; -1/6 1/6 -1/6 1/6 -1/6;
+//            1/24 1/12 1/6 1/3 2/3; 1/24 -1/12 1/6 -1/3 2/3; 0 0 0 0 1]
+//     A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 1]
+//
+// All compute correlation: y[i] = sum_k g[k] d[i+k].  Every 2-D transform is
 // the 1-D transform applied along rows (left factor), then along columns
 // (right factor): B^T d B = ((B^T d)) then .B, and likewise A^T M A.  For m = 2
 // this is the two-pass order the paper prints, so each value is exactly two
@@ -58,6 +63,11 @@ __device__ __forceinline__ void at_1d(const float (&a)[4], float (&r)[2]) {
     r[1] = a[1] - a[2] - a[3];
 }
 
+__device__ __forceinline__ void at_1d(const float (&a)[6], float (&r)[2]) {      // F(2,5)
+    r[0] = (a[0] + (a[1] + a[2])) + (a[3] + a[4]);            // a0 + a1 + a2 + a3 + a4
+    r[1] = __builtin_fmaf(2.0f, a[3] - a[4], a[1] - a[2]) + a[5];   // a1 - a2 + 2a3 - 2a4 + a5
+}
+
 __device__ __forceinline__ void at_1d(const float (&a)[6], float (&r)[4]) {
     const float s12 = a[1] + a[2], d12 = a[1] - a[2];
     const float s34 = a[3] + a[4], d34 = a[3] - a[4];
@@ -91,10 +101,10 @@ __device__ __forceinline__ void input_tf(const float (&d)[MT + 2][MT + 2], float
     }
 }
 
-// o[i][j] = (A^T M A)[i][j], M[xi][nu] = mv[xi*A + nu]
-template <int MT>
-__device__ __forceinline__ void output_tf(const float (&mv)[(MT + 2) * (MT + 2)], float (&o)[MT][MT]) {
-    constexpr int A = MT + 2;
+// o[i][j] = (A^T M A)[i][j], M[xi][nu] = mv[xi*A + nu]; A = MT + R - 1
+template <int MT, int R = 3>
+__device__ __forceinline__ void output_tf(const float (&mv)[(MT + R - 1) * (MT + R - 1)], float (&o)[MT][MT]) {
+    constexpr int A = MT + R - 1;
     float s[MT][A];
 #pragma unroll
     for (int j = 0; j < A; ++j) {          // along rows: column j of A^T M
@@ -207,11 +217,12 @@ __device__ __forceinline__ void output_tf_rows(const float (&mv)[RN * (MT + 2)],
 
 // ---------------------------------------------------------------- filter, fp64
 // U = G g G^T evaluated in fp64 with an integer-scaled G (S*G has integer
-// entries: S = 2 for m = 2, S = 24 for m = 4): the two small-integer products
-// are exact or nearly so in fp64, the scale 1/S^2 is applied once as a
-// multiplication (relative error <= 2^-52), and the result is rounded to fp32.
-// Integer-valued results (g a multiple of S^2) come out exact.
-template <int MT> struct GScaled;
+// entries: S = 2 for F(2,3), S = 24 for F(4,3) and F(2,5)): the two
+// small-integer products are exact or nearly so in fp64, the scale 1/S^2 is
+// applied once as a multiplication (relative error <= 2^-52), and the result
+// is rounded to fp32.  Integer-valued results (g a multiple of S^2) come out
+// exact.
+template <int MT, int R = 3> struct GScaled;
 template <> struct GScaled<2> {
     static constexpr double INV_S2 = 1.0 / 4.0;
     __device__ static void rows(const double (&a)[3], double (&r)[4]) {
@@ -232,27 +243,44 @@ template <> struct GScaled<4> {
         r[5] = 24.0 * a[2];
     }
 };
+template <> struct GScaled<2, 5> {
+    static constexpr double INV_S2 = 1.0 / 576.0;
+    __device__ static void rows(const double (&a)[5], double (&r)[6]) {
+        const double se = a[0] + a[2] + a[4], so = a[1] + a[3];
+        r[0] = 6.0 * a[0];
+        r[1] = -4.0 * (se + so);
+        r[2] = -4.0 * (se - so);
+        const double ev = a[0] + 4.0 * a[2] + 16.0 * a[4], od = 2.0 * a[1] + 8.0 * a[3];
+        r[3] = ev + od;
+        r[4] = ev - od;
+        r[5] = 24.0 * a[4];
+    }
+};
 
 // Positions T0 .. T0+3 of U = G g G^T (t = xi*A + nu), fp64 inside, each
 // rounded once to fp32.  Only the rows of (S G) g that these positions need are
 // live after unrolling; the rest is dead code.
-template <int MT, int T0>
-__device__ __forceinline__ float4 filter_tf4(const float (&g)[3][3]) {
-    constexpr int A = MT + 2;
-    double cs[3][A];                       // (S G) g, column c, every row
+template <int MT, int T0, int R = 3>
+__device__ __forceinline__ float4 filter_tf4(const float (&g)[R][R]) {
+    constexpr int A = MT + R - 1;
+    double cs[R][A];                       // (S G) g, column c, every row
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
-        const double col[3] = {(double)g[0][c], (double)g[1][c], (double)g[2][c]};
-        GScaled<MT>::rows(col, cs[c]);
+    for (int c = 0; c < R; ++c) {
+        double col[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) col[k] = (double)g[k][c];
+        GScaled<MT, R>::rows(col, cs[c]);
     }
     float o[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {          // ((S G) g) (S G)^T at row xi, column nu
         const int t = T0 + e, xi = t / A, nu = t % A;
-        const double row[3] = {cs[0][xi], cs[1][xi], cs[2][xi]};
+        double row[R];
+#pragma unroll
+        for (int c = 0; c < R; ++c) row[c] = cs[c][xi];
         double r[A];
-        GScaled<MT>::rows(row, r);
-        o[e] = (float)(r[nu] * GScaled<MT>::INV_S2);
+        GScaled<MT, R>::rows(row, r);
+        o[e] = (float)(r[nu] * GScaled<MT, R>::INV_S2);
     }
     return make_float4(o[0], o[1], o[2], o[3]);
 }

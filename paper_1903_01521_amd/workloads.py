@@ -4,11 +4,12 @@ This module holds no arithmetic of the method.  It is the one module that both
 the HIP path's tests/benchmark and the oracle-side checks draw their inputs
 from, so that both see identical fp32 arrays.
 
-Shapes stand in for the 3x3 layers of the CNNs the paper evaluates (Sec. 3:
-VGG-16/19, GoogleNet, Inception-v3, SqueezeNet); no dataset images or trained
-weights are used.  Recipe: ``numpy.random.default_rng(seed)`` (PCG64), the input
-tensor is drawn first, then each layer's weights in layer order, all in fp64 and
-then rounded to fp32.  Weights are He-normal, i.e. N(0, variance 2/(9*C_in)).
+Shapes stand in for the 3x3 (and 5x5) layers of the CNNs the paper evaluates
+(Sec. 3: VGG-16/19, GoogleNet, Inception-v3, SqueezeNet); no dataset images or
+trained weights are used.  Recipe: ``numpy.random.default_rng(seed)`` (PCG64),
+the input tensor is drawn first, then each layer's weights in layer order, all
+in fp64 and then rounded to fp32.  Weights are He-normal, i.e. N(0, variance
+2/(r*r*C_in)) for r x r filters.
 """
 from __future__ import annotations
 
@@ -27,6 +28,7 @@ class Layer:
     pad: int = 1
     relu: bool = False        # ReLU applied to this layer's output
     pool: bool = False        # 2x2/2 max-pool applied after (the ReLU of) this layer
+    r: int = 3                # filter side (3, or 5 with m = 2)
 
 
 @dataclass(frozen=True)
@@ -78,6 +80,8 @@ WORKLOADS = {w.name: w for w in [
              x_dist="uniform", note="low-C first layer"),
     Workload("f4_lowc_n1_c3_k64_224x224", 1, (Layer(3, 64, 224, 224, m=4),),
              x_dist="uniform", note="low-C first layer, batch 1"),
+    Workload("f2r5_n32_c48_k64_35x35", 32, (Layer(48, 64, 35, 35, m=2, pad=2, r=5),),
+             note="5x5 layer shaped like Inception-v3's 5x5 branch, F(2x2,5x5)"),
 ]}
 
 # The single-layer workload the benchmark times by default.
@@ -85,7 +89,7 @@ DEFAULT_BENCH = "f4_n1_c64_k64_112x112"
 
 
 def generate(w: Workload, seed: int = 0, N: int | None = None):
-    """Draw (x, [g_layer, ...]) as fp32 arrays: x [N,C,H,W], g [K,C,3,3]."""
+    """Draw (x, [g_layer, ...]) as fp32 arrays: x [N,C,H,W], g [K,C,r,r]."""
     rng = np.random.default_rng(seed)
     L0 = w.first
     n = w.N if N is None else N
@@ -99,8 +103,8 @@ def generate(w: Workload, seed: int = 0, N: int | None = None):
     x = x.astype(np.float32)
     gs = []
     for L in w.layers:
-        std = np.sqrt(2.0 / (9.0 * L.C))
-        gs.append((rng.standard_normal((L.K, L.C, 3, 3)) * std).astype(np.float32))
+        std = np.sqrt(2.0 / (L.r * L.r * L.C))
+        gs.append((rng.standard_normal((L.K, L.C, L.r, L.r)) * std).astype(np.float32))
     return x, gs
 
 

@@ -76,9 +76,9 @@ def _pad_counts(C, K, P):
     return CQ, KB, PB
 
 
-def unpack_U(U: np.ndarray, C: int, K: int, m: int, crop=True) -> np.ndarray:
+def unpack_U(U: np.ndarray, C: int, K: int, m: int, crop=True, r: int = 3) -> np.ndarray:
     """U[KB][CQ][T/4][64][4] (lane = (c%4)*16 + k%16, slot t%4) -> logical [T][C][K]."""
-    T = (m + 2) ** 2
+    T = (m + r - 1) ** 2
     CQ, KB, _ = _pad_counts(C, K, 1)
     a = U[:KB * CQ * T * 64].reshape(KB, CQ, T // 4, 4, 16, 4)           # kb, cq, tg, cl, kl, tt
     a = a.transpose(2, 5, 1, 3, 0, 4).reshape(T, CQ * 4, KB * 16)        # t, c, k

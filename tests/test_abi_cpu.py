@@ -112,3 +112,40 @@ def test_stage_entry_points_reject():
     assert B.wino_maxpool2x2(FAKE, None, 1, 1, 4, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_maxpool2x2(FAKE, FAKE + 0x10000, 1, 1, 1, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_maxpool2x2(FAKE, FAKE + 4, 1, 1, 4, 4) == B.WINO_ERR_INVALID_ARG     # overlap
+
+
+def test_5x5_sizes_and_rejections():
+    # F(2x2,5x5): T = 36, so U has the F(4x4,3x3) size for the same (C, K).
+    assert B.wino_filter_bytes_r(3, 20, 2, 5) == 4 * 36 * 4 * 32
+    assert B.wino_filter_bytes_r(3, 20, 2, 3) == B.wino_filter_bytes(3, 20, 2)
+    assert B.wino_filter_bytes_r(3, 20, 4, 5) == 0                 # F(4x4,5x5): not supported
+    assert B.wino_filter_bytes_r(3, 20, 2, 7) == 0
+    # 35x35, pad 2 -> 35x35 output, 18x18 tiles = 324 -> 21 blocks; V + M of the staged path
+    ws = B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, 0)
+    v = 4 * 21 * 12 * 36 * 64
+    assert ws == (v + 255) // 256 * 256 + 4 * 21 * 4 * 36 * 256
+    assert B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, B.WINO_ALGO_STAGED) == ws
+    for flags in (B.WINO_ALGO_FUSED, B.WINO_ALGO_SPLIT, B.WINO_ALGO_LOWC, B.WINO_BLOCK_4x4, B.WINO_CSPLIT(2)):
+        assert B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, flags) == 2**64 - 1
+    assert B.wino_workspace_bytes_r(1, 4, 3, 3, 4, 0, 2, 5, 0) == 2**64 - 1        # Ho < 1
+    # the 3x3 calls are the r = 3 case
+    assert B.wino_workspace_bytes_r(1, 64, 112, 112, 64, 1, 4, 3, B.WINO_ALGO_STAGED) == \
+        B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_STAGED)
+
+
+def test_5x5_entry_points_reject():
+    y = FAKE + 0x100000
+    assert B.wino_filter_transform_r(None, FAKE, 4, 4, 2, 5) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform_r(FAKE, FAKE + 0x10000, 4, 4, 4, 5) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_filter_transform_r(FAKE, FAKE + 4 * 25, 4, 4, 2, 5) == B.WINO_ERR_INVALID_ARG  # overlap
+    conv = lambda **kw: B.wino_conv2d_r(kw.get("x", FAKE), FAKE + 0x800000, kw.get("y", y), 1, 4, 8, 8, 4,
+                                        kw.get("pad", 2), kw.get("m", 2), kw.get("r", 5), kw.get("flags", 0),
+                                        kw.get("ws"), kw.get("wsb", 0), None)
+    assert conv() == B.WINO_ERR_WORKSPACE                          # the three stages need V and M
+    assert conv(flags=B.WINO_ALGO_FUSED) == B.WINO_ERR_UNSUPPORTED
+    assert conv(r=7) == B.WINO_ERR_UNSUPPORTED
+    assert conv(m=4) == B.WINO_ERR_UNSUPPORTED
+    assert conv(pad=-1) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_conv2d_r(FAKE, FAKE + 0x800000, y, 1, 4, 3, 3, 4, 0, 2, 5, 0, None, 0, None) == \
+        B.WINO_ERR_INVALID_ARG                                     # Ho = -1
+    assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG             # y overlaps x
