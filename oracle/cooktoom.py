@@ -311,3 +311,162 @@ def input_transform_m2_paper_order_f32(x: np.ndarray, pad: int) -> np.ndarray:
     assert V.dtype == np.float32
     V = np.transpose(V, (4, 5, 1, 0, 2, 3))        # xi, nu, c, n, ti, tj
     return np.ascontiguousarray(V.reshape(16, C, N * th * tw))
+
+
+# ----------------------------------------------------------------------------
+# 1-D layers (1 x r and r x 1 filters): F(1 x m, 1 x r, 1 x 8)
+# ----------------------------------------------------------------------------
+# The paper applies variants of the method to 1-D layers as well (1xN and Nx1
+# filters, Table 2's 1x7 and 7x1 Inception-v3 layers) and names F(1x6,1x3,1x8),
+# F(1x4,1x5,1x8) and F(1x2,1x7,1x8).  A 1-D layer is Eq. 1 with regions of one
+# row (or column) of alpha = 8 inputs producing m outputs along that axis.
+
+SUPPORTED_1D = ((6, 3), (4, 5), (2, 7))
+
+
+def interpolation_points_1d(m: int, r: int) -> list[Q]:
+    """The seven finite points of the alpha = 8 variants; infinity is implied.
+
+    The paper gives none.  Reading taken: {0, 1, -1, 2, -2, 1/2, -1/2}, the
+    usual choice once the small integers run out (powers of two keep every
+    entry of A^T and B^T a dyadic rational, exact in fp32).
+    """
+    if (m, r) not in SUPPORTED_1D:
+        raise ValueError("(m, r) must be one of %s" % (SUPPORTED_1D,))
+    return [Q(0), Q(1), Q(-1), Q(2), Q(-2), Q(1, 2), Q(-1, 2)]
+
+
+@lru_cache(maxsize=None)
+def cook_toom_1d(m: int, r: int):
+    """Exact (A^T, G, B^T) of F(1 x m, 1 x r, 1 x 8): m x 8, 8 x r, 8 x 8.
+
+    Same construction as the 2-D matrices (A^T from the points, G with the
+    Lagrange denominators, B^T the unique exact solution of the bilinear
+    identity); no sign normalisation (nothing is printed for these)."""
+    pts = interpolation_points_1d(m, r)       # validates (m, r)
+    a = m + r - 1
+    nf = a - 1
+    AT = [[(pts[j] ** i if j < nf else Q(int(i == m - 1))) for j in range(a)] for i in range(m)]
+    G = []
+    for j in range(nf):
+        den = prod((pts[j] - pts[l] for l in range(nf) if l != j), start=Q(1))
+        G.append([pts[j] ** k / den for k in range(r)])
+    G.append([Q(int(k == r - 1)) for k in range(r)])
+    E = [[AT[i][j] * G[j][k] for j in range(a)] for i in range(m) for k in range(r)]
+    cols = [_solve_consistent(E, [Q(int(ap == i + k)) for i in range(m) for k in range(r)]) for ap in range(a)]
+    BT = [[cols[ap][j] for ap in range(a)] for j in range(a)]
+    return AT, G, BT
+
+
+def matrices_1d_f64(m: int, r: int):
+    AT, G, BT = cook_toom_1d(m, r)
+    f = lambda M: np.array([[float(v) for v in row] for row in M], dtype=np.float64)
+    return f(AT), f(G), f(BT)
+
+
+def geometry_1d(N: int, H: int, W: int, pad: int, m: int, r: int, axis: str):
+    """(Ho, Wo, th, tw, P) of a 1 x r (axis 'w') or r x 1 (axis 'h') layer.  The
+    padding applies along the filter's axis only (the other extent is 1);
+    tiles are 1 x m (axis 'w') or m x 1 (axis 'h')."""
+    if axis == "w":
+        Ho, Wo = H, W + 2 * pad - (r - 1)
+        th, tw = Ho, -(-Wo // m)
+    elif axis == "h":
+        Ho, Wo = H + 2 * pad - (r - 1), W
+        th, tw = -(-Ho // m), Wo
+    else:
+        raise ValueError("axis must be 'w' or 'h'")
+    return Ho, Wo, th, tw, N * th * tw
+
+
+def _as_1d(x, g, axis):
+    """Move the filtered axis last: x [N, C, L_other, L], g [K, C, r]."""
+    x = np.asarray(x)
+    g = np.asarray(g)
+    if axis == "h":
+        x = np.swapaxes(x, 2, 3)
+    return x, g.reshape(g.shape[0], g.shape[1], -1)
+
+
+def conv1d_exact(x, g, pad: int, m: int, axis: str):
+    """Eq. 1 / Listing 1 for a 1-D layer over the rationals: each region of 8
+    inputs along the axis, per channel, to the transform domain; Hadamard
+    products with G g summed over channels; one inverse transform per region.
+    g: [K, C, 1, r] (axis 'w') or [K, C, r, 1] (axis 'h').  Tiny inputs only."""
+    r = max(np.asarray(g).shape[2:])
+    AT, G, BT = cook_toom_1d(m, r)
+    xs, gs = _as_1d(np.asarray(x, dtype=object), np.asarray(g, dtype=object), axis)
+    N, C, Lo, L = xs.shape
+    K = gs.shape[0]
+    Lout = L + 2 * pad - (r - 1)
+    nt = -(-Lout // m)
+    U = [[[sum((G[t][k] * Q(gs[kk, c, k]) for k in range(r)), Q(0)) for t in range(8)]
+          for c in range(C)] for kk in range(K)]
+    y = np.empty((N, K, Lo, Lout), dtype=object)
+    for n in range(N):
+        for row in range(Lo):
+            for tj in range(nt):
+                V = []
+                for c in range(C):
+                    d = [Q(xs[n, c, row, tj * m - pad + u]) if 0 <= tj * m - pad + u < L else Q(0)
+                         for u in range(8)]
+                    V.append([sum((BT[t][u] * d[u] for u in range(8)), Q(0)) for t in range(8)])
+                for kk in range(K):
+                    acc = [sum((U[kk][c][t] * V[c][t] for c in range(C)), Q(0)) for t in range(8)]
+                    for i in range(m):
+                        j = tj * m + i
+                        if j < Lout:
+                            y[n, kk, row, j] = sum((AT[i][t] * acc[t] for t in range(8)), Q(0))
+    return np.swapaxes(y, 2, 3) if axis == "h" else y
+
+
+def filter_transform_1d(g: np.ndarray, m: int) -> np.ndarray:
+    """U[t][c][k] = (G g[k,c])[t] in fp64; g [K, C, 1, r] or [K, C, r, 1]."""
+    g = np.asarray(g, dtype=np.float64)
+    K, C = g.shape[:2]
+    g = g.reshape(K, C, -1)
+    _, G, _ = matrices_1d_f64(m, g.shape[2])
+    return np.ascontiguousarray(np.einsum("tr,kcr->tck", G, g))
+
+
+def input_transform_1d(x: np.ndarray, pad: int, m: int, r: int, axis: str) -> np.ndarray:
+    """V[t][c][p] = (B^T d_{n,c,tile})[t] in fp64, p = (n*th + ti)*tw + tj."""
+    _, _, BT = matrices_1d_f64(m, r)
+    x = np.asarray(x, dtype=np.float64)
+    N, C, H, W = x.shape
+    Ho, Wo, th, tw, P = geometry_1d(N, H, W, pad, m, r, axis)
+    xs = np.swapaxes(x, 2, 3) if axis == "h" else x        # filtered axis last
+    Lo, L = xs.shape[2], xs.shape[3]
+    nt = tw if axis == "w" else th
+    ext = np.zeros((N, C, Lo, nt * m + 7))
+    n_in = min(L, nt * m + 7 - pad)
+    ext[:, :, :, pad:pad + n_in] = xs[:, :, :, :n_in]
+    d = np.stack([ext[:, :, :, j * m:j * m + 8] for j in range(nt)], axis=3)   # n, c, row, tile, u
+    v = np.einsum("tu,ncrju->tcnrj", BT, d)              # t, c, n, row(other axis), tile
+    if axis == "h":                                      # tiles run along H: p = (n*th + tile)*tw + col
+        v = np.swapaxes(v, 3, 4)
+    return np.ascontiguousarray(v.reshape(8, C, P))
+
+
+def output_transform_1d(M: np.ndarray, N: int, Ho: int, Wo: int, m: int, r: int, axis: str) -> np.ndarray:
+    """y = A^T M_{k,p} along the axis, cropped to Ho x Wo, in fp64."""
+    AT, _, _ = matrices_1d_f64(m, r)
+    T, K, P = M.shape
+    if axis == "w":
+        th, tw = Ho, -(-Wo // m)
+        Mr = np.asarray(M, dtype=np.float64).reshape(8, K, N, th, tw)
+        Y = np.einsum("it,tknaj->nkaji", AT, Mr).reshape(N, K, th, tw * m)
+        return np.ascontiguousarray(Y[:, :, :, :Wo])
+    th, tw = -(-Ho // m), Wo
+    Mr = np.asarray(M, dtype=np.float64).reshape(8, K, N, th, tw)
+    Y = np.einsum("it,tknjb->nkjib", AT, Mr).reshape(N, K, th * m, tw)
+    return np.ascontiguousarray(Y[:, :, :Ho, :])
+
+
+def winograd_conv1d_f64(x: np.ndarray, g: np.ndarray, pad: int, m: int, axis: str) -> np.ndarray:
+    N, C, H, W = np.asarray(x).shape
+    r = max(np.asarray(g).shape[2:])
+    Ho, Wo, _, _, _ = geometry_1d(N, H, W, pad, m, r, axis)
+    U = filter_transform_1d(g, m)
+    V = input_transform_1d(x, pad, m, r, axis)
+    return output_transform_1d(batched_gemm(U, V), N, Ho, Wo, m, r, axis)
