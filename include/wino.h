@@ -191,6 +191,34 @@ int wino_batched_gemm_r(const float* U, const float* V, float* M,
 int wino_output_transform_r(const float* M, float* y, int N, int K, int H, int W,
                             int pad, int m, int r, unsigned flags, void* stream);
 
+/* ---- 1-D layers: F(1xm, 1xr, 1x8) ------------------------------------------
+ * 1 x r filters (axis WINO_AXIS_W: correlation along rows) or r x 1 filters
+ * (WINO_AXIS_H: along columns) -- the paper applies the method to 1xN and Nx1
+ * layers (Table 2's 1x7 and 7x1 Inception-v3 layers) with the variants
+ * F(1x6,1x3,1x8), F(1x4,1x5,1x8) and F(1x2,1x7,1x8): (m, r) in {(6,3), (4,5),
+ * (2,7)}.  alpha = 8 inputs per region, T = 8 positions, points
+ * {0, 1, -1, 2, -2, 1/2, -1/2, inf}.
+ *   g : [K][C][r] fp32 (the taps of a [K][C][1][r] or [K][C][r][1] filter).
+ *   pad : zero padding along the filtered axis only (the other extent is 1).
+ *   Axis W: y[n,k,i,j] = sum_c sum_{s<r} x[n,c,i,j+s-pad] * g[k,c,s],
+ *           Ho = H, Wo = W + 2*pad - (r-1); tiles of 1 x m outputs.
+ *   Axis H: y[n,k,i,j] = sum_c sum_{s<r} x[n,c,i+s-pad,j] * g[k,c,s],
+ *           Ho = H + 2*pad - (r-1), Wo = W; tiles of m x 1 outputs.
+ * Tile p = (n*th + ti)*tw + tj as above (th = Ho, tw = ceil(Wo/m) along W;
+ * th = ceil(Ho/m), tw = Wo along H); U, V and M use the blocked layouts above
+ * with T = 8.  The three stages run (flags: WINO_ALGO_AUTO or _STAGED, and
+ * WINO_FLAG_RELU); the workspace is always required.  Errors as for
+ * wino_conv2d; UNSUPPORTED for other (m, r) or axis values. */
+#define WINO_AXIS_W 1
+#define WINO_AXIS_H 2
+size_t wino_filter_bytes_1d(int C, int K, int m, int r);
+int wino_filter_transform_1d(const float* g, float* U, int C, int K, int m, int r, void* stream);
+size_t wino_workspace_bytes_1d(int N, int C, int H, int W, int K, int pad, int m, int r, int axis,
+                               unsigned flags);
+int wino_conv2d_1d(const float* x, const float* U, float* y,
+                   int N, int C, int H, int W, int K, int pad, int m, int r, int axis,
+                   unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Glue between the blocks of a VGG-style stack (not part of the method):
  * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);

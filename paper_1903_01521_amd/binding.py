@@ -72,6 +72,10 @@ _SIGS = {
     "wino_input_transform_r": ([_vp, _vp] + [_c_int] * 7 + [_vp], _c_int),
     "wino_batched_gemm_r": ([_vp, _vp, _vp] + [_c_int] * 8 + [_vp], _c_int),
     "wino_output_transform_r": ([_vp, _vp] + [_c_int] * 7 + [_c_uint, _vp], _c_int),
+    "wino_filter_bytes_1d": ([_c_int] * 4, _c_size),
+    "wino_filter_transform_1d": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
+    "wino_workspace_bytes_1d": ([_c_int] * 9 + [_c_uint], _c_size),
+    "wino_conv2d_1d": ([_vp, _vp, _vp] + [_c_int] * 9 + [_c_uint, _vp, _c_size, _vp], _c_int),
 }
 
 
@@ -216,6 +220,28 @@ def wino_batched_gemm_r(U, V, M, N, C, H, W, K, pad, m, r, stream=None) -> int:
 
 def wino_output_transform_r(M, y, N, K, H, W, pad, m, r, flags=0, stream=None) -> int:
     return lib().wino_output_transform_r(_fptr(M), _fptr(y), N, K, H, W, pad, m, r, flags, _stream(stream))
+
+
+WINO_AXIS_W = 1
+WINO_AXIS_H = 2
+
+
+def wino_filter_bytes_1d(C, K, m, r) -> int:
+    return lib().wino_filter_bytes_1d(C, K, m, r)
+
+
+def wino_filter_transform_1d(g, U, C, K, m, r, stream=None) -> int:
+    return lib().wino_filter_transform_1d(_fptr(g), _fptr(U), C, K, m, r, _stream(stream))
+
+
+def wino_workspace_bytes_1d(N, C, H, W, K, pad, m, r, axis, flags=0) -> int:
+    return lib().wino_workspace_bytes_1d(N, C, H, W, K, pad, m, r, axis, flags)
+
+
+def wino_conv2d_1d(x, U, y, N, C, H, W, K, pad, m, r, axis, flags=0, workspace=None, workspace_bytes=0,
+                   stream=None) -> int:
+    return lib().wino_conv2d_1d(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, r, axis, flags,
+                                _ptr(workspace), workspace_bytes, _stream(stream))
 
 
 def check(status: int, where: str = "wino") -> None:

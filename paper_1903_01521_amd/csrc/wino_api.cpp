@@ -43,13 +43,39 @@ int make_geom_r(int N, int C, int H, int W, int K, int pad, int m, int r, Geom* 
     if (!mul_ok(PB * CQ, T * 64, &v) || !mul_ok(PB * KB, T * 256, &mm)) return WINO_ERR_INVALID_ARG;
     g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
     g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
-    g->A = (int)A; g->T = (int)T; g->r = r;
+    g->A = (int)A; g->T = (int)T; g->r = r; g->axis = 0;
     g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
     return WINO_OK;
 }
 
 int make_geom(int N, int C, int H, int W, int K, int pad, int m, Geom* g) {
     return make_geom_r(N, C, H, W, K, pad, m, 3, g);
+}
+
+// 1-D layers: (m, r) in {(6,3), (4,5), (2,7)}, alpha = 8; padding along the
+// filtered axis only; tiles 1 x m (along W) or m x 1 (along H).
+bool supported_1d(int m, int r) { return (m == 6 && r == 3) || (m == 4 && r == 5) || (m == 2 && r == 7); }
+
+int make_geom_1d(int N, int C, int H, int W, int K, int pad, int m, int r, int axis, Geom* g) {
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || pad < 0) return WINO_ERR_INVALID_ARG;
+    if (!supported_1d(m, r) || (axis != WINO_AXIS_W && axis != WINO_AXIS_H)) return WINO_ERR_UNSUPPORTED;
+    const bool aw = axis == WINO_AXIS_W;
+    const int64_t L = (aw ? W : H) + 2 * (int64_t)pad - (r - 1);
+    if (L < 1 || L > INT32_MAX / 2) return WINO_ERR_INVALID_ARG;
+    const int64_t Ho = aw ? H : L, Wo = aw ? L : W;
+    const int64_t th = aw ? Ho : (Ho + m - 1) / m, tw = aw ? (Wo + m - 1) / m : Wo;
+    int64_t t1, P, xin, xout;
+    if (!mul_ok(th, tw, &t1) || !mul_ok(t1, N, &P) || P > kMaxTiles) return WINO_ERR_INVALID_ARG;
+    if (!mul_ok((int64_t)N * C, (int64_t)H * W, &xin)) return WINO_ERR_INVALID_ARG;
+    if (!mul_ok((int64_t)N * K, Ho * Wo, &xout)) return WINO_ERR_INVALID_ARG;
+    const int64_t CQ = (C + 3) / 4, KB = (K + 15) / 16, PB = (P + 15) / 16;
+    int64_t v, mm;
+    if (!mul_ok(PB * CQ, 8 * 64, &v) || !mul_ok(PB * KB, 8 * 256, &mm)) return WINO_ERR_INVALID_ARG;
+    g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
+    g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
+    g->A = 8; g->T = 8; g->r = r; g->axis = axis;
+    g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
+    return WINO_OK;
 }
 
 bool overlap(const void* a, size_t na, const void* b, size_t nb) {
@@ -124,9 +150,9 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
         return WINO_ERR_UNSUPPORTED;
     if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
-    // 5x5 filters run the three stages (input transform, GEMMs, output
-    // transform); the one-kernel variants are written for 3x3 regions.
-    if (g.r != 3) {
+    // 5x5 and 1-D filters run the three stages (input transform, GEMMs,
+    // output transform); the one-kernel variants are written for 3x3 regions.
+    if (g.r != 3 || g.axis != 0) {
         if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->algo = WINO_ALGO_STAGED;
@@ -339,6 +365,59 @@ int wino_output_transform_r(const float* M, float* y, int N, int K, int H, int W
 int wino_output_transform(const float* M, float* y, int N, int K, int H, int W, int pad, int m, unsigned flags,
                           void* stream) {
     return wino_output_transform_r(M, y, N, K, H, W, pad, m, 3, flags, stream);
+}
+
+size_t wino_filter_bytes_1d(int C, int K, int m, int r) {
+    if (C <= 0 || K <= 0 || !supported_1d(m, r)) return 0;
+    int64_t e;
+    if (!mul_ok((int64_t)(C + 3) / 4 * 4, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, 8, &e)) return 0;
+    return (size_t)e * sizeof(float);
+}
+
+int wino_filter_transform_1d(const float* gw, float* U, int C, int K, int m, int r, void* stream) {
+    if (!gw || !U || C <= 0 || K <= 0) return WINO_ERR_INVALID_ARG;
+    if (!supported_1d(m, r)) return WINO_ERR_UNSUPPORTED;
+    const size_t ub = wino_filter_bytes_1d(C, K, m, r);
+    if (ub == 0) return WINO_ERR_INVALID_ARG;
+    if (overlap(gw, (size_t)K * C * r * sizeof(float), U, ub)) return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_filter_transform_1d(gw, U, C, K, m, r, (hipStream_t)stream));
+}
+
+size_t wino_workspace_bytes_1d(int N, int C, int H, int W, int K, int pad, int m, int r, int axis,
+                               unsigned flags) {
+    Geom g;
+    Plan p;
+    if (make_geom_1d(N, C, H, W, K, pad, m, r, axis, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
+        return (size_t)-1;
+    return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
+}
+
+int wino_conv2d_1d(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
+                   int r, int axis, unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    int st = make_geom_1d(N, C, H, W, K, pad, m, r, axis, &g);
+    if (st != WINO_OK) return st;
+    Plan p;
+    st = make_plan(g, flags, &p);
+    if (st != WINO_OK) return st;
+    const size_t xb = (size_t)N * C * H * W * sizeof(float);
+    const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
+    const size_t ub = wino_filter_bytes_1d(C, K, m, r);
+    if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
+    const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
+    const size_t need = vb + m_elems(g) * sizeof(float);
+    if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+    if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+        return WINO_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    float* V = (float*)workspace;
+    float* M = (float*)((char*)workspace + vb);
+    st = hip_status(launch_input_transform(x, V, g, s));
+    if (st != WINO_OK) return st;
+    st = hip_status(launch_batched_gemm(U, V, M, g, s));
+    if (st != WINO_OK) return st;
+    return hip_status(launch_output_transform(M, y, g, (flags & WINO_FLAG_RELU) != 0, s));
 }
 
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream) {

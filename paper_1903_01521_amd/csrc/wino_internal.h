@@ -14,8 +14,9 @@ struct Geom {
     int N, C, H, W, K, pad, m;
     int Ho, Wo, th, tw;
     int P;          // tiles, N*th*tw
-    int A, T;       // alpha = m + r - 1, T = alpha^2
-    int r;          // filter side
+    int A, T;       // alpha = m + r - 1; T = alpha^2 (2-D) or alpha (1-D)
+    int r;          // filter side (the filter's length for 1-D layers)
+    int axis;       // 0: r x r filter; 1: 1 x r (along W); 2: r x 1 (along H)
     int CQ, KB, PB; // 4-channel quads, 16-filter blocks, 16-tile blocks
 };
 
@@ -55,5 +56,9 @@ hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, con
 // Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.
 hipError_t launch_lowc(const float* x, const float* U, float* y, const Geom& g, bool relu, hipStream_t s);
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s);
+// 1-D layers (1 x r or r x 1 filters, F(1xm, 1xr, 1x8)): filter transform; the
+// input and output transforms dispatch on g.axis inside launch_input_transform
+// and launch_output_transform.
+hipError_t launch_filter_transform_1d(const float* g, float* U, int C, int K, int m, int r, hipStream_t s);
 
 }  // namespace wino

@@ -1318,6 +1318,138 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
     }
 }
 
+// ------------------------------------------------------------------ 1-D
+// 1 x r (axis 1, along W) and r x 1 (axis 2, along H) layers: regions of 8
+// inputs along the axis give m = 9 - r outputs; T = 8 transform positions, so
+// the blocked U, V and M layouts are those of the 2-D path with T = 8, and the
+// GEMM stage is k_gemm unchanged.
+
+// One wave per (16-filter block, 4-channel quad); lane = (c%4)*16 + k%16.
+template <int R>
+__global__ __launch_bounds__(256) void k_filter1d(const float* __restrict__ gw, float* __restrict__ U, int C,
+                                                  int K, int CQ, long nw) {
+    const int lane = threadIdx.x & 63;
+    const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= nw) return;
+    const int kb = (int)(w / CQ), cq = (int)(w % CQ);
+    const int k = kb * 16 + (lane & 15), c = cq * 4 + (lane >> 4);
+    const bool ok = k < K && c < C;
+    const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c : 0)) * R;
+    float g[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) g[j] = ok ? src[j] : 0.0f;
+    float u[8];
+    filter_tf8<R>(g, u);
+    store_t4<8, false>(U + (size_t)w * 8 * 64, lane, u);
+}
+
+// One wave per (16-tile block, 4-channel quad), XCD-contiguous runs as in
+// k_input; lane = (tile p%16, channel c%4) loads its 8 inputs along the axis
+// (zero outside the image, past C and past P) and writes B^T d.
+template <int MT, int AX>
+__global__ __launch_bounds__(256) void k_input1d(const float* __restrict__ x, float* __restrict__ V, Geom g,
+                                                 long nwg) {
+    const int lane = threadIdx.x & 63;
+    const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nwg) return;
+    const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= (long)g.PB * g.CQ) return;
+    const int cq = (int)(w / g.PB), pb = (int)(w % g.PB);
+    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const int c = cq * 4 + (lane >> 4);
+    const bool ok = tc.valid && c < g.C;
+    const float* xc = x + ((size_t)tc.n * g.C + (ok ? c : 0)) * g.H * g.W;
+    float d[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        int row, col;
+        if constexpr (AX == 1) {
+            row = tc.ti;
+            col = tc.tj * MT - g.pad + u;
+        } else {
+            row = tc.ti * MT - g.pad + u;
+            col = tc.tj;
+        }
+        const bool in = ok && (unsigned)row < (unsigned)g.H && (unsigned)col < (unsigned)g.W;
+        d[u] = in ? xc[(size_t)row * g.W + col] : 0.0f;
+    }
+    float v[8];
+    bt8(d, v);
+    store_t4<8, true>(V + ((size_t)pb * g.CQ + cq) * 8 * 64, lane, v);
+}
+
+// One wave per (16-tile block, 16-filter block): lane = (tile p%16, filter
+// quad); gathers the 8 values of its four (tile, filter) pairs, applies A^T
+// and writes m outputs per filter along the axis.
+template <int MT, int AX>
+__global__ __launch_bounds__(256) void k_output1d(const float* __restrict__ M, float* __restrict__ y, Geom g,
+                                                  int relu) {
+    const int lane = threadIdx.x & 63;
+    const long w = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (long)g.PB * g.KB) return;
+    const int pb = (int)(w / g.KB), kb = (int)(w % g.KB);
+    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const float* src = M + ((size_t)w * 8) * 256 + lane * 4;
+    f32x4 mv[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) mv[t] = *(const f32x4*)(src + t * 256);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int k = kb * 16 + 4 * (lane >> 4) + r;
+        if (!tc.valid || k >= g.K) continue;
+        float a[8], o[MT];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) a[t] = mv[t][r];
+        at8<MT>(a, o);
+        float* yk = y + ((size_t)tc.n * g.K + k) * g.Ho * g.Wo;
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const float v = relu ? fmaxf(o[i], 0.0f) : o[i];
+            if constexpr (AX == 1) {
+                const int col = tc.tj * MT + i;
+                if (col < g.Wo) yk[(size_t)tc.ti * g.Wo + col] = v;
+            } else {
+                const int row = tc.ti * MT + i;
+                if (row < g.Ho) yk[(size_t)row * g.Wo + tc.tj] = v;
+            }
+        }
+    }
+}
+
+hipError_t launch_filter_transform_1d(const float* gw, float* U, int C, int K, int m, int r, hipStream_t s) {
+    const int CQ = (C + 3) / 4, KB = (K + 15) / 16;
+    const long waves = (long)KB * CQ;
+    if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    (void)m;
+    if (r == 3) hipLaunchKernelGGL(k_filter1d<3>, grid, block, 0, s, gw, U, C, K, CQ, waves);
+    else if (r == 5) hipLaunchKernelGGL(k_filter1d<5>, grid, block, 0, s, gw, U, C, K, CQ, waves);
+    else hipLaunchKernelGGL(k_filter1d<7>, grid, block, 0, s, gw, U, C, K, CQ, waves);
+    return hipGetLastError();
+}
+
+static hipError_t launch_input_1d(const float* x, float* V, const Geom& g, hipStream_t s) {
+    const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
+    if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
+#define WINO_IN1D(MT, AX) \
+    if (g.m == MT && g.axis == AX) { hipLaunchKernelGGL((k_input1d<MT, AX>), grid, block, 0, s, x, V, g, nwg); return hipGetLastError(); }
+    WINO_IN1D(6, 1) WINO_IN1D(4, 1) WINO_IN1D(2, 1) WINO_IN1D(6, 2) WINO_IN1D(4, 2) WINO_IN1D(2, 2)
+#undef WINO_IN1D
+    return hipErrorInvalidValue;
+}
+
+static hipError_t launch_output_1d(const float* M, float* y, const Geom& g, bool relu, hipStream_t s) {
+    const long waves = (long)g.PB * g.KB;
+    if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+#define WINO_OUT1D(MT, AX) \
+    if (g.m == MT && g.axis == AX) { hipLaunchKernelGGL((k_output1d<MT, AX>), grid, block, 0, s, M, y, g, (int)relu); return hipGetLastError(); }
+    WINO_OUT1D(6, 1) WINO_OUT1D(4, 1) WINO_OUT1D(2, 1) WINO_OUT1D(6, 2) WINO_OUT1D(4, 2) WINO_OUT1D(2, 2)
+#undef WINO_OUT1D
+    return hipErrorInvalidValue;
+}
+
 // ------------------------------------------------------------------ maxpool
 __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x, float* __restrict__ y,
                                                     long total, int H, int W, int Ho, int Wo) {
@@ -1359,6 +1491,7 @@ hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int 
 }
 
 hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s) {
+    if (g.axis != 0) return launch_input_1d(x, V, g, s);
     const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
@@ -1381,6 +1514,7 @@ hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const G
 }
 
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s) {
+    if (g.axis != 0) return launch_output_1d(M, y, g, relu, s);
     const int vec_ok = (g.Wo % g.m == 0) && aligned(y, 4 * g.m);
     int R = 0, segs = 0, ipi;                      // items per image
     if (g.tw <= 64) {

@@ -286,3 +286,77 @@ __device__ __forceinline__ float4 filter_tf4(const float (&g)[R][R]) {
 }
 
 }  // namespace wino
+
+namespace wino {
+
+// ---------------------------------------------------------------- 1-D, alpha = 8
+// F(1xm, 1xr, 1x8) for 1xr / rx1 filters, (m, r) = (6, 3), (4, 5), (2, 7), with
+// the points {0, 1, -1, 2, -2, 1/2, -1/2, inf}.  B^T is the same for the three
+// (it depends only on the points); every entry of B^T and A^T is a dyadic
+// rational, exact in fp32:
+//   B^T = [-1   0  21/4    0  -21/4    0   1  0;
+//           0   1     1 -17/4 -17/4    1   1  0;
+//           0  -1     1  17/4 -17/4   -1   1  0;
+//           0 1/2   1/4  -5/2  -5/4    2   1  0;
+//           0 -1/2  1/4   5/2  -5/4   -2   1  0;
+//           0   2     4  -5/2    -5  1/2   1  0;
+//           0  -2     4   5/2    -5 -1/2   1  0;
+//           0  -1     0  21/4     0 -21/4  0  1]
+//   A^T[i] = [i == 0, 1, (-1)^i, 2^i, (-2)^i, 2^-i, (-2)^-i, i == m-1]
+//   G[j][k] = p_j^k / prod_{l != j} (p_j - p_l) (finite points), G[7] = e_{r-1};
+//   90 G is an integer matrix: rows -90 e_0, -20 (1)^k, -20 (-1)^k, 2^k,
+//   (-2)^k, 2^(6-k), (-1)^k 2^(6-k), 90 e_{r-1}.
+__device__ __forceinline__ void bt8(const float (&d)[8], float (&v)[8]) {
+    const float d24 = d[2] - d[4], d35 = d[3] - d[5];
+    v[0] = __builtin_fmaf(5.25f, d24, d[6] - d[0]);
+    v[7] = __builtin_fmaf(5.25f, d35, d[7] - d[1]);
+    const float s15 = d[1] + d[5], s26 = d[2] + d[6];
+    v[1] = __builtin_fmaf(-4.25f, d[3] + d[4], s15 + s26);
+    v[2] = __builtin_fmaf(4.25f, d[3] - d[4], s26 - s15);
+    const float o3 = __builtin_fmaf(0.5f, d[1], __builtin_fmaf(-2.5f, d[3], 2.0f * d[5]));
+    const float e3 = __builtin_fmaf(0.25f, d[2], __builtin_fmaf(-1.25f, d[4], d[6]));
+    v[3] = e3 + o3;
+    v[4] = e3 - o3;
+    const float o5 = __builtin_fmaf(2.0f, d[1], __builtin_fmaf(-2.5f, d[3], 0.5f * d[5]));
+    const float e5 = __builtin_fmaf(4.0f, d[2], __builtin_fmaf(-5.0f, d[4], d[6]));
+    v[5] = e5 + o5;
+    v[6] = e5 - o5;
+}
+
+template <int M>
+__device__ __forceinline__ void at8(const float (&a)[8], float (&o)[M]) {
+    const float s1 = a[1] + a[2], d1 = a[1] - a[2];
+    const float s2 = a[3] + a[4], d2 = a[3] - a[4];
+    const float s3 = a[5] + a[6], d3 = a[5] - a[6];
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        const float p = (float)(1 << i), q = 1.0f / (float)(1 << i);     // 2^i, 2^-i (exact)
+        float v = (i & 1) ? __builtin_fmaf(p, d2, __builtin_fmaf(q, d3, d1))
+                          : __builtin_fmaf(p, s2, __builtin_fmaf(q, s3, s1));
+        if (i == 0) v += a[0];
+        if (i == M - 1) v += a[7];
+        o[i] = v;
+    }
+}
+
+// U = G g in fp64 with the integer matrix 90 G, scaled once by 1/90, rounded
+// once to fp32.
+template <int R>
+__device__ __forceinline__ void filter_tf8(const float (&g)[R], float (&u)[8]) {
+    double s = 0, a = 0, p2 = 0, m2 = 0, h = 0, mh = 0;
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const double v = (double)g[k], sg = (k & 1) ? -1.0 : 1.0;
+        s += v;
+        a += sg * v;
+        p2 += (double)(1 << k) * v;
+        m2 += sg * (double)(1 << k) * v;
+        h += (double)(1 << (6 - k)) * v;
+        mh += sg * (double)(1 << (6 - k)) * v;
+    }
+    const double r[8] = {-90.0 * g[0], -20.0 * s, -20.0 * a, p2, m2, h, mh, 90.0 * g[R - 1]};
+#pragma unroll
+    for (int t = 0; t < 8; ++t) u[t] = (float)(r[t] * (1.0 / 90.0));
+}
+
+}  // namespace wino

@@ -28,7 +28,8 @@ class Layer:
     pad: int = 1
     relu: bool = False        # ReLU applied to this layer's output
     pool: bool = False        # 2x2/2 max-pool applied after (the ReLU of) this layer
-    r: int = 3                # filter side (3, or 5 with m = 2)
+    r: int = 3                # filter side (3, or 5 with m = 2), or a 1-D filter's length
+    axis: str = ""            # "" for r x r filters; "w" for 1 x r, "h" for r x 1 (1-D layers)
 
 
 @dataclass(frozen=True)
@@ -82,6 +83,10 @@ WORKLOADS = {w.name: w for w in [
              x_dist="uniform", note="low-C first layer, batch 1"),
     Workload("f2r5_n32_c48_k64_35x35", 32, (Layer(48, 64, 35, 35, m=2, pad=2, r=5),),
              note="5x5 layer shaped like Inception-v3's 5x5 branch, F(2x2,5x5)"),
+    Workload("f2r7w_n32_c192_k160_17x17", 32, (Layer(192, 160, 17, 17, m=2, pad=3, r=7, axis="w"),),
+             note="1x7 layer shaped like Inception-v3's 17x17 blocks, F(1x2,1x7,1x8)"),
+    Workload("f2r7h_n32_c192_k160_17x17", 32, (Layer(192, 160, 17, 17, m=2, pad=3, r=7, axis="h"),),
+             note="7x1 layer shaped like Inception-v3's 17x17 blocks, F(2x1,7x1,8x1)"),
 ]}
 
 # The single-layer workload the benchmark times by default.
@@ -89,7 +94,7 @@ DEFAULT_BENCH = "f4_n1_c64_k64_112x112"
 
 
 def generate(w: Workload, seed: int = 0, N: int | None = None):
-    """Draw (x, [g_layer, ...]) as fp32 arrays: x [N,C,H,W], g [K,C,r,r]."""
+    """Draw (x, [g_layer, ...]) as fp32 arrays: x [N,C,H,W], g [K,C,R,S]."""
     rng = np.random.default_rng(seed)
     L0 = w.first
     n = w.N if N is None else N
@@ -103,8 +108,9 @@ def generate(w: Workload, seed: int = 0, N: int | None = None):
     x = x.astype(np.float32)
     gs = []
     for L in w.layers:
-        std = np.sqrt(2.0 / (L.r * L.r * L.C))
-        gs.append((rng.standard_normal((L.K, L.C, L.r, L.r)) * std).astype(np.float32))
+        R, S = {"": (L.r, L.r), "w": (1, L.r), "h": (L.r, 1)}[L.axis]
+        std = np.sqrt(2.0 / (R * S * L.C))
+        gs.append((rng.standard_normal((L.K, L.C, R, S)) * std).astype(np.float32))
     return x, gs
 
 

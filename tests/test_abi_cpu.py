@@ -149,3 +149,35 @@ def test_5x5_entry_points_reject():
     assert B.wino_conv2d_r(FAKE, FAKE + 0x800000, y, 1, 4, 3, 3, 4, 0, 2, 5, 0, None, 0, None) == \
         B.WINO_ERR_INVALID_ARG                                     # Ho = -1
     assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG             # y overlaps x
+
+
+def test_1d_sizes_and_rejections():
+    W_, H_ = B.WINO_AXIS_W, B.WINO_AXIS_H
+    assert B.wino_filter_bytes_1d(3, 20, 6, 3) == 4 * 8 * 4 * 32
+    assert B.wino_filter_bytes_1d(3, 20, 2, 7) == 4 * 8 * 4 * 32
+    assert B.wino_filter_bytes_1d(3, 20, 4, 3) == 0                  # not a supported variant
+    # 1x7 on 17x17, pad 3 along W: 17 x 17 output, 17 x 9 tiles = 153 -> 10 blocks
+    ws = B.wino_workspace_bytes_1d(1, 192, 17, 17, 160, 3, 2, 7, W_, 0)
+    assert ws == (4 * 10 * 48 * 8 * 64 + 255) // 256 * 256 + 4 * 10 * 10 * 8 * 256
+    assert B.wino_workspace_bytes_1d(1, 192, 17, 17, 160, 3, 2, 7, H_, 0) == ws   # 9 x 17 tiles, same count
+    assert B.wino_workspace_bytes_1d(1, 192, 17, 17, 160, 3, 2, 7, 3, 0) == 2**64 - 1     # unknown axis
+    assert B.wino_workspace_bytes_1d(1, 192, 17, 17, 160, 3, 2, 7, W_, B.WINO_ALGO_FUSED) == 2**64 - 1
+    assert B.wino_workspace_bytes_1d(1, 4, 5, 5, 4, 0, 2, 7, W_, 0) == 2**64 - 1          # Wo < 1
+
+
+def test_1d_entry_points_reject():
+    y = FAKE + 0x100000
+    assert B.wino_filter_transform_1d(None, FAKE, 4, 4, 2, 7) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform_1d(FAKE, FAKE + 0x10000, 4, 4, 2, 5) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_filter_transform_1d(FAKE, FAKE + 4 * 7, 4, 4, 2, 7) == B.WINO_ERR_INVALID_ARG   # overlap
+    conv = lambda **kw: B.wino_conv2d_1d(kw.get("x", FAKE), FAKE + 0x800000, kw.get("y", y), 1, 4, 8, 8, 4,
+                                         kw.get("pad", 3), kw.get("m", 2), kw.get("r", 7),
+                                         kw.get("axis", B.WINO_AXIS_W), kw.get("flags", 0), None, 0, None)
+    assert conv() == B.WINO_ERR_WORKSPACE
+    assert conv(axis=0) == B.WINO_ERR_UNSUPPORTED
+    assert conv(m=6) == B.WINO_ERR_UNSUPPORTED
+    assert conv(flags=B.WINO_ALGO_SPLIT) == B.WINO_ERR_UNSUPPORTED
+    assert conv(pad=0, axis=B.WINO_AXIS_H, m=2, r=7) == B.WINO_ERR_WORKSPACE           # Ho = 2: valid
+    assert B.wino_conv2d_1d(FAKE, FAKE + 0x800000, y, 1, 4, 5, 5, 4, 0, 2, 7, B.WINO_AXIS_W, 0, None, 0,
+                            None) == B.WINO_ERR_INVALID_ARG                           # Wo = -1
+    assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG
