@@ -45,9 +45,12 @@ CSRC = os.path.join(HERE, "paper_1903_01521_amd", "csrc")
 PROFILES = os.path.join(HERE, "profiles")
 
 # Kernel-name prefixes as rocprofv3 reports them, per kind of launch.
+AXIS = {"w": 1, "h": 2}   # WINO_AXIS_W, WINO_AXIS_H
+
 KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
-                "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2"}
+                "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
+                "conv1d": "void wino::k_gemm"}
 
 
 def log(*a):
@@ -66,26 +69,34 @@ def sources_hash() -> str:
 
 def layer_numbers(N, L):
     """Sizes and algorithmic work of one layer (m x m tiles, alpha = m+2)."""
-    Ho, Wo = L.H + 2 * L.pad - (L.r - 1), L.W + 2 * L.pad - (L.r - 1)
-    th, tw = -(-Ho // L.m), -(-Wo // L.m)
+    if L.axis == "w":              # 1 x r filter: tiles of 1 x m, padding along W only
+        Ho, Wo = L.H, L.W + 2 * L.pad - (L.r - 1)
+        th, tw, T, taps = Ho, -(-Wo // L.m), 8, L.r
+    elif L.axis == "h":            # r x 1 filter
+        Ho, Wo = L.H + 2 * L.pad - (L.r - 1), L.W
+        th, tw, T, taps = -(-Ho // L.m), Wo, 8, L.r
+    else:
+        Ho, Wo = L.H + 2 * L.pad - (L.r - 1), L.W + 2 * L.pad - (L.r - 1)
+        th, tw, T, taps = -(-Ho // L.m), -(-Wo // L.m), (L.m + L.r - 1) ** 2, L.r * L.r
     P = N * th * tw
-    T = (L.m + L.r - 1) ** 2
     f = dict(Ho=Ho, Wo=Wo, P=P, T=T)
-    f["direct_flops"] = 2 * N * L.K * L.C * L.r * L.r * Ho * Wo
+    f["direct_flops"] = 2 * N * L.K * L.C * taps * Ho * Wo
     f["gemm_flops"] = 2 * T * P * L.C * L.K
     x_b, y_b, u_b = 4 * N * L.C * L.H * L.W, 4 * N * L.K * Ho * Wo, 4 * T * L.C * L.K
     v_b, m_b = 4 * T * P * L.C, 4 * T * P * L.K
     # minimum HBM bytes per kernel launch (what the method must move, padding excluded)
     f["bytes"] = {
-        "filter": 4 * L.K * L.C * L.r * L.r + u_b,
+        "filter": 4 * L.K * L.C * taps + u_b,
         "fused": x_b + u_b + y_b,
         "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
         "gemm": v_b + u_b + m_b,
         "output": m_b + y_b,
         "maxpool": y_b + y_b // 4,
+        # the three stages of a 1-D layer in one call: x -> V -> M -> y
+        "conv1d": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
     }
-    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"]}
+    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "conv1d": f["gemm_flops"]}
     return f
 
 
@@ -286,11 +297,15 @@ def main():
     H, W = w.first.H, w.first.W
     for L, f in zip(w.layers, nums):
         assert (L.H, L.W) == (H, W)
-        Us.append(torch.empty(B.wino_filter_bytes_r(L.C, L.K, L.m, L.r) // 4, dtype=torch.float32, device=dev))
+        ub = B.wino_filter_bytes_1d(L.C, L.K, L.m, L.r) if L.axis else B.wino_filter_bytes_r(L.C, L.K, L.m, L.r)
+        Us.append(torch.empty(ub // 4, dtype=torch.float32, device=dev))
         ys.append(torch.empty((N, L.K, f["Ho"], f["Wo"]), dtype=torch.float32, device=dev))
-        wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
+        if L.axis:
+            wsb = B.wino_workspace_bytes_1d(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, AXIS[L.axis], flags)
+        else:
+            wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
         wss.append((torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev), wsb))
-        if staged or L.r != 3:
+        if (staged or L.r != 3) and not L.axis:
             Vs.append(torch.empty(B.wino_input_tf_bytes_r(N, L.C, L.H, L.W, L.pad, L.m, L.r) // 4,
                                   dtype=torch.float32, device=dev))
             Ms.append(torch.empty(B.wino_gemm_out_bytes_r(N, L.K, L.H, L.W, L.pad, L.m, L.r) // 4,
@@ -311,6 +326,16 @@ def main():
         a = hx
         for i, L in enumerate(w.layers):
             relu = B.WINO_FLAG_RELU if L.relu else 0
+            if L.axis:                     # 1-D layer: the three stages in one call
+                ws, wsb = wss[i]
+                out.append((f"L{i}.filter", i, "filter", (lambda sp, i=i, L=L: B.wino_filter_transform_1d(
+                    hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
+                out.append((f"L{i}.conv", i, "conv1d", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                                                         B.wino_conv2d_1d(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
+                                                                          L.pad, L.m, L.r, AXIS[L.axis],
+                                                                          flags | relu, ws, wsb, sp))))
+                a = ys[i]
+                continue
             out.append((f"L{i}.filter", i, "filter",
                         (lambda sp, i=i, L=L: B.wino_filter_transform_r(hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
             if staged or L.r != 3:         # 5x5 layers run the three stages
@@ -514,7 +539,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": name, "N": N, "layers": len(w.layers),
                    "C": w.first.C, "K": w.first.K, "H": w.first.H, "W": w.first.W,
-                   "m": w.first.m, "r": w.first.r, "pad": w.first.pad, "flags": hex(flags),
+                   "m": w.first.m, "r": w.first.r, "axis": w.first.axis or "2d", "pad": w.first.pad,
+                   "flags": hex(flags),
                    "launch": "eager" if graph is None else "hip_graph", "parallelism": "none"},
         "roofline": roof,
         "per_launch_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, per_launch)},
@@ -539,9 +565,14 @@ def main():
         L0, g0 = w.first, gs[0]
         y_gpu = ys[0].detach().cpu().numpy()      # holds the last step's output (ReLU applied)
         reps_cpu, t_cpu, ref = 0, 0.0, None
+        xin, pad_in = x, L0.pad
+        if L0.axis:                    # 1-D layer: padding along the filtered axis only
+            pw = [(0, 0)] * 4
+            pw[3 if L0.axis == "w" else 2] = (L0.pad, L0.pad)
+            xin, pad_in = np.pad(x, pw), 0
         while t_cpu < args.cpu_seconds and reps_cpu < 100000:
             t0 = time.perf_counter()
-            ref = odirect.conv2d(x, g0, L0.pad)
+            ref = odirect.conv2d(xin, g0, pad_in)
             t_cpu += time.perf_counter() - t0
             reps_cpu += 1
         if L0.relu:
