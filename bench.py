@@ -50,7 +50,7 @@ AXIS = {"w": 1, "h": 2}   # WINO_AXIS_W, WINO_AXIS_H
 KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
-                "conv1d": "void wino::k_gemm"}
+                "stages": "void wino::k_gemm"}
 
 
 def log(*a):
@@ -93,10 +93,10 @@ def layer_numbers(N, L):
         "gemm": v_b + u_b + m_b,
         "output": m_b + y_b,
         "maxpool": y_b + y_b // 4,
-        # the three stages of a 1-D layer in one call: x -> V -> M -> y
-        "conv1d": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
+        # the three stages in one call (1-D and channel-last layers): x -> V -> M -> y
+        "stages": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
     }
-    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "conv1d": f["gemm_flops"]}
+    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "stages": f["gemm_flops"]}
     return f
 
 
@@ -288,7 +288,8 @@ def main():
 
     x, gs = wl.generate(w)
     dev = torch.device("cuda:0")
-    hx = torch.from_numpy(x).to(dev)
+    # channel-last workloads get x as [N][H][W][C] (outside the timed region)
+    hx = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 2, 3, 1)) if w.first.nhwc else x).to(dev)
     hg = [torch.from_numpy(g).to(dev) for g in gs]
     nums = [layer_numbers(N, L) for L in w.layers]
 
@@ -299,13 +300,16 @@ def main():
         assert (L.H, L.W) == (H, W)
         ub = B.wino_filter_bytes_1d(L.C, L.K, L.m, L.r) if L.axis else B.wino_filter_bytes_r(L.C, L.K, L.m, L.r)
         Us.append(torch.empty(ub // 4, dtype=torch.float32, device=dev))
-        ys.append(torch.empty((N, L.K, f["Ho"], f["Wo"]), dtype=torch.float32, device=dev))
-        if L.axis:
+        ys.append(torch.empty((N, f["Ho"], f["Wo"], L.K) if L.nhwc else (N, L.K, f["Ho"], f["Wo"]),
+                              dtype=torch.float32, device=dev))
+        if L.nhwc:
+            wsb = B.wino_workspace_bytes_nhwc(N, L.C, L.H, L.W, L.K, L.pad, L.m, flags)
+        elif L.axis:
             wsb = B.wino_workspace_bytes_1d(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, AXIS[L.axis], flags)
         else:
             wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
         wss.append((torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev), wsb))
-        if (staged or L.r != 3) and not L.axis:
+        if (staged or L.r != 3) and not L.axis and not L.nhwc:
             Vs.append(torch.empty(B.wino_input_tf_bytes_r(N, L.C, L.H, L.W, L.pad, L.m, L.r) // 4,
                                   dtype=torch.float32, device=dev))
             Ms.append(torch.empty(B.wino_gemm_out_bytes_r(N, L.K, L.H, L.W, L.pad, L.m, L.r) // 4,
@@ -326,11 +330,20 @@ def main():
         a = hx
         for i, L in enumerate(w.layers):
             relu = B.WINO_FLAG_RELU if L.relu else 0
+            if L.nhwc:                     # channel-last layer: the three stages in one call
+                ws, wsb = wss[i]
+                out.append((f"L{i}.filter", i, "filter", (lambda sp, i=i, L=L: B.wino_filter_transform(
+                    hg[i], Us[i], L.C, L.K, L.m, sp))))
+                out.append((f"L{i}.conv", i, "stages", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                                                         B.wino_conv2d_nhwc(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
+                                                                            L.pad, L.m, flags | relu, ws, wsb, sp))))
+                a = ys[i]
+                continue
             if L.axis:                     # 1-D layer: the three stages in one call
                 ws, wsb = wss[i]
                 out.append((f"L{i}.filter", i, "filter", (lambda sp, i=i, L=L: B.wino_filter_transform_1d(
                     hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
-                out.append((f"L{i}.conv", i, "conv1d", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                out.append((f"L{i}.conv", i, "stages", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                          B.wino_conv2d_1d(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                           L.pad, L.m, L.r, AXIS[L.axis],
                                                                           flags | relu, ws, wsb, sp))))
@@ -539,7 +552,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": name, "N": N, "layers": len(w.layers),
                    "C": w.first.C, "K": w.first.K, "H": w.first.H, "W": w.first.W,
-                   "m": w.first.m, "r": w.first.r, "axis": w.first.axis or "2d", "pad": w.first.pad,
+                   "m": w.first.m, "r": w.first.r, "axis": w.first.axis or "2d",
+                   "layout": "nhwc" if w.first.nhwc else "nchw", "pad": w.first.pad,
                    "flags": hex(flags),
                    "launch": "eager" if graph is None else "hip_graph", "parallelism": "none"},
         "roofline": roof,
@@ -564,6 +578,8 @@ def main():
         from oracle import direct as odirect
         L0, g0 = w.first, gs[0]
         y_gpu = ys[0].detach().cpu().numpy()      # holds the last step's output (ReLU applied)
+        if L0.nhwc:
+            y_gpu = y_gpu.transpose(0, 3, 1, 2)
         reps_cpu, t_cpu, ref = 0, 0.0, None
         xin, pad_in = x, L0.pad
         if L0.axis:                    # 1-D layer: padding along the filtered axis only

@@ -219,6 +219,17 @@ int wino_conv2d_1d(const float* x, const float* U, float* y,
                    int N, int C, int H, int W, int K, int pad, int m, int r, int axis,
                    unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- channel-last tensors ---------------------------------------------------
+ * The 3x3 layer of wino_conv2d with x as [N][H][W][C] and y as [N][Ho][Wo][K]
+ * (NHWC, the layout the paper chooses for its channel-vectorised transforms,
+ * Sec. 2.1).  U comes from wino_filter_transform as before; the three stages
+ * run through the workspace (flags: WINO_ALGO_AUTO or _STAGED, and
+ * WINO_FLAG_RELU).  Errors as for wino_conv2d. */
+size_t wino_workspace_bytes_nhwc(int N, int C, int H, int W, int K, int pad, int m, unsigned flags);
+int wino_conv2d_nhwc(const float* x, const float* U, float* y,
+                     int N, int C, int H, int W, int K, int pad, int m,
+                     unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Glue between the blocks of a VGG-style stack (not part of the method):
  * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);

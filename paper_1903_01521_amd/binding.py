@@ -76,6 +76,8 @@ _SIGS = {
     "wino_filter_transform_1d": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
     "wino_workspace_bytes_1d": ([_c_int] * 9 + [_c_uint], _c_size),
     "wino_conv2d_1d": ([_vp, _vp, _vp] + [_c_int] * 9 + [_c_uint, _vp, _c_size, _vp], _c_int),
+    "wino_workspace_bytes_nhwc": ([_c_int] * 7 + [_c_uint], _c_size),
+    "wino_conv2d_nhwc": ([_vp, _vp, _vp] + [_c_int] * 7 + [_c_uint, _vp, _c_size, _vp], _c_int),
 }
 
 
@@ -242,6 +244,16 @@ def wino_conv2d_1d(x, U, y, N, C, H, W, K, pad, m, r, axis, flags=0, workspace=N
                    stream=None) -> int:
     return lib().wino_conv2d_1d(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, r, axis, flags,
                                 _ptr(workspace), workspace_bytes, _stream(stream))
+
+
+def wino_workspace_bytes_nhwc(N, C, H, W, K, pad, m, flags=0) -> int:
+    return lib().wino_workspace_bytes_nhwc(N, C, H, W, K, pad, m, flags)
+
+
+def wino_conv2d_nhwc(x, U, y, N, C, H, W, K, pad, m, flags=0, workspace=None, workspace_bytes=0,
+                     stream=None) -> int:
+    return lib().wino_conv2d_nhwc(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, flags,
+                                  _ptr(workspace), workspace_bytes, _stream(stream))
 
 
 def check(status: int, where: str = "wino") -> None:

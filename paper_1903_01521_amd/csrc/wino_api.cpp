@@ -43,7 +43,7 @@ int make_geom_r(int N, int C, int H, int W, int K, int pad, int m, int r, Geom* 
     if (!mul_ok(PB * CQ, T * 64, &v) || !mul_ok(PB * KB, T * 256, &mm)) return WINO_ERR_INVALID_ARG;
     g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
     g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
-    g->A = (int)A; g->T = (int)T; g->r = r; g->axis = 0;
+    g->A = (int)A; g->T = (int)T; g->r = r; g->axis = 0; g->nhwc = 0;
     g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
     return WINO_OK;
 }
@@ -73,7 +73,7 @@ int make_geom_1d(int N, int C, int H, int W, int K, int pad, int m, int r, int a
     if (!mul_ok(PB * CQ, 8 * 64, &v) || !mul_ok(PB * KB, 8 * 256, &mm)) return WINO_ERR_INVALID_ARG;
     g->N = N; g->C = C; g->H = H; g->W = W; g->K = K; g->pad = pad; g->m = m;
     g->Ho = (int)Ho; g->Wo = (int)Wo; g->th = (int)th; g->tw = (int)tw; g->P = (int)P;
-    g->A = 8; g->T = 8; g->r = r; g->axis = axis;
+    g->A = 8; g->T = 8; g->r = r; g->axis = axis; g->nhwc = 0;
     g->CQ = (int)CQ; g->KB = (int)KB; g->PB = (int)PB;
     return WINO_OK;
 }
@@ -150,9 +150,10 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
         return WINO_ERR_UNSUPPORTED;
     if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
-    // 5x5 and 1-D filters run the three stages (input transform, GEMMs,
-    // output transform); the one-kernel variants are written for 3x3 regions.
-    if (g.r != 3 || g.axis != 0) {
+    // 5x5 and 1-D filters and channel-last tensors run the three stages
+    // (input transform, GEMMs, output transform); the one-kernel variants are
+    // written for 3x3 regions of NCHW tensors.
+    if (g.r != 3 || g.axis != 0 || g.nhwc) {
         if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->algo = WINO_ALGO_STAGED;
@@ -404,6 +405,44 @@ int wino_conv2d_1d(const float* x, const float* U, float* y, int N, int C, int H
     const size_t xb = (size_t)N * C * H * W * sizeof(float);
     const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
     const size_t ub = wino_filter_bytes_1d(C, K, m, r);
+    if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
+    const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
+    const size_t need = vb + m_elems(g) * sizeof(float);
+    if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+    if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+        return WINO_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    float* V = (float*)workspace;
+    float* M = (float*)((char*)workspace + vb);
+    st = hip_status(launch_input_transform(x, V, g, s));
+    if (st != WINO_OK) return st;
+    st = hip_status(launch_batched_gemm(U, V, M, g, s));
+    if (st != WINO_OK) return st;
+    return hip_status(launch_output_transform(M, y, g, (flags & WINO_FLAG_RELU) != 0, s));
+}
+
+size_t wino_workspace_bytes_nhwc(int N, int C, int H, int W, int K, int pad, int m, unsigned flags) {
+    Geom g;
+    Plan p;
+    if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK) return (size_t)-1;
+    g.nhwc = 1;
+    if (make_plan(g, flags, &p) != WINO_OK) return (size_t)-1;
+    return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
+}
+
+int wino_conv2d_nhwc(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
+                     unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    int st = make_geom(N, C, H, W, K, pad, m, &g);
+    if (st != WINO_OK) return st;
+    g.nhwc = 1;
+    Plan p;
+    st = make_plan(g, flags, &p);
+    if (st != WINO_OK) return st;
+    const size_t xb = (size_t)N * C * H * W * sizeof(float);
+    const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
+    const size_t ub = wino_filter_bytes(C, K, m);
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
     const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
     const size_t need = vb + m_elems(g) * sizeof(float);

@@ -17,6 +17,7 @@ struct Geom {
     int A, T;       // alpha = m + r - 1; T = alpha^2 (2-D) or alpha (1-D)
     int r;          // filter side (the filter's length for 1-D layers)
     int axis;       // 0: r x r filter; 1: 1 x r (along W); 2: r x 1 (along H)
+    int nhwc;       // 1: x is [N][H][W][C] and y is [N][Ho][Wo][K] (three-stage path)
     int CQ, KB, PB; // 4-channel quads, 16-filter blocks, 16-tile blocks
 };
 

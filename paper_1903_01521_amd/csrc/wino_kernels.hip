@@ -1318,6 +1318,88 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
     }
 }
 
+// ------------------------------------------------------------------ NHWC
+// Channel-last tensors (x [N][H][W][C], y [N][Ho][Wo][K]) on the three-stage
+// path: only the input and output transforms see the layout; V, M and the GEMM
+// are the same.  Input: one wave per (16-tile block, channel quad), quads of a
+// block consecutive, each lane loading its region of one channel (the 4 lanes
+// of a tile read 16 contiguous bytes per pixel).  Output: one wave per (16-tile block,
+// 16-filter block); a lane holds its tile's four consecutive filters, so every
+// output pixel is one 16-byte store.
+template <int MT>
+__global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x, float* __restrict__ V, Geom g,
+                                                    long nwg) {
+    constexpr int A = MT + 2, T = A * A;
+    const int lane = threadIdx.x & 63;
+    const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nwg) return;
+    const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= (long)g.PB * g.CQ) return;
+    // channel quad fastest: the waves reading one pixel's C channels run together
+    const int pb = (int)(w / g.CQ), cq = (int)(w % g.CQ);
+    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const int c = cq * 4 + (lane >> 4);
+    const bool ok = tc.valid && c < g.C;
+    const float* xn = x + (size_t)tc.n * g.H * g.W * g.C + (ok ? c : 0);
+    const int r0 = tc.ti * MT - g.pad, c0 = tc.tj * MT - g.pad;
+    float d[A][A];
+#pragma unroll
+    for (int u = 0; u < A; ++u)
+#pragma unroll
+        for (int v = 0; v < A; ++v) {
+            const int row = r0 + u, col = c0 + v;
+            const bool in = ok && (unsigned)row < (unsigned)g.H && (unsigned)col < (unsigned)g.W;
+            d[u][v] = in ? xn[((size_t)row * g.W + col) * g.C] : 0.0f;
+        }
+    float vv[T];
+    input_tf<MT>(d, vv);
+    store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, vv);
+}
+
+template <int MT>
+__global__ __launch_bounds__(256) void k_output_nhwc(const float* __restrict__ M, float* __restrict__ y, Geom g,
+                                                     int relu, int vec_ok) {
+    constexpr int T = (MT + 2) * (MT + 2);
+    const int lane = threadIdx.x & 63;
+    const long w = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (long)g.PB * g.KB) return;
+    const int kb = (int)(w % g.KB);
+    const TileCoord tc = decode_tile((int)(w / g.KB) * 16 + (lane & 15), g);
+    const float* src = M + ((size_t)w * T) * 256 + lane * 4;
+    f32x4 mv[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) mv[t] = *(const f32x4*)(src + t * 256);
+    float o[4][MT][MT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float m1[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) m1[t] = mv[t][r];
+        output_tf<MT>(m1, o[r]);
+    }
+    if (!tc.valid) return;
+    const int k0 = kb * 16 + 4 * (lane >> 4);
+    if (k0 >= g.K) return;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            const int oi = tc.ti * MT + i, oj = tc.tj * MT + j;
+            if (oi >= g.Ho || oj >= g.Wo) continue;
+            float* py = y + (((size_t)tc.n * g.Ho + oi) * g.Wo + oj) * g.K + k0;
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = relu ? fmaxf(o[r][i][j], 0.0f) : o[r][i][j];
+            if (vec_ok && k0 + 4 <= g.K) {
+                *(float4*)py = make_float4(v[0], v[1], v[2], v[3]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (k0 + r < g.K) py[r] = v[r];
+            }
+        }
+}
+
 // ------------------------------------------------------------------ 1-D
 // 1 x r (axis 1, along W) and r x 1 (axis 2, along H) layers: regions of 8
 // inputs along the axis give m = 9 - r outputs; T = 8 transform positions, so
@@ -1495,6 +1577,11 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
     const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
+    if (g.nhwc) {
+        if (g.m == 2) hipLaunchKernelGGL(k_input_nhwc<2>, grid, block, 0, s, x, V, g, nwg);
+        else hipLaunchKernelGGL(k_input_nhwc<4>, grid, block, 0, s, x, V, g, nwg);
+        return hipGetLastError();
+    }
     if (g.r == 5)
         hipLaunchKernelGGL((k_input<2, 5>), grid, block, 0, s, x, V, g, nwg);
     else if (g.m == 2)
@@ -1515,6 +1602,15 @@ hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const G
 
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s) {
     if (g.axis != 0) return launch_output_1d(M, y, g, relu, s);
+    if (g.nhwc) {
+        const long waves = (long)g.PB * g.KB;
+        if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+        const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+        const int vk = (g.K % 4 == 0) && aligned(y, 16);
+        if (g.m == 2) hipLaunchKernelGGL(k_output_nhwc<2>, grid, block, 0, s, M, y, g, (int)relu, vk);
+        else hipLaunchKernelGGL(k_output_nhwc<4>, grid, block, 0, s, M, y, g, (int)relu, vk);
+        return hipGetLastError();
+    }
     const int vec_ok = (g.Wo % g.m == 0) && aligned(y, 4 * g.m);
     int R = 0, segs = 0, ipi;                      // items per image
     if (g.tw <= 64) {

@@ -30,6 +30,7 @@ class Layer:
     pool: bool = False        # 2x2/2 max-pool applied after (the ReLU of) this layer
     r: int = 3                # filter side (3, or 5 with m = 2), or a 1-D filter's length
     axis: str = ""            # "" for r x r filters; "w" for 1 x r, "h" for r x 1 (1-D layers)
+    nhwc: bool = False        # channel-last x and y (the generator still returns x as NCHW)
 
 
 @dataclass(frozen=True)
@@ -83,6 +84,8 @@ WORKLOADS = {w.name: w for w in [
              x_dist="uniform", note="low-C first layer, batch 1"),
     Workload("f2r5_n32_c48_k64_35x35", 32, (Layer(48, 64, 35, 35, m=2, pad=2, r=5),),
              note="5x5 layer shaped like Inception-v3's 5x5 branch, F(2x2,5x5)"),
+    Workload("f4_nhwc_n64_c256_k256_56x56", 64, (Layer(256, 256, 56, 56, m=4, nhwc=True),),
+             x_dist="uniform", note="the large-batch layer with channel-last tensors"),
     Workload("f2r7w_n32_c192_k160_17x17", 32, (Layer(192, 160, 17, 17, m=2, pad=3, r=7, axis="w"),),
              note="1x7 layer shaped like Inception-v3's 17x17 blocks, F(1x2,1x7,1x8)"),
     Workload("f2r7h_n32_c192_k160_17x17", 32, (Layer(192, 160, 17, 17, m=2, pad=3, r=7, axis="h"),),

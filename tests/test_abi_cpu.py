@@ -181,3 +181,19 @@ def test_1d_entry_points_reject():
     assert B.wino_conv2d_1d(FAKE, FAKE + 0x800000, y, 1, 4, 5, 5, 4, 0, 2, 7, B.WINO_AXIS_W, 0, None, 0,
                             None) == B.WINO_ERR_INVALID_ARG                           # Wo = -1
     assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG
+
+
+def test_nhwc_entry_points():
+    staged = B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_STAGED)
+    assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, 0) == staged
+    assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_FUSED) == 2**64 - 1
+    assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 3, 0) == 2**64 - 1
+    y = FAKE + 0x100000
+    conv = lambda **kw: B.wino_conv2d_nhwc(kw.get("x", FAKE), FAKE + 0x800000, kw.get("y", y), 1, 4, 8, 8, 4,
+                                           kw.get("pad", 1), kw.get("m", 4), kw.get("flags", 0), None, 0, None)
+    assert conv() == B.WINO_ERR_WORKSPACE
+    assert conv(m=3) == B.WINO_ERR_UNSUPPORTED
+    assert conv(flags=B.WINO_ALGO_LOWC) == B.WINO_ERR_UNSUPPORTED
+    assert conv(pad=-1) == B.WINO_ERR_INVALID_ARG
+    assert conv(x=None) == B.WINO_ERR_INVALID_ARG
+    assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG
