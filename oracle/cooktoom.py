@@ -470,3 +470,43 @@ def winograd_conv1d_f64(x: np.ndarray, g: np.ndarray, pad: int, m: int, axis: st
     U = filter_transform_1d(g, m)
     V = input_transform_1d(x, pad, m, r, axis)
     return output_transform_1d(batched_gemm(U, V), N, Ho, Wo, m, r, axis)
+
+
+# ----------------------------------------------------------------------------
+# 16-bit transform-domain operands (fp16 / bf16 GEMM with fp32 accumulation)
+# ----------------------------------------------------------------------------
+# A reduced-precision variant: U and V are rounded to a 16-bit format before
+# the T per-position GEMMs, which accumulate in higher precision; the output
+# transform is unchanged.  The reference below rounds the exact (fp64) U and V
+# once, to nearest with ties to even, and does everything else in fp64: it is
+# the definition the 16-bit GEMM path approximates up to fp32 accumulation and
+# the fp32 rounding of its transforms.
+
+def round_fp16(a: np.ndarray) -> np.ndarray:
+    """Nearest IEEE binary16 value (ties to even; overflow to inf), as fp64."""
+    return np.asarray(a, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
+def round_bf16(a: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 value (8-bit significand; ties to even), as fp64.
+
+    bfloat16 is the upper half of an IEEE binary32: round the fp64 value to the
+    nearest binary32 first only where that cannot change the bf16 result, i.e.
+    do the rounding in integer arithmetic on the fp64 bits directly."""
+    a = np.asarray(a, dtype=np.float64)
+    m, e = np.frexp(a)                      # a = m * 2^e, 0.5 <= |m| < 1
+    scaled = np.ldexp(m, 8)                 # 8 significant bits above the point
+    r = np.round(scaled)                    # numpy rounds half to even
+    out = np.ldexp(r, e - 8)
+    return np.where(a == 0, 0.0, out)
+
+
+def reduced_precision_conv_f64(x: np.ndarray, g: np.ndarray, pad: int, m: int, prec: str) -> np.ndarray:
+    """Output of the method when U and V are rounded to ``prec`` ('fp16' or
+    'bf16') and everything else is exact (fp64)."""
+    rnd = {"fp16": round_fp16, "bf16": round_bf16}[prec]
+    N, C, H, W = np.asarray(x).shape
+    Ho, Wo, _, _, _ = geometry(N, H, W, pad, m)
+    U = rnd(filter_transform(g, m))
+    V = rnd(input_transform(x, pad, m))
+    return output_transform(batched_gemm(U, V), N, Ho, Wo, m)
