@@ -39,6 +39,7 @@ import numpy as np
 
 HBM_PEAK = 8.0e12          # B/s, MI355X HBM3E
 FP32_MFMA_PEAK = 157.3e12  # FLOP/s, MI355X dense fp32 matrix
+FP16_MFMA_PEAK = 2.5e15    # FLOP/s, MI355X dense fp16 / bf16 matrix
 COPY_BYTES = 64 << 20      # size of the plain copy that calibrates the byte counters
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "paper_1903_01521_amd", "csrc")
@@ -50,7 +51,7 @@ AXIS = {"w": 1, "h": 2}   # WINO_AXIS_W, WINO_AXIS_H
 KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
-                "stages": "void wino::k_gemm"}
+                "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16"}
 
 
 def log(*a):
@@ -95,20 +96,24 @@ def layer_numbers(N, L):
         "maxpool": y_b + y_b // 4,
         # the three stages in one call (1-D and channel-last layers): x -> V -> M -> y
         "stages": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
+        # the same with 16-bit V and U (fp16 / bf16 GEMM operands)
+        "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
     }
-    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "stages": f["gemm_flops"]}
+    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "stages": f["gemm_flops"],
+                  "stages16": f["gemm_flops"]}
     return f
 
 
 def roofline(kind, nums, seconds):
     b = nums["bytes"].get(kind, 0)
     fl = nums["flops"].get(kind, 0)
+    peak = FP16_MFMA_PEAK if kind == "stages16" else FP32_MFMA_PEAK   # the GEMM's own operand type
     t_hbm = b / HBM_PEAK
-    t_mfma = fl / FP32_MFMA_PEAK
+    t_mfma = fl / peak
     if t_mfma >= t_hbm and fl > 0:
         ach = fl / seconds / 1e12
-        return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK / 1e12,
-                "unit": "TFLOP/s", "frac": round(ach / (FP32_MFMA_PEAK / 1e12), 4), "traffic": None,
+        return {"bound": "mfma", "achieved": round(ach, 3), "peak": peak / 1e12,
+                "unit": "TFLOP/s", "frac": round(ach / (peak / 1e12), 4), "traffic": None,
                 "algorithmic_flops": fl, "algorithmic_bytes": b}
     ach = b / seconds / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
@@ -285,6 +290,9 @@ def main():
     flags = args.flags if args.flags is not None else {
         "auto": B.WINO_ALGO_AUTO, "fused": B.WINO_ALGO_FUSED, "staged": B.WINO_ALGO_STAGED}[args.algo]
     staged = (flags & B.WINO_ALGO_MASK) == B.WINO_ALGO_STAGED
+    prec = flags & B.WINO_PREC_MASK       # 16-bit GEMM operands (reduced precision, opt-in)
+    if prec:
+        staged = False                    # the three stages run inside one wino_conv2d call
 
     x, gs = wl.generate(w)
     dev = torch.device("cuda:0")
@@ -298,7 +306,12 @@ def main():
     H, W = w.first.H, w.first.W
     for L, f in zip(w.layers, nums):
         assert (L.H, L.W) == (H, W)
-        ub = B.wino_filter_bytes_1d(L.C, L.K, L.m, L.r) if L.axis else B.wino_filter_bytes_r(L.C, L.K, L.m, L.r)
+        if L.axis:
+            ub = B.wino_filter_bytes_1d(L.C, L.K, L.m, L.r)
+        elif prec:
+            ub = B.wino_filter_bytes_p(L.C, L.K, L.m, prec)
+        else:
+            ub = B.wino_filter_bytes_r(L.C, L.K, L.m, L.r)
         Us.append(torch.empty(ub // 4, dtype=torch.float32, device=dev))
         ys.append(torch.empty((N, f["Ho"], f["Wo"], L.K) if L.nhwc else (N, L.K, f["Ho"], f["Wo"]),
                               dtype=torch.float32, device=dev))
@@ -349,9 +362,13 @@ def main():
                                                                           flags | relu, ws, wsb, sp))))
                 a = ys[i]
                 continue
-            out.append((f"L{i}.filter", i, "filter",
-                        (lambda sp, i=i, L=L: B.wino_filter_transform_r(hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
-            if staged or L.r != 3:         # 5x5 layers run the three stages
+            if prec:
+                out.append((f"L{i}.filter", i, "filter", (lambda sp, i=i, L=L: B.wino_filter_transform_p(
+                    hg[i], Us[i], L.C, L.K, L.m, prec, sp))))
+            else:
+                out.append((f"L{i}.filter", i, "filter",
+                            (lambda sp, i=i, L=L: B.wino_filter_transform_r(hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
+            if (staged or L.r != 3) and not prec:   # 5x5 layers run the three stages
                 out.append((f"L{i}.input", i, "input", (lambda sp, i=i, L=L, a=a: B.wino_input_transform_r(
                     a, Vs[i], N, L.C, L.H, L.W, L.pad, L.m, L.r, sp))))
                 out.append((f"L{i}.gemm", i, "gemm", (lambda sp, i=i, L=L: B.wino_batched_gemm_r(
@@ -362,7 +379,8 @@ def main():
                 ws, wsb = wss[i]
                 algo = flags & B.WINO_ALGO_MASK
                 lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4)
-                out.append((f"L{i}.conv", i, "lowc" if lowc else "fused", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                kind = "stages16" if prec else "lowc" if lowc else "fused"
+                out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                        L.pad, L.m, L.r, flags | relu,
                                                                      ws if wsb else None, wsb, sp))))
@@ -548,7 +566,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": {0: "f32", B.WINO_PREC_F16: "f16 operands, f32 accumulate",
+                  B.WINO_PREC_BF16: "bf16 operands, f32 accumulate"}[prec],
         "data": "synthetic",
         "config": {"workload": name, "N": N, "layers": len(w.layers),
                    "C": w.first.C, "K": w.first.K, "H": w.first.H, "W": w.first.W,

@@ -81,6 +81,15 @@ extern "C" {
 #define WINO_ALGO_LOWC     0x400u   /* one kernel for C <= 4 (a network's first layer): a
                                        lane per tile, vector FMAs over the channels */
 #define WINO_ALGO_MASK     0xF00u
+/* Reduced-precision GEMM operands (three-stage algorithm, 3x3 NCHW layers only):
+ * U and V rounded to fp16 or bf16 (nearest, ties to even), the T per-position
+ * GEMMs on 16-bit MFMA with fp32 accumulation, M and the output transform in
+ * fp32.  U must come from wino_filter_transform_p with the same format.  Not
+ * within the fp32 gates: measured normwise errors against the exact result are
+ * about 5e-4 (fp16) and 4e-3 (bf16) for m = 2, 7e-3 and 6e-2 for m = 4. */
+#define WINO_PREC_F16      0x010u
+#define WINO_PREC_BF16     0x020u
+#define WINO_PREC_MASK     0x030u
 /* Optional overrides of the fused kernel's variant (0 = planner's choice):
  *   WINO_BLOCK_1x16 / WINO_BLOCK_4x4: a workgroup's 16 tiles are one row of 16
  *                  tiles, or a 4 x 4 square of tiles;
@@ -160,6 +169,16 @@ int wino_batched_gemm(const float* U, const float* V, float* M,
  * the m x m block into y (NCHW), cropped to Ho x Wo.  flags: WINO_FLAG_RELU. */
 int wino_output_transform(const float* M, float* y, int N, int K, int H, int W,
                           int pad, int m, unsigned flags, void* stream);
+
+/* Transformed filters in a 16-bit GEMM format (prec = WINO_PREC_F16 or
+ * WINO_PREC_BF16; 0 gives the fp32 calls above):
+ *   UH[KB][C16][T][64][4] 16-bit values, C16 = ceil(C/16): element (t,c,k) at
+ *   lane ((c%16)/4)*16 + k%16, half c%4 of group (k/16, c/16, t) -- one 8-byte
+ *   word per lane, the A operand of v_mfma_f32_16x16x16 (four consecutive
+ *   channels per lane).  Each value is G g G^T in fp64, rounded to fp32, then to
+ *   the 16-bit format.  Bytes: 2*T*roundup(C,16)*roundup(K,16). */
+size_t wino_filter_bytes_p(int C, int K, int m, unsigned prec);
+int wino_filter_transform_p(const float* g, void* U, int C, int K, int m, unsigned prec, void* stream);
 
 /* ---- 5x5 filters: F(2x2,5x5) ----------------------------------------------
  * The same method for r x r filters (Eq. 1 with a 5x5 filter; the paper's

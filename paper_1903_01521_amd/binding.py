@@ -77,6 +77,8 @@ _SIGS = {
     "wino_workspace_bytes_1d": ([_c_int] * 9 + [_c_uint], _c_size),
     "wino_conv2d_1d": ([_vp, _vp, _vp] + [_c_int] * 9 + [_c_uint, _vp, _c_size, _vp], _c_int),
     "wino_workspace_bytes_nhwc": ([_c_int] * 7 + [_c_uint], _c_size),
+    "wino_filter_bytes_p": ([_c_int] * 3 + [_c_uint], _c_size),
+    "wino_filter_transform_p": ([_vp, _vp] + [_c_int] * 3 + [_c_uint, _vp], _c_int),
     "wino_conv2d_nhwc": ([_vp, _vp, _vp] + [_c_int] * 7 + [_c_uint, _vp, _c_size, _vp], _c_int),
 }
 
@@ -222,6 +224,19 @@ def wino_batched_gemm_r(U, V, M, N, C, H, W, K, pad, m, r, stream=None) -> int:
 
 def wino_output_transform_r(M, y, N, K, H, W, pad, m, r, flags=0, stream=None) -> int:
     return lib().wino_output_transform_r(_fptr(M), _fptr(y), N, K, H, W, pad, m, r, flags, _stream(stream))
+
+
+WINO_PREC_F16 = 0x010
+WINO_PREC_BF16 = 0x020
+WINO_PREC_MASK = 0x030
+
+
+def wino_filter_bytes_p(C, K, m, prec) -> int:
+    return lib().wino_filter_bytes_p(C, K, m, prec)
+
+
+def wino_filter_transform_p(g, U, C, K, m, prec, stream=None) -> int:
+    return lib().wino_filter_transform_p(_fptr(g), _ptr(U), C, K, m, prec, _stream(stream))
 
 
 WINO_AXIS_W = 1

@@ -13,7 +13,17 @@ constexpr int64_t kMaxElems = (int64_t)1 << 40;      // per tensor, well inside 
 constexpr int64_t kMaxTiles = ((int64_t)1 << 31) - 64;
 
 constexpr unsigned kBlockMask = WINO_BLOCK_1x16 | WINO_BLOCK_4x4, kCsplitShift = 16;
-constexpr unsigned kKnownFlags = WINO_FLAG_RELU | WINO_ALGO_MASK | kBlockMask | (0xFu << kCsplitShift);
+constexpr unsigned kKnownFlags =
+    WINO_FLAG_RELU | WINO_PREC_MASK | WINO_ALGO_MASK | kBlockMask | (0xFu << kCsplitShift);
+
+// 16-bit GEMM operand format from the flags: 0 (fp32), 1 (fp16), 2 (bf16), -1 (invalid).
+int prec_of(unsigned flags) {
+    const unsigned p = flags & WINO_PREC_MASK;
+    return p == 0 ? 0 : p == WINO_PREC_F16 ? 1 : p == WINO_PREC_BF16 ? 2 : -1;
+}
+
+size_t c16_elems(const Geom& g) { return (size_t)(g.C + 15) / 16; }
+size_t vh_bytes(const Geom& g) { return (size_t)g.PB * c16_elems(g) * g.T * 64 * 8; }
 
 // Checked product of non-negative int64 values; false on overflow past kMaxElems.
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
@@ -153,7 +163,10 @@ int make_plan(const Geom& g, unsigned flags, Plan* p) {
     // 5x5 and 1-D filters and channel-last tensors run the three stages
     // (input transform, GEMMs, output transform); the one-kernel variants are
     // written for 3x3 regions of NCHW tensors.
-    if (g.r != 3 || g.axis != 0 || g.nhwc) {
+    const int prec = prec_of(flags);
+    if (prec < 0) return WINO_ERR_UNSUPPORTED;
+    if (prec && (g.r != 3 || g.axis != 0 || g.nhwc)) return WINO_ERR_UNSUPPORTED;
+    if (g.r != 3 || g.axis != 0 || g.nhwc || prec) {
         if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->algo = WINO_ALGO_STAGED;
@@ -224,6 +237,15 @@ size_t wino_filter_bytes_r(int C, int K, int m, int r) {
 
 size_t wino_filter_bytes(int C, int K, int m) { return wino_filter_bytes_r(C, K, m, 3); }
 
+size_t wino_filter_bytes_p(int C, int K, int m, unsigned prec) {
+    if (prec == 0) return wino_filter_bytes(C, K, m);
+    if (C <= 0 || K <= 0 || (m != 2 && m != 4) || prec_of(prec) <= 0 || (prec & ~WINO_PREC_MASK)) return 0;
+    int64_t e;
+    if (!mul_ok((int64_t)(C + 15) / 16 * 16, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, (m + 2) * (m + 2), &e))
+        return 0;
+    return (size_t)e * 2;
+}
+
 size_t wino_input_tf_bytes_r(int N, int C, int H, int W, int pad, int m, int r) {
     Geom g;
     if (make_geom_r(N, C, H, W, 1, pad, m, r, &g) != WINO_OK) return 0;
@@ -249,6 +271,7 @@ size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m,
     Plan p;
     if (make_geom_r(N, C, H, W, K, pad, m, r, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
+    if (prec_of(flags)) return round_up(vh_bytes(g), 256) + m_elems(g) * sizeof(float);
     if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
     if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
@@ -271,6 +294,16 @@ int wino_filter_transform(const float* gw, float* U, int C, int K, int m, void* 
     return wino_filter_transform_r(gw, U, C, K, m, 3, stream);
 }
 
+int wino_filter_transform_p(const float* gw, void* U, int C, int K, int m, unsigned prec, void* stream) {
+    if (prec == 0) return wino_filter_transform(gw, (float*)U, C, K, m, stream);
+    if (!gw || !U || C <= 0 || K <= 0) return WINO_ERR_INVALID_ARG;
+    if ((m != 2 && m != 4) || prec_of(prec) <= 0 || (prec & ~WINO_PREC_MASK)) return WINO_ERR_UNSUPPORTED;
+    const size_t ub = wino_filter_bytes_p(C, K, m, prec);
+    if (ub == 0) return WINO_ERR_INVALID_ARG;
+    if (overlap(gw, (size_t)K * C * 9 * sizeof(float), U, ub)) return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_filter_transform16(gw, U, C, K, m, prec_of(prec), (hipStream_t)stream));
+}
+
 int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad, int m,
                   int r, unsigned flags, void* workspace, size_t workspace_bytes, void* stream) {
     if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
@@ -282,10 +315,19 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
     if (st != WINO_OK) return st;
     const size_t xb = (size_t)N * C * H * W * sizeof(float);
     const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
-    const size_t ub = wino_filter_bytes_r(C, K, m, r);
+    const int prec = prec_of(flags);
+    const size_t ub = prec ? wino_filter_bytes_p(C, K, m, flags & WINO_PREC_MASK) : wino_filter_bytes_r(C, K, m, r);
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
     const bool relu = (flags & WINO_FLAG_RELU) != 0;
     hipStream_t s = (hipStream_t)stream;
+    if (prec) {
+        const size_t vb = round_up(vh_bytes(g), 256);
+        const size_t need = vb + m_elems(g) * sizeof(float);
+        if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+        if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+            return WINO_ERR_INVALID_ARG;
+        return hip_status(launch_staged16(x, U, y, workspace, (float*)((char*)workspace + vb), g, prec, relu, s));
+    }
     if (p.algo == WINO_ALGO_SPLIT) {
         const size_t need = split_workspace(g, p.cfg.bw);
         if (!workspace || workspace_bytes < need) {

@@ -61,5 +61,10 @@ hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int 
 // input and output transforms dispatch on g.axis inside launch_input_transform
 // and launch_output_transform.
 hipError_t launch_filter_transform_1d(const float* g, float* U, int C, int K, int m, int r, hipStream_t s);
+// 16-bit GEMM operands (prec 1: fp16, 2: bf16): filter transform into UH, and
+// the three stages through VH (16-bit) and M (fp32).
+hipError_t launch_filter_transform16(const float* g, void* UH, int C, int K, int m, int prec, hipStream_t s);
+hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, float* M, const Geom& g, int prec,
+                           bool relu, hipStream_t s);
 
 }  // namespace wino

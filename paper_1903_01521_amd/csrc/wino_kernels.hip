@@ -1318,6 +1318,246 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
     }
 }
 
+// ------------------------------------------------------------------ 16-bit operands
+// Reduced-precision three-stage path: U and V are rounded to fp16 (PREC 1) or
+// bf16 (PREC 2), to nearest with ties to even, and the T per-position GEMMs run
+// on v_mfma_f32_16x16x16_{f16,bf16} with fp32 accumulation; M and the output
+// transform stay fp32.  MFMA lane layout (16 x 16 x 16): lane l holds A[l%16]
+// [4*(l/16) .. +3] and B[4*(l/16) .. +3][l%16]; D as for the fp32 MFMA.  So a
+// lane carries four consecutive channels, and the 16-bit layouts are
+//   UH[KB][C16][T][64][4]: element (t, c, k) at lane ((c%16)/4)*16 + k%16, half c%4
+//   VH[PB][C16][T][64][4]: element (t, c, p) at lane ((c%16)/4)*16 + p%16, half c%4
+// (C16 = ceil(C/16), padding zero): one 8-byte word per lane and position.
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+template <int PREC>
+__device__ __forceinline__ uint32_t to16(float v) {
+    if constexpr (PREC == 1) {
+        return (uint32_t)__builtin_bit_cast(unsigned short, (_Float16)v);
+    } else {
+        const uint32_t u = __builtin_bit_cast(uint32_t, v);
+        if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;        // NaN stays NaN
+        return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;               // nearest, ties to even
+    }
+}
+
+template <int PREC>
+__device__ __forceinline__ uint2 pack16(float a, float b, float c, float d) {
+    return make_uint2(to16<PREC>(a) | (to16<PREC>(b) << 16), to16<PREC>(c) | (to16<PREC>(d) << 16));
+}
+
+template <int PREC>
+__device__ __forceinline__ f32x4 mfma16x16x16(uint2 a, uint2 b, f32x4 c) {
+    if constexpr (PREC == 1)
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b),
+                                                      c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
+                                                          __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
+}
+
+// One wave per (16-filter block, 16-channel group): lane = (k%16, channel
+// quad); four channels' transforms per lane, one 8-byte store per position.
+template <int MT, int PREC, int... G>
+__device__ __forceinline__ void filter16_groups(const float (&gg)[4][3][3], uint2* __restrict__ dst,
+                                                std::integer_sequence<int, G...>) {
+    auto one = [&](auto gc) {
+        constexpr int GG = decltype(gc)::value;
+        float4 f[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f[e] = filter_tf4<MT, 4 * GG>(gg[e]);
+        dst[(4 * GG + 0) * 64] = pack16<PREC>(f[0].x, f[1].x, f[2].x, f[3].x);
+        dst[(4 * GG + 1) * 64] = pack16<PREC>(f[0].y, f[1].y, f[2].y, f[3].y);
+        dst[(4 * GG + 2) * 64] = pack16<PREC>(f[0].z, f[1].z, f[2].z, f[3].z);
+        dst[(4 * GG + 3) * 64] = pack16<PREC>(f[0].w, f[1].w, f[2].w, f[3].w);
+    };
+    (one(std::integral_constant<int, G>{}), ...);
+}
+
+template <int MT, int PREC>
+__global__ __launch_bounds__(256) void k_filter16(const float* __restrict__ gw, uint2* __restrict__ UH, int C,
+                                                  int K, int C16, long nw) {
+    constexpr int T = (MT + 2) * (MT + 2), TG = T / 4;
+    const int lane = threadIdx.x & 63;
+    const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= nw) return;
+    const int kb = (int)(w / C16), c16 = (int)(w % C16);
+    const int k = kb * 16 + (lane & 15), c0 = c16 * 16 + (lane >> 4) * 4;
+    float gg[4][3][3];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const bool ok = k < K && c0 + e < C;
+        const float* src = gw + ((size_t)(ok ? k : 0) * C + (ok ? c0 + e : 0)) * 9;
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+            for (int s2 = 0; s2 < 3; ++s2) gg[e][r][s2] = ok ? src[r * 3 + s2] : 0.0f;
+    }
+    filter16_groups<MT, PREC>(gg, UH + (size_t)w * T * 64 + lane, std::make_integer_sequence<int, TG>{});
+}
+
+// One wave per (16-tile block, 16-channel group), XCD-contiguous runs; lane =
+// (tile p%16, channel quad): four regions, their transforms packed four
+// channels to an 8-byte word.
+template <int MT, int PREC>
+__global__ __launch_bounds__(256) void k_input16(const float* __restrict__ x, uint2* __restrict__ VH, Geom g,
+                                                 int C16, long nwg) {
+    constexpr int A = MT + 2, T = A * A;
+    const int lane = threadIdx.x & 63;
+    const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nwg) return;
+    const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= (long)g.PB * C16) return;
+    const int pb = (int)(w / C16), c16 = (int)(w % C16);
+    const int cq4 = lane >> 4;                                  // channel quad within the group
+    const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
+    const RegionPlan<MT> rp = make_region_plan<MT>(x, g, pb * 16, tc, cq4 * 4);
+    uint32_t ph[T][2];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        // channel c16*16 + cq4*4 + e: the plan holds cq4*4, the wave-uniform
+        // offset adds c16*16 + e planes
+        const uint32_t chan = (c16 * 16 + cq4 * 4 + e < g.C) ? 0u : kInvalid;
+        const int soff = __builtin_amdgcn_readfirstlane((c16 * 16 + e) * (int)rp.plane_bytes);
+        float d[A][A];
+#pragma unroll
+        for (int u = 0; u < A; ++u) {
+            const uint32_t rowq = rp.row[u] + chan;
+#pragma unroll
+            for (int v = 0; v < A; ++v)
+                d[u][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                              rp.rsrc, (int)(rowq + rp.col[v]), soff, 0));
+        }
+        float vv[T];
+        input_tf<MT>(d, vv);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const uint32_t hbits = to16<PREC>(vv[t]);
+            if (e & 1) ph[t][e >> 1] |= hbits << 16;
+            else ph[t][e >> 1] = hbits;
+        }
+    }
+    uint2* dst = VH + ((size_t)pb * C16 + c16) * T * 64 + lane;
+#pragma unroll
+    for (int t = 0; t < T; ++t) dst[t * 64] = make_uint2(ph[t][0], ph[t][1]);
+}
+
+// The T GEMMs on 16-bit operands: workgroup = 4 positions x 4 k-blocks x 4
+// p-blocks as in k_gemm (same XCD-contiguous item order), 16 channels per
+// chunk through an LDS double buffer, 16 MFMAs per wave and chunk.
+template <int PREC>
+__global__ __launch_bounds__(256) void k_gemm16(const uint2* __restrict__ UH, const uint2* __restrict__ VH,
+                                                float* __restrict__ M, Geom g, int C16) {
+    __shared__ uint2 As[2][4][4][64];    // [buf][position][k-block][lane]
+    __shared__ uint2 Bs[2][4][4][64];    // [buf][position][p-block][lane]
+    const int T = g.T, TG = g.T / 4;
+    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
+    const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
+    const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nitems) return;
+    const int kb0 = (int)(item % KB4) * 4;
+    const long rest = item / KB4;
+    const int pb0 = (int)(rest % PB4) * 4;
+    const int tg = (int)(rest / PB4);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wk = wave >> 1, wp = wave & 1;
+
+    // Loader: a chunk is 16 A and 16 B blocks (position x block) of 64 words;
+    // thread tid moves word (tid & 63) of blocks (tid >> 6) + 4*i, i < 4.
+    uint2 ra[4], rb[4];
+    auto fetch = [&](int c16) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int blk = (tid >> 6) + 4 * i, t4 = blk >> 2, bi = blk & 3;
+            const int kb = kb0 + bi, pb = pb0 + bi, t = 4 * tg + t4;
+            ra[i] = make_uint2(0u, 0u);
+            rb[i] = ra[i];
+            if (kb < g.KB) ra[i] = UH[(((size_t)kb * C16 + c16) * T + t) * 64 + lane];
+            if (pb < g.PB) rb[i] = VH[(((size_t)pb * C16 + c16) * T + t) * 64 + lane];
+        }
+    };
+    auto stage = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int blk = (tid >> 6) + 4 * i;
+            As[buf][blk >> 2][blk & 3][lane] = ra[i];
+            Bs[buf][blk >> 2][blk & 3][lane] = rb[i];
+        }
+    };
+    f32x4 acc[4][2][2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    fetch(0);
+    stage(0);
+    __syncthreads();
+    for (int ch = 0; ch < C16; ++ch) {
+        const int buf = ch & 1;
+        if (ch + 1 < C16) fetch(ch + 1);
+#pragma unroll
+        for (int t4 = 0; t4 < 4; ++t4) {
+            const uint2 a0 = As[buf][t4][wk * 2 + 0][lane], a1 = As[buf][t4][wk * 2 + 1][lane];
+            const uint2 b0 = Bs[buf][t4][wp * 2 + 0][lane], b1 = Bs[buf][t4][wp * 2 + 1][lane];
+            acc[t4][0][0] = mfma16x16x16<PREC>(a0, b0, acc[t4][0][0]);
+            acc[t4][0][1] = mfma16x16x16<PREC>(a0, b1, acc[t4][0][1]);
+            acc[t4][1][0] = mfma16x16x16<PREC>(a1, b0, acc[t4][1][0]);
+            acc[t4][1][1] = mfma16x16x16<PREC>(a1, b1, acc[t4][1][1]);
+        }
+        if (ch + 1 < C16) stage(buf ^ 1);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
+                if (kb < g.KB && pb < g.PB)
+                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
+            }
+}
+
+hipError_t launch_filter_transform16(const float* gw, void* UH, int C, int K, int m, int prec, hipStream_t s) {
+    const int C16 = (C + 15) / 16, KB = (K + 15) / 16;
+    const long waves = (long)KB * C16;
+    if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    uint2* u = (uint2*)UH;
+    if (m == 2 && prec == 1) hipLaunchKernelGGL((k_filter16<2, 1>), grid, block, 0, s, gw, u, C, K, C16, waves);
+    else if (m == 2) hipLaunchKernelGGL((k_filter16<2, 2>), grid, block, 0, s, gw, u, C, K, C16, waves);
+    else if (prec == 1) hipLaunchKernelGGL((k_filter16<4, 1>), grid, block, 0, s, gw, u, C, K, C16, waves);
+    else hipLaunchKernelGGL((k_filter16<4, 2>), grid, block, 0, s, gw, u, C, K, C16, waves);
+    return hipGetLastError();
+}
+
+hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, float* M, const Geom& g, int prec,
+                           bool relu, hipStream_t s) {
+    const int C16 = (g.C + 15) / 16;
+    const long waves = (long)g.PB * C16, nwg = (waves + 3) / 4;
+    if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 gi((unsigned)((nwg + 7) / 8 * 8)), block(256);
+    uint2* vh = (uint2*)VH;
+    if (g.m == 2 && prec == 1) hipLaunchKernelGGL((k_input16<2, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
+    else if (g.m == 2) hipLaunchKernelGGL((k_input16<2, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
+    else if (prec == 1) hipLaunchKernelGGL((k_input16<4, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
+    else hipLaunchKernelGGL((k_input16<4, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
+    const long wgs = (nitems + 7) / 8 * 8;
+    if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    if (prec == 1) hipLaunchKernelGGL((k_gemm16<1>), dim3((unsigned)wgs), block, 0, s, (const uint2*)UH, vh, M, g, C16);
+    else hipLaunchKernelGGL((k_gemm16<2>), dim3((unsigned)wgs), block, 0, s, (const uint2*)UH, vh, M, g, C16);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_output_transform(M, y, g, relu, s);
+}
+
 // ------------------------------------------------------------------ NHWC
 // Channel-last tensors (x [N][H][W][C], y [N][Ho][Wo][K]) on the three-stage
 // path: only the input and output transforms see the layout; V, M and the GEMM

@@ -197,3 +197,25 @@ def test_nhwc_entry_points():
     assert conv(pad=-1) == B.WINO_ERR_INVALID_ARG
     assert conv(x=None) == B.WINO_ERR_INVALID_ARG
     assert conv(y=FAKE + 64) == B.WINO_ERR_INVALID_ARG
+
+
+def test_16bit_operand_entry_points():
+    F16, BF16 = B.WINO_PREC_F16, B.WINO_PREC_BF16
+    # UH: 2 bytes x T x roundup(C,16) x roundup(K,16)
+    assert B.wino_filter_bytes_p(20, 20, 4, F16) == 2 * 36 * 32 * 32
+    assert B.wino_filter_bytes_p(20, 20, 2, BF16) == 2 * 16 * 32 * 32
+    assert B.wino_filter_bytes_p(20, 20, 4, 0) == B.wino_filter_bytes(20, 20, 4)
+    assert B.wino_filter_bytes_p(20, 20, 4, 0x30) == 0          # both formats at once
+    assert B.wino_filter_bytes_p(20, 20, 3, F16) == 0
+    # workspace: VH (8 bytes per lane and position) + fp32 M
+    ws = B.wino_workspace_bytes(1, 20, 16, 16, 20, 1, 4, F16)
+    vh = 1 * 2 * 36 * 64 * 8                                  # PB = 1 (16 tiles), C16 = 2
+    assert ws == (vh + 255) // 256 * 256 + B.wino_gemm_out_bytes(1, 20, 16, 16, 1, 4)
+    for flags in (F16 | B.WINO_ALGO_FUSED, BF16 | B.WINO_ALGO_SPLIT, F16 | B.WINO_ALGO_LOWC, 0x30):
+        assert B.wino_workspace_bytes(1, 20, 16, 16, 20, 1, 4, flags) == 2**64 - 1
+    assert B.wino_workspace_bytes_r(1, 20, 16, 16, 20, 2, 2, 5, F16) == 2**64 - 1   # 3x3 only
+    assert B.wino_filter_transform_p(None, FAKE, 4, 4, 4, F16) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_filter_transform_p(FAKE, FAKE + 0x10000, 4, 4, 4, 0x40) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_filter_transform_p(FAKE, FAKE + 8, 4, 4, 4, F16) == B.WINO_ERR_INVALID_ARG     # overlap
+    assert _conv(flags=F16) == B.WINO_ERR_WORKSPACE
+    assert _conv(flags=F16 | B.WINO_ALGO_FUSED) == B.WINO_ERR_UNSUPPORTED
