@@ -41,6 +41,7 @@ HBM_PEAK = 8.0e12          # B/s, MI355X HBM3E
 FP32_MFMA_PEAK = 157.3e12  # FLOP/s, MI355X dense fp32 matrix
 FP16_MFMA_PEAK = 2.5e15    # FLOP/s, MI355X dense fp16 / bf16 matrix
 COPY_BYTES = 64 << 20      # size of the plain copy that calibrates the byte counters
+EVICT_BYTES = 512 << 20    # read before each cold launch: twice the 256 MB last-level cache
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "paper_1903_01521_amd", "csrc")
 PROFILES = os.path.join(HERE, "profiles")
@@ -472,7 +473,7 @@ def main():
     # durations below show what each kernel takes after its real predecessors.
     R = 20
     reps = max(1, min(args.steps // 10, 50))
-    per_launch = []
+    per_launch, per_launch_spread = [], []
     for label, _, _, fn in step:
         if args.no_graphs:
             g = None
@@ -491,6 +492,7 @@ def main():
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1) / R)
         per_launch.append(float(np.median(ts)))
+        per_launch_spread.append((float(np.percentile(ts, 10)), float(np.percentile(ts, 90))))
         launch_r = g = None
 
     # In-sequence durations: HIP events around every launch of KP more eager
@@ -525,6 +527,37 @@ def main():
     in_seq = [float(np.mean([evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(KP)]))
               for i in range(len(step))]
     torch.cuda.synchronize()
+
+    # Cold durations: before a launch a 512 MB read (a reduction into one
+    # float) evicts L2 and the last-level cache, so the launch reads its inputs
+    # from HBM; the same launch then runs once more, warm.  Both are timed with
+    # HIP events in the enqueue-while-held scheme above; the cold figure is the
+    # graph-timed duration plus the cold-minus-warm difference of those events,
+    # so the events' own dispatch latency cancels.
+    KC = max(3, min(10, 300 // len(step)))
+    evict_src = torch.empty(EVICT_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    evict_dst = torch.empty((), dtype=torch.float32, device=dev)
+    cev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in step] for _ in range(KC)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(20.0 * cyc_per_ms))
+    for k in range(KC):
+        for i, (label, _, _, fn) in enumerate(step):
+            ev = cev[k][i]
+            torch.sum(evict_src, dim=0, out=evict_dst)
+            ev[0].record(stream)
+            st = fn(sp)
+            ev[1].record(stream)
+            st |= fn(sp)
+            ev[2].record(stream)
+            if st != 0:
+                raise RuntimeError(f"{label}: {B.wino_status_string(st)}")
+    torch.cuda.synchronize()
+    cold = []
+    for i in range(len(step)):
+        c = [cev[k][i][0].elapsed_time(cev[k][i][1]) for k in range(KC)]
+        wm = float(np.median([cev[k][i][1].elapsed_time(cev[k][i][2]) for k in range(KC)]))
+        cold.append([per_launch[i] + ck - wm for ck in c])
+    del evict_src
 
     total_by = {}
     for (label, li, kind, _), t in zip(step, per_launch):
@@ -580,6 +613,13 @@ def main():
         "per_kind_us": {k: round(t * 1e3, 3) for k, t in total_by.items()},
         "per_launch_in_sequence_us": {lbl: round(t * 1e3, 3) for (lbl, *_), t in zip(step, in_seq)},
         "in_sequence_timing": {"steps": KP, "host_gaps": not gapless},
+        # graph-timed launches: p10 / median / p90 over the replays
+        "per_launch_spread_us": {lbl: [round(a * 1e3, 3), round(t * 1e3, 3), round(b * 1e3, 3)]
+                                 for (lbl, *_), t, (a, b) in zip(step, per_launch, per_launch_spread)},
+        # after evicting L2 and the last-level cache: p10 / median / p90
+        "per_launch_cold_us": {lbl: [round(float(np.percentile(c, q)) * 1e3, 3) for q in (10, 50, 90)]
+                               for (lbl, *_), c in zip(step, cold)},
+        "cold_timing": {"launches": KC, "evict_bytes": EVICT_BYTES},
         # every launch against the roof that bounds it (algorithmic work / duration)
         "per_launch_roofline": {lbl: (lambda r: f"{r['bound']} {r['frac']:.3f}")(
             roofline(kind, nums[li], t / 1e3)) for (lbl, li, kind, _), t in zip(step, per_launch)},

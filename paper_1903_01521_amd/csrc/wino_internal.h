@@ -27,6 +27,14 @@ struct FusedCfg {
     int bw;         // tile-block width: 16 (1 x 16 tiles) or 4 (4 x 4 tiles)
 };
 
+// Division of n < 2^31 by a fixed d >= 1 as ((mulhi(n, m) + n) >> l), with
+// l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1 (Granlund and
+// Montgomery's round-up method; mulhi(n, m) + n < 2^32 for such n).
+struct FastDiv {
+    uint32_t m;
+    int l;
+};
+
 // Runtime part of the fused kernel's work decomposition (host-computed).
 struct FusedTiling {
     int nbh, nbw;   // tile blocks per image along rows / columns
@@ -36,6 +44,9 @@ struct FusedTiling {
     int nsteps;     // channel steps, ceil(CQ / csplit)
     int kfast;      // item order: 1 = filter group fastest (tile major), 0 = group major
     int bw;         // split path: tile-block width (16 or 4)
+    FastDiv d_item; // fused path: item -> (quotient, remainder) by nkg (kfast) or nt
+    FastDiv d_img;  // by nbh * nbw (tile blocks per image)
+    FastDiv d_nbw;  // by nbw
 };
 
 size_t filter_elems(int C, int K, int m, int r);         // T*Cp*Kp

@@ -36,6 +36,8 @@ __device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c) {
 
 // ------------------------------------------------------------------ helpers
 
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) { return (__umulhi(n, d.m) + n) >> d.l; }
+
 struct TileCoord {
     int n, ti, tj;
     bool valid;
@@ -732,11 +734,12 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     const int b = blockIdx.x;
     const int item = (b & 7) * ft.per + (b >> 3);
     if (item >= ft.nt * ft.nkg) return;
-    const int kgi = ft.kfast ? item % ft.nkg : item / ft.nt;
-    const int tb = ft.kfast ? item / ft.nkg : item - kgi * ft.nt;
-    const int per_img = ft.nbh * ft.nbw;
-    const int n = tb / per_img, r2 = tb - n * per_img;
-    const int ti0 = (r2 / ft.nbw) * S::BH, tj0 = (r2 % ft.nbw) * BW;
+    const int iq = (int)fdiv((uint32_t)item, ft.d_item), ir = item - iq * (ft.kfast ? ft.nkg : ft.nt);
+    const int kgi = ft.kfast ? ir : iq;
+    const int tb = ft.kfast ? iq : ir;
+    const int n = (int)fdiv((uint32_t)tb, ft.d_img), r2 = tb - n * (ft.nbh * ft.nbw);
+    const int bq = (int)fdiv((uint32_t)r2, ft.d_nbw);
+    const int ti0 = bq * S::BH, tj0 = (r2 - bq * ft.nbw) * BW;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1961,11 +1964,19 @@ hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool
 
 constexpr int kMaxLdsBytes = 160 * 1024;
 
+static FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f;
+    f.l = 0;
+    while ((1ull << f.l) < d) ++f.l;
+    f.m = (uint32_t)(((1ull << 32) * ((1ull << f.l) - d)) / d + 1);
+    return f;
+}
+
 template <int MT, int TS, int CS, int BW>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
                                  hipStream_t s) {
     using S = FusedShape<MT, TS, CS, BW, 0>;
-    FusedTiling ft;
+    FusedTiling ft{};
     ft.nbh = (g.th + S::BH - 1) / S::BH;
     ft.nbw = (g.tw + BW - 1) / BW;
     ft.nt = g.N * ft.nbh * ft.nbw;
@@ -1983,6 +1994,9 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
         const double tile_major = xb + ub * sets * (ft.nkg < 32 ? 1.0 : 32.0 / ft.nkg);
         ft.kfast = tile_major < group_major ? 1 : 0;
     }
+    ft.d_item = make_fastdiv((uint32_t)(ft.kfast ? ft.nkg : ft.nt));
+    ft.d_img = make_fastdiv((uint32_t)(ft.nbh * ft.nbw));
+    ft.d_nbw = make_fastdiv((uint32_t)ft.nbw);
     const dim3 grid((unsigned)(8 * ft.per)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
     // 16-byte patch loads need rows of whole chunks and an aligned image base,
@@ -2033,7 +2047,7 @@ template <int MT, int BW>
 static hipError_t split_instance(const float* x, const float* U, float* y, float* Vb, const Geom& g, bool relu,
                                  hipStream_t s) {
     using GS = GoShape<MT>;
-    FusedTiling ft;
+    FusedTiling ft{};
     ft.bw = BW;
     ft.nbh = (g.th + 16 / BW - 1) / (16 / BW);
     ft.nbw = (g.tw + BW - 1) / BW;
