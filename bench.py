@@ -52,7 +52,15 @@ AXIS = {"w": 1, "h": 2}   # WINO_AXIS_W, WINO_AXIS_H
 KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
-                "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16"}
+                "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
+                # the split path's call: the input transform, then the GEMMs with the output transform
+                "split": ("void wino::k_vblk", "void wino::k_gemm_out")}
+
+
+def kernel_label(kind: str) -> str:
+    names = KERNEL_NAMES[kind]
+    names = (names,) if isinstance(names, str) else names
+    return " + ".join(n[5:] if n.startswith("void ") else n for n in names)
 
 
 def log(*a):
@@ -90,6 +98,7 @@ def layer_numbers(N, L):
     f["bytes"] = {
         "filter": 4 * L.K * L.C * taps + u_b,
         "fused": x_b + u_b + y_b,
+        "split": x_b + u_b + y_b,
         "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
         "gemm": v_b + u_b + m_b,
@@ -100,7 +109,8 @@ def layer_numbers(N, L):
         # the same with 16-bit V and U (fp16 / bf16 GEMM operands)
         "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
     }
-    f["flops"] = {"fused": f["gemm_flops"], "gemm": f["gemm_flops"], "stages": f["gemm_flops"],
+    f["flops"] = {"fused": f["gemm_flops"], "split": f["gemm_flops"], "gemm": f["gemm_flops"],
+                  "stages": f["gemm_flops"],
                   "stages16": f["gemm_flops"]}
     return f
 
@@ -125,7 +135,7 @@ def roofline(kind, nums, seconds):
 def traffic_file(workload: str, kind: str) -> str:
     """Counter summary of a workload's convolution kernel (fused, low-C), or of
     one stage of its staged path (input, gemm, output)."""
-    if kind in ("fused", "lowc"):
+    if kind in ("fused", "split", "lowc"):
         return os.path.join(PROFILES, f"traffic_{workload}.txt")
     return os.path.join(PROFILES, f"traffic_{workload}_{kind}.txt")
 
@@ -175,18 +185,21 @@ def pmc_summary(args):
     w = wl.WORKLOADS[name]
     nums = [layer_numbers(w.N, L) for L in w.layers]
     kind = args.kind
-    prefix = KERNEL_NAMES[kind]
+    prefixes = KERNEL_NAMES[kind]
+    prefixes = (prefixes,) if isinstance(prefixes, str) else prefixes
     out = {}
     for counter, d in (("FETCH_SIZE", args.pmc_summary[0]), ("WRITE_SIZE", args.pmc_summary[1])):
         rows = [r for r in pmc_rows(d) if r["Counter_Name"] == counter]
         # the calibration launches: torch's elementwise negation over COPY_BYTES
-        kern = [float(r["Counter_Value"]) for r in rows if kernel_is(r["Kernel_Name"], prefix)]
         copy = [float(r["Counter_Value"]) for r in rows
                 if "neg" in r["Kernel_Name"].lower() and int(r["Grid_Size"]) * 16 >= COPY_BYTES // 4]
-        if not kern or not copy:
-            raise SystemExit(f"{counter}: {len(kern)} {kind} dispatches, {len(copy)} copy dispatches in {d}")
-        out[counter] = (float(np.mean(kern)), len(kern), float(np.median(copy)), len(copy),
-                        sorted(set(r["Kernel_Name"] for r in rows if kernel_is(r["Kernel_Name"], prefix))))
+        # a call of several kernels (the split path): the sum of their per-dispatch means
+        per = [[float(r["Counter_Value"]) for r in rows if kernel_is(r["Kernel_Name"], p)] for p in prefixes]
+        if not all(per) or not copy:
+            raise SystemExit(f"{counter}: {[len(k) for k in per]} {kind} dispatches, {len(copy)} copy dispatches in {d}")
+        out[counter] = (sum(float(np.mean(k)) for k in per), min(len(k) for k in per), float(np.median(copy)),
+                        len(copy), sorted(set(r["Kernel_Name"] for r in rows
+                                              if any(kernel_is(r["Kernel_Name"], p) for p in prefixes))))
     fk, fn_, fc, fcn, names = out["FETCH_SIZE"]
     wk, wn, wc, wcn, _ = out["WRITE_SIZE"]
     fscale = fc * 1024 / COPY_BYTES
@@ -380,7 +393,7 @@ def main():
                 ws, wsb = wss[i]
                 algo = flags & B.WINO_ALGO_MASK
                 lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4)
-                kind = "stages16" if prec else "lowc" if lowc else "fused"
+                kind = "stages16" if prec else "lowc" if lowc else "split" if wsb else "fused"
                 out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                        L.pad, L.m, L.r, flags | relu,
@@ -565,7 +578,7 @@ def main():
     dom = int(np.argmax(per_launch))
     dlabel, dlayer, dkind, _ = step[dom]
     roof = roofline(dkind, nums[dlayer], per_launch[dom] / 1e3)
-    roof["kernel"] = f"{dlabel} ({KERNEL_NAMES[dkind][5:]})"
+    roof["kernel"] = f"{dlabel} ({kernel_label(dkind)})"
     roof["avg_us"] = round(per_launch[dom] * 1e3, 3)
     traffic, src = read_traffic(name, dkind) if len(w.layers) == 1 else (None, "multi-layer workload")
     roof["traffic"] = traffic
