@@ -488,13 +488,18 @@ struct FusedShape {
     // a wave then owns NF whole filters (CS <= 4) or one filter's rows of one of
     // PH halves of the row group (CS = 8).  Output sum: the G2 waves holding
     // partial outputs of one filter set (row groups x halves) keep NR2 of its NR
-    // output rows each.
+    // output rows each.  Only runs bound for another wave pass through LDS
+    // (G2*(G2-1) blocks per filter set; CS*(CS-1) per (filter block, row
+    // group) when CS <= 4); with CS = 8 every run does, so that the sum needs
+    // no per-wave copy of its code (measured faster there).
     static constexpr int NFG = CS < 4 ? CS : 4, NF = 4 / NFG, PH = CS > 4 ? CS / 4 : 1;
     static constexpr int V1 = 4 * TH / CS, VW1 = V1 % 4 == 0 ? 4 : 2;
     static constexpr int G2 = TS * PH, NR = NF * MT, NR2 = NR / G2;
-    static constexpr int EX1 = CS > 1 ? KGW * TS * CS * CS * V1 * 64 : 0;     // floats of the channel sum
-    static constexpr int EX2 = G2 > 1 ? KGW * NFG * G2 * NR * MT * 64 : 0;    // floats of the output sum
-    static constexpr int EXF = EX1 > EX2 ? EX1 : EX2;
+    static constexpr bool OWN1 = CS <= 4;                                    // own run kept in registers
+    static constexpr int NB1 = OWN1 ? CS - 1 : CS;                           // channel-sum blocks per run
+    static constexpr int EX1 = KGW * TS * CS * NB1 * V1 * 64;                // floats of the channel sum
+    static constexpr int EX2 = KGW * NFG * G2 * (G2 - 1) * NR2 * MT * 64;    // floats of the output sum
+    static constexpr int EXF = EX1 + EX2;                                    // disjoint ranges
     // LDS: three patch stages, then the transform stages (SHARE); the epilogue
     // reuses the whole allocation, which the last object is sized to cover.
     static constexpr int VSN0 = SHARE ? 2 * VSZ : 0;
@@ -525,6 +530,12 @@ __device__ __forceinline__ void wait_vm_lds() {
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <int R> using IC = std::integral_constant<int, R>;
+
+// f(IC<v>) for the runtime value v in [0, N) (wave-uniform): one instance per value.
+template <typename F, int... I>
+__device__ __forceinline__ void with_ic(int v, F&& f, std::integer_sequence<int, I...>) {
+    ((v == I ? (f(IC<I>{}), 0) : 0), ...);
+}
 
 template <int MT, int TS, int CS, int BW, int VEC, int H>
 __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
@@ -813,13 +824,19 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     float msum[CS > 1 ? V1 : 1];
 #define WINO_ACC(f) acc[(f) % TH][(f) / TH]
     if constexpr (CS > 1) {
-        // Channel sum: run dst of every part goes to block (dst, src) of this
-        // (filter block, row group); wave dst adds its CS blocks in part order.
-        lds_f* const e1 = ex + (kw * TS + h) * (CS * CS * V1 * 64) + lane * VW1;
+        // Channel sum: run dst of part src goes to block (dst, src) of this
+        // (filter block, row group) -- src != dst only, with OWN1 -- and wave
+        // dst adds the CS runs in part order (its own from its registers).
+        constexpr int NB1 = S::NB1;
+        lds_f* const e1 = ex + (kw * TS + h) * (CS * NB1 * V1 * 64) + lane * VW1;
+        auto blk1 = [&](int dst, int src) {
+            return e1 + (dst * NB1 + (S::OWN1 && src > dst ? src - 1 : src)) * (V1 * 64);
+        };
         __syncthreads();
 #pragma unroll
         for (int dst = 0; dst < CS; ++dst) {
-            lds_f* blk = e1 + (dst * CS + cs) * (V1 * 64);
+            if (S::OWN1 && dst == cs) continue;
+            lds_f* blk = blk1(dst, cs);
 #pragma unroll
             for (int q = 0; q < V1 / VW1; ++q) {
                 const int f0 = dst * V1 + q * VW1;
@@ -834,24 +851,33 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
             }
         }
         __syncthreads();
+        auto sum1 = [&](auto csc) {
+            constexpr int OWN = decltype(csc)::value;         // -1: own run from LDS too
+            const int me = OWN >= 0 ? OWN : cs;
 #pragma unroll
-        for (int src = 0; src < CS; ++src) {
-            const lds_f* blk = e1 + (cs * CS + src) * (V1 * 64);
+            for (int src = 0; src < CS; ++src) {
+                const lds_f* blk = src == OWN ? e1 : blk1(me, src);
 #pragma unroll
-            for (int q = 0; q < V1 / VW1; ++q) {
-                float w[VW1];
-                if constexpr (VW1 == 4) {
-                    const f32x4 a4 = *(const __attribute__((address_space(3))) f32x4*)(blk + q * 64 * 4);
-                    w[0] = a4[0]; w[1] = a4[1]; w[2] = a4[2]; w[3] = a4[3];
-                } else {
-                    typedef float f32x2 __attribute__((ext_vector_type(2)));
-                    const f32x2 a2 = *(const __attribute__((address_space(3))) f32x2*)(blk + q * 64 * 2);
-                    w[0] = a2[0]; w[1] = a2[1];
+                for (int q = 0; q < V1 / VW1; ++q) {
+                    float w[VW1];
+                    if (src == OWN) {
+#pragma unroll
+                        for (int i = 0; i < VW1; ++i) w[i] = WINO_ACC((OWN >= 0 ? OWN : 0) * V1 + q * VW1 + i);
+                    } else if constexpr (VW1 == 4) {
+                        const f32x4 a4 = *(const __attribute__((address_space(3))) f32x4*)(blk + q * 64 * 4);
+                        w[0] = a4[0]; w[1] = a4[1]; w[2] = a4[2]; w[3] = a4[3];
+                    } else {
+                        typedef float f32x2 __attribute__((ext_vector_type(2)));
+                        const f32x2 a2 = *(const __attribute__((address_space(3))) f32x2*)(blk + q * 64 * 2);
+                        w[0] = a2[0]; w[1] = a2[1];
+                    }
+#pragma unroll
+                    for (int i = 0; i < VW1; ++i) msum[q * VW1 + i] = src == 0 ? w[i] : msum[q * VW1 + i] + w[i];
                 }
-#pragma unroll
-                for (int i = 0; i < VW1; ++i) msum[q * VW1 + i] = src == 0 ? w[i] : msum[q * VW1 + i] + w[i];
             }
-        }
+        };
+        if constexpr (S::OWN1) with_ic(cs, sum1, std::make_integer_sequence<int, CS>{});
+        else sum1(IC<-1>{});
     }
 
     // This wave's part of A^T M A for its NF filters: the rows of its row group
@@ -894,11 +920,16 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
 #pragma unroll
             for (int jj = 0; jj < MT; ++jj) fin[rr][jj] = WINO_O(rr, jj);
     } else {
-        lds_f* const e2 = ex + (kw * S::NFG + fset) * (G2 * G2 * NR2 * MT * 64) + lane * MT;
-        __syncthreads();                         // the channel sum's blocks are consumed
+        // after the channel sum's blocks (a disjoint range: no barrier between)
+        lds_f* const e2 = ex + S::EX1 + (kw * S::NFG + fset) * (G2 * (G2 - 1) * NR2 * MT * 64) + lane * MT;
+        auto blk2 = [&](int dst, int src) {
+            return e2 + (dst * (G2 - 1) + (src < dst ? src : src - 1)) * (NR2 * MT * 64);
+        };
+        if constexpr (CS == 1) __syncthreads();  // the loop's LDS is free (CS > 1 synchronised above)
 #pragma unroll
         for (int dst = 0; dst < G2; ++dst) {
-            lds_f* blk = e2 + (dst * G2 + q) * (NR2 * MT * 64);
+            if (dst == q) continue;
+            lds_f* blk = blk2(dst, q);
 #pragma unroll
             for (int rr = 0; rr < NR2; ++rr) {
                 const int rho = dst * NR2 + rr;
@@ -913,24 +944,30 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
             }
         }
         __syncthreads();
+        with_ic(q, [&](auto qc) {
+            constexpr int OWN = decltype(qc)::value;
 #pragma unroll
-        for (int src = 0; src < G2; ++src) {
-            const lds_f* blk = e2 + (q * G2 + src) * (NR2 * MT * 64);
+            for (int src = 0; src < G2; ++src) {
+                const lds_f* blk = src == OWN ? e2 : blk2(OWN, src);
 #pragma unroll
-            for (int rr = 0; rr < NR2; ++rr) {
-                float w[MT];
-                if constexpr (MT == 4) {
-                    const f32x4 a4 = *(const __attribute__((address_space(3))) f32x4*)(blk + rr * 64 * 4);
-                    w[0] = a4[0]; w[1] = a4[1]; w[2] = a4[2]; w[3] = a4[3];
-                } else {
-                    typedef float f32x2 __attribute__((ext_vector_type(2)));
-                    const f32x2 a2 = *(const __attribute__((address_space(3))) f32x2*)(blk + rr * 64 * 2);
-                    w[0] = a2[0]; w[1] = a2[1];
+                for (int rr = 0; rr < NR2; ++rr) {
+                    float w[MT];
+                    if (src == OWN) {
+#pragma unroll
+                        for (int jj = 0; jj < MT; ++jj) w[jj] = WINO_O(OWN * NR2 + rr, jj);
+                    } else if constexpr (MT == 4) {
+                        const f32x4 a4 = *(const __attribute__((address_space(3))) f32x4*)(blk + rr * 64 * 4);
+                        w[0] = a4[0]; w[1] = a4[1]; w[2] = a4[2]; w[3] = a4[3];
+                    } else {
+                        typedef float f32x2 __attribute__((ext_vector_type(2)));
+                        const f32x2 a2 = *(const __attribute__((address_space(3))) f32x2*)(blk + rr * 64 * 2);
+                        w[0] = a2[0]; w[1] = a2[1];
+                    }
+#pragma unroll
+                    for (int jj = 0; jj < MT; ++jj) fin[rr][jj] = src == 0 ? w[jj] : fin[rr][jj] + w[jj];
                 }
-#pragma unroll
-                for (int jj = 0; jj < MT; ++jj) fin[rr][jj] = src == 0 ? w[jj] : fin[rr][jj] + w[jj];
             }
-        }
+        }, std::make_integer_sequence<int, G2>{});
     }
 #undef WINO_O
     const int kset = (kgi * KGW + kw) * 16 + 4 * cl + fset * NF;   // first filter of this wave's set
