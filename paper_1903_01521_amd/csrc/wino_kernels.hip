@@ -21,6 +21,7 @@
 // for all T positions, and after the channel loop holds the T accumulators of
 // tile l%16 for output channels 4*(l/16) .. 4*(l/16)+3 -- everything the output
 // transform of those four (tile, channel) pairs needs, in its own registers.
+#include <atomic>
 #include <type_traits>
 
 #include "wino_internal.h"
@@ -2009,6 +2010,25 @@ static FastDiv make_fastdiv(uint32_t d) {
     return f;
 }
 
+// The fused kernel's epilogue addresses its four LDS objects as one packed
+// range: check once per instance that the compiled allocation is exactly their
+// total (no padding between them) before its first launch outside a stream
+// capture (the query is not made while a capture is being recorded).
+template <int MT, int TS, int CS, int BW, int VEC>
+static hipError_t fused_lds_check(hipStream_t s) {
+    static std::atomic<int> state{0};             // 0 unchecked, 1 checked, 2 mismatch
+    const int st = state.load(std::memory_order_acquire);
+    if (st) return st == 1 ? hipSuccess : hipErrorInvalidKernelFile;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return hipSuccess;
+    hipFuncAttributes a;
+    const hipError_t e = hipFuncGetAttributes(&a, reinterpret_cast<const void*>(&k_fused<MT, TS, CS, BW, VEC>));
+    if (e != hipSuccess) return e;
+    const bool ok = a.sharedSizeBytes == (size_t)FusedShape<MT, TS, CS, BW, VEC>::LDS_BYTES;
+    state.store(ok ? 1 : 2, std::memory_order_release);
+    return ok ? hipSuccess : hipErrorInvalidKernelFile;
+}
+
 template <int MT, int TS, int CS, int BW>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
                                  hipStream_t s) {
@@ -2040,11 +2060,15 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
     // and the variant's larger stages must fit in LDS.
     if constexpr (FusedShape<MT, TS, CS, BW, 1>::LDS_BYTES <= kMaxLdsBytes) {
         if (g.W % 4 == 0 && aligned(x, 16)) {
+            const hipError_t e = fused_lds_check<MT, TS, CS, BW, 1>(s);
+            if (e != hipSuccess) return e;
             hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 1>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
                                stream_stores(g));
             return hipGetLastError();
         }
     }
+    const hipError_t e = fused_lds_check<MT, TS, CS, BW, 0>(s);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 0>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
                        stream_stores(g));
     return hipGetLastError();
