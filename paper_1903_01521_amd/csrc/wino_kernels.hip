@@ -308,8 +308,12 @@ __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, floa
 // MFMA operand quadruple is one ds_read_b128.
 __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
                                               float* __restrict__ M, Geom g) {
-    __shared__ float4 As[2][4][4][64];   // [buf][quad][k-block][lane] -> 4 positions
-    __shared__ float4 Bs[2][4][4][64];   // [buf][quad][p-block][lane]
+    // One LDS buffer (32 KB, so that five workgroups fit a CU): measured faster
+    // than a double buffer of 64 KB at every staged shape (N=64 256-channel
+    // layer 595 -> 558 us), the extra occupancy hiding more latency than the
+    // second barrier per chunk costs.
+    __shared__ float4 As[4][4][64];      // [quad][k-block][lane] -> 4 positions
+    __shared__ float4 Bs[4][4][64];      // [quad][p-block][lane]
     const int T = g.T, TG = g.T / 4;
     const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
     // Items (position group, p-tile, k-tile), k-tile fastest; each XCD runs one
@@ -344,12 +348,12 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
                 rb[i] = *(const float4*)(V + ((((size_t)pb * g.CQ + cq) * TG + tg) * 64 + lane) * 4);
         }
     };
-    auto stage = [&](int buf) {
+    auto stage = [&]() {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int blk = (tid >> 6) + 4 * i;
-            As[buf][blk >> 2][blk & 3][lane] = ra[i];
-            Bs[buf][blk >> 2][blk & 3][lane] = rb[i];
+            As[blk >> 2][blk & 3][lane] = ra[i];
+            Bs[blk >> 2][blk & 3][lane] = rb[i];
         }
     };
 
@@ -362,17 +366,16 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
             for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     fetch(0);
-    stage(0);
-    __syncthreads();
+    stage();
     for (int ch = 0; ch < nchunks; ++ch) {
-        const int buf = ch & 1;
+        __syncthreads();                 // chunk ch is in LDS
         if (ch + 1 < nchunks) fetch(ch + 1);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float4 a0 = As[buf][q][wk * 2 + 0][lane];
-            const float4 a1 = As[buf][q][wk * 2 + 1][lane];
-            const float4 b0 = Bs[buf][q][wp * 2 + 0][lane];
-            const float4 b1 = Bs[buf][q][wp * 2 + 1][lane];
+            const float4 a0 = As[q][wk * 2 + 0][lane];
+            const float4 a1 = As[q][wk * 2 + 1][lane];
+            const float4 b0 = Bs[q][wp * 2 + 0][lane];
+            const float4 b1 = Bs[q][wp * 2 + 1][lane];
             const float av[2][4] = {{a0.x, a0.y, a0.z, a0.w}, {a1.x, a1.y, a1.z, a1.w}};
             const float bv[2][4] = {{b0.x, b0.y, b0.z, b0.w}, {b1.x, b1.y, b1.z, b1.w}};
 #pragma unroll
@@ -382,8 +385,8 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
 #pragma unroll
                     for (int j = 0; j < 2; ++j) acc[t4][i][j] = mfma16x16x4(av[i][t4], bv[j][t4], acc[t4][i][j]);
         }
-        if (ch + 1 < nchunks) stage(buf ^ 1);
-        __syncthreads();
+        __syncthreads();                 // every wave is done with chunk ch
+        if (ch + 1 < nchunks) stage();
     }
 #pragma unroll
     for (int t4 = 0; t4 < 4; ++t4)
@@ -1715,6 +1718,60 @@ __global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x,
     store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, vv);
 }
 
+// With C % 4 == 0 a channel quad of a pixel is one aligned 16-byte word: one
+// wave per (16-tile block, group of four channel quads); lane q*16 + t loads,
+// for every region pixel of tile t, the four channels of quad 4*cg + q in one
+// 16-byte load (the four lanes of a tile read 64 contiguous bytes), then
+// transforms the four channels one after another into their lane slots
+// c%4*16 + t of that quad's V block.  Offsets are 32-bit from the first image
+// the block touches (the host checks that they fit below kInvalid); pixels
+// outside the image and quads past CQ read as zero.
+template <int MT>
+__global__ __launch_bounds__(256) void k_input_nhwc4(const float* __restrict__ x, float* __restrict__ V, Geom g,
+                                                     int CG, long nwg) {
+    constexpr int A = MT + 2, T = A * A;
+    const int lane = threadIdx.x & 63;
+    const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nwg) return;
+    const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (w >= (long)g.PB * CG) return;
+    // quad groups of a block consecutive: the waves reading a pixel's C channels run together
+    const int pb = (int)(w / CG), cg = (int)(w % CG);
+    const int t = lane & 15, cq = cg * 4 + (lane >> 4);
+    const TileCoord tc = decode_tile(pb * 16 + t, g);
+    const int n0 = __builtin_amdgcn_readfirstlane(min(pb * 16, g.P - 1) / (g.th * g.tw));
+    const size_t img = (size_t)g.H * g.W * g.C;
+    const size_t left = ((size_t)g.N - n0) * img * 4;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + (size_t)n0 * img), (short)0, (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
+    const bool ok = tc.valid && cq < g.CQ;
+    const uint32_t base = (uint32_t)(tc.n - n0) * (uint32_t)(img * 4) + (uint32_t)cq * 16u;
+    const int r0 = tc.ti * MT - g.pad, c0 = tc.tj * MT - g.pad;
+    f32x4 d4[A][A];
+#pragma unroll
+    for (int u = 0; u < A; ++u)
+#pragma unroll
+        for (int v = 0; v < A; ++v) {
+            const int row = r0 + u, col = c0 + v;
+            const bool in = ok && (unsigned)row < (unsigned)g.H && (unsigned)col < (unsigned)g.W;
+            const uint32_t off = in ? base + ((uint32_t)row * g.W + (uint32_t)col) * (uint32_t)g.C * 4u : kInvalid;
+            d4[u][v] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
+        }
+    if (cq >= g.CQ) return;
+    float* blk = V + ((size_t)pb * g.CQ + cq) * T * 64;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        float d[A][A];
+#pragma unroll
+        for (int u = 0; u < A; ++u)
+#pragma unroll
+            for (int v = 0; v < A; ++v) d[u][v] = d4[u][v][e];
+        float vv[T];
+        input_tf<MT>(d, vv);
+        store_t4<T, true>(blk, e * 16 + t, vv);
+    }
+}
+
 template <int MT>
 __global__ __launch_bounds__(256) void k_output_nhwc(const float* __restrict__ M, float* __restrict__ y, Geom g,
                                                      int relu, int vec_ok) {
@@ -1945,8 +2002,22 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
     if (g.nhwc) {
-        if (g.m == 2) hipLaunchKernelGGL(k_input_nhwc<2>, grid, block, 0, s, x, V, g, nwg);
-        else hipLaunchKernelGGL(k_input_nhwc<4>, grid, block, 0, s, x, V, g, nwg);
+        // 16-byte channel-quad loads when the quads are aligned and the 32-bit
+        // offsets of the images one tile block spans (at most 16 / (th*tw) + 2)
+        // stay below kInvalid
+        const size_t img_b = (size_t)g.H * g.W * g.C * 4;
+        const size_t span = (size_t)(16 / (g.th * g.tw) + 2);
+        if (g.C % 4 == 0 && aligned(x, 16) && span * img_b < (size_t)kInvalid) {
+            const int CG = (g.CQ + 3) / 4;
+            const long nwg4 = ((long)g.PB * CG + 3) / 4;
+            const dim3 grid4((unsigned)((nwg4 + 7) / 8 * 8));
+            if (g.m == 2) hipLaunchKernelGGL(k_input_nhwc4<2>, grid4, block, 0, s, x, V, g, CG, nwg4);
+            else hipLaunchKernelGGL(k_input_nhwc4<4>, grid4, block, 0, s, x, V, g, CG, nwg4);
+        } else if (g.m == 2) {
+            hipLaunchKernelGGL(k_input_nhwc<2>, grid, block, 0, s, x, V, g, nwg);
+        } else {
+            hipLaunchKernelGGL(k_input_nhwc<4>, grid, block, 0, s, x, V, g, nwg);
+        }
         return hipGetLastError();
     }
     if (g.r == 5)
