@@ -504,9 +504,9 @@ struct FusedShape {
     static constexpr int EX1 = KGW * TS * CS * NB1 * V1 * 64;                // floats of the channel sum
     static constexpr int EX2 = KGW * NFG * G2 * (G2 - 1) * NR2 * MT * 64;    // floats of the output sum
     static constexpr int EXF = EX1 + EX2;                                    // disjoint ranges
-    // LDS: three patch stages, then the transform stages (SHARE); the epilogue
+    // LDS: three patch stages, then the transform stage (SHARE); the epilogue
     // reuses the whole allocation, which the last object is sized to cover.
-    static constexpr int VSN0 = SHARE ? 2 * VSZ : 0;
+    static constexpr int VSN0 = SHARE ? VSZ : 0;
     static constexpr int VSN1 = EXF > 3 * XST + VSN0 ? EXF - 3 * XST : VSN0;
     static constexpr int VSN = VSN1 > 4 ? VSN1 : 4;
     static constexpr int LDS_FLOATS = 3 * XST + VSN;
@@ -645,13 +645,16 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         if (s < ft.nsteps) step(IC<0>{}, s);
         if (s + 1 < ft.nsteps) step(IC<1>{}, s + 1);
     } else {
-        // Step s: transform quad jt of step s+1 into V stage (s+1)&1, then for
-        // each filter-block slot kw' the MFMAs of quad kw'*CS + cs of step s from
-        // V stage s&1.  V stage (j&1) holds [(h*QS + quad)][t][64].
+        // Step s: for each filter-block slot kw' the MFMAs of quad kw'*CS + cs
+        // from the V stage, then (after every wave has read it) the transform of
+        // quad jt of step s+1 into the same stage.  One V stage [(h*QS + quad)][t][64]:
+        // VALU and MFMA work of one SIMD do not overlap on this chip, so a second
+        // stage would only buy scheduling freedom, and without it the patch
+        // stages fit LDS with 16-byte loads.
         constexpr int WAITN = S::JX + KGW * NG;    // loads issued in the previous step
         float* vbase = vs + (H * QS) * TH * 64 + lane;
-        auto put_v = [&](int j, const float (&v)[TH]) {
-            float* p = vbase + (j & 1) * S::VSZ + jt * TH * 64;
+        auto put_v = [&](const float (&v)[TH]) {
+            float* p = vbase + jt * TH * 64;
 #pragma unroll
             for (int t = 0; t < TH; ++t) p[t * 64] = v[t];
         };
@@ -664,22 +667,17 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         {
             float v[TH];
             transform(IC<0>{}, v);
-            put_v(0, v);
+            put_v(v);
         }
         auto step = [&](auto rc, int s) {  // s % 3 == R
             constexpr int R = decltype(rc)::value;
             wait_vm_lds<WAITN>();          // step s+1's patch has landed; V(s) written
             wg_barrier();                  // ... by everyone; step s-1 is fully consumed
             issue_x(IC<R>{}, s + 3);       // stage R held step s's patch, transformed at step s-1
-            if (s + 1 < ft.nsteps) {
-                float v[TH];
-                transform(IC<(R + 1) % 3>{}, v);
-                put_v(s + 1, v);
-            }
             // Quad slots k2 = 0 .. KGW-1: the V values and filters of slot k2+1
             // are requested before slot k2's MFMAs (scheduling barriers keep the
             // compiler from sinking them back next to their uses).
-            const float* vp = vbase + (s & 1) * S::VSZ + cs * TH * 64;
+            const float* vp = vbase + cs * TH * 64;
             float va[TH], vb[TH];
 #pragma unroll
             for (int t = 0; t < TH; ++t) va[t] = vp[t * 64];
@@ -704,6 +702,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             if constexpr (KGW & 1) {       // keep "ua holds the current filters" at step starts
 #pragma unroll
                 for (int i = 0; i < NG; ++i) ua[i] = ub[i];
+            }
+            if (s + 1 < ft.nsteps) {
+                wait_vm_lds<63>();         // this wave's reads of V(s) are done (LDS only)
+                wg_barrier();              // ... every wave's
+                float v[TH];
+                transform(IC<(R + 1) % 3>{}, v);
+                put_v(v);
             }
         };
         int s = 0;
