@@ -651,7 +651,14 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         // VALU and MFMA work of one SIMD do not overlap on this chip, so a second
         // stage would only buy scheduling freedom, and without it the patch
         // stages fit LDS with 16-byte loads.
-        constexpr int WAITN = S::JX + KGW * NG;    // loads issued in the previous step
+        // The loads of a step, in issue order: the filters of its quad slots
+        // (KGW * NG, the last NG for the next step's first slot), then at its
+        // end the patch DMA three steps ahead (JX).  A filter load waits (by
+        // its register) for every older load, so the DMA goes last: the
+        // filters of step s then wait only for the DMA issued at the end of
+        // step s-1.  Before transforming patch s+1 (DMA'd at the end of step
+        // s-2, or in the prologue) at most WAITT newer loads may be pending.
+        constexpr int WAITT = S::JX + NG + KGW * NG < 63 ? S::JX + NG + KGW * NG : 63;
         float* vbase = vs + (H * QS) * TH * 64 + lane;
         auto put_v = [&](const float (&v)[TH]) {
             float* p = vbase + jt * TH * 64;
@@ -671,9 +678,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         }
         auto step = [&](auto rc, int s) {  // s % 3 == R
             constexpr int R = decltype(rc)::value;
-            wait_vm_lds<WAITN>();          // step s+1's patch has landed; V(s) written
-            wg_barrier();                  // ... by everyone; step s-1 is fully consumed
-            issue_x(IC<R>{}, s + 3);       // stage R held step s's patch, transformed at step s-1
+            wait_vm_lds<63>();             // this wave's V(s) writes are done (LDS only)
+            wg_barrier();                  // ... every wave's
             // Quad slots k2 = 0 .. KGW-1: the V values and filters of slot k2+1
             // are requested before slot k2's MFMAs (scheduling barriers keep the
             // compiler from sinking them back next to their uses).
@@ -704,12 +710,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
                 for (int i = 0; i < NG; ++i) ua[i] = ub[i];
             }
             if (s + 1 < ft.nsteps) {
-                wait_vm_lds<63>();         // this wave's reads of V(s) are done (LDS only)
-                wg_barrier();              // ... every wave's
+                wait_vm_lds<WAITT>();      // patch s+1 has landed and V(s) is read (this wave)
+                wg_barrier();              // ... every wave
                 float v[TH];
                 transform(IC<(R + 1) % 3>{}, v);
                 put_v(v);
             }
+            issue_x(IC<R>{}, s + 3);       // stage R held patch s, transformed at the end of step s-1
         };
         int s = 0;
         for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
