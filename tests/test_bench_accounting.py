@@ -1,0 +1,59 @@
+"""The algorithmic work bench.py divides by (CPU only): FLOP and byte counts
+of the roofline against closed forms for known layers, and the choice of the
+bound."""
+import os
+import sys
+
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+import bench  # noqa: E402
+from paper_1903_01521_amd import workloads as wl  # noqa: E402
+
+
+def test_bench_layer_counts():
+    # N=1, C=K=64, 112x112, pad 1, F(4x4,3x3): 28 x 28 tiles, 36 positions
+    L = wl.WORKLOADS["f4_n1_c64_k64_112x112"].first
+    f = bench.layer_numbers(1, L)
+    assert (f["Ho"], f["Wo"], f["P"], f["T"]) == (112, 112, 784, 36)
+    assert f["direct_flops"] == 2 * 64 * 64 * 9 * 112 * 112
+    # the multiplication count drops exactly 4x when the tiles cover the output
+    assert f["gemm_flops"] * 4 == f["direct_flops"]
+    assert f["bytes"]["fused"] == 4 * (64 * 112 * 112 * 2 + 36 * 64 * 64)
+
+
+def test_f2_ratio_and_ragged_tiles():
+    L = wl.WORKLOADS["f2_n1_c32_k32_56x56"].first
+    f = bench.layer_numbers(1, L)
+    assert f["gemm_flops"] * 9 == f["direct_flops"] * 4          # 2.25x fewer
+    # 57x57 with m = 4: 15 x 15 tiles, the last row and column mostly padding
+    L = wl.WORKLOADS["f4_n1_c48_k48_57x57"].first
+    f = bench.layer_numbers(1, L)
+    assert (f["Ho"], f["P"]) == (57, 225)
+    assert f["gemm_flops"] == 2 * 36 * 225 * 48 * 48
+
+
+def test_1d_and_5x5_counts():
+    L = wl.WORKLOADS["f2r7w_n32_c192_k160_17x17"].first   # 1 x 7 along W, pad 3, m = 2
+    f = bench.layer_numbers(32, L)
+    assert (f["Ho"], f["Wo"], f["T"]) == (17, 17, 8)
+    assert f["P"] == 32 * 17 * 9
+    assert f["direct_flops"] == 2 * 32 * 160 * 192 * 7 * 17 * 17
+    L = wl.WORKLOADS["f2r5_n32_c48_k64_35x35"].first       # 5 x 5, pad 2, m = 2: alpha = 6
+    f = bench.layer_numbers(32, L)
+    assert (f["Ho"], f["T"], f["P"]) == (35, 36, 32 * 18 * 18)
+
+
+@pytest.mark.parametrize("name,kind,bound", [("f4_n1_c64_k64_112x112", "fused", "mfma"),
+                                              ("f4_lowc_n64_c3_k64_224x224", "lowc", "hbm"),
+                                              ("f4_n64_c256_k256_56x56", "input", "hbm"),
+                                              ("f4_n64_c256_k256_56x56", "gemm", "mfma")])
+def test_roofline_bound(name, kind, bound):
+    w = wl.WORKLOADS[name]
+    f = bench.layer_numbers(w.N, w.first)
+    r = bench.roofline(kind, f, 1e-3)
+    assert r["bound"] == bound
+    if bound == "mfma":
+        assert r["achieved"] == pytest.approx(f["flops"][kind] / 1e-3 / 1e12, rel=1e-3)
+    else:
+        assert r["achieved"] == pytest.approx(f["bytes"][kind] / 1e-3 / 1e9, rel=1e-3)
