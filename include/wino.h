@@ -31,6 +31,12 @@
  *     with x read as zero outside [0,H) x [0,W).
  *   - Floating point is IEEE fp32 storage and fp32 arithmetic (the paper's
  *     precision, Sec. 3); FMA contraction is allowed; the GEMMs run on fp32 MFMA.
+ *   - Size limit of the NCHW (channel-first) paths: one image's input,
+ *     C*H*W*4 bytes, must be below 1 GiB for the fused and split algorithms,
+ *     and (16 / (th*tw) + 2) such images below 1 GiB for the staged input
+ *     transform (the images one 16-tile block spans); otherwise the call
+ *     returns WINO_ERR_UNSUPPORTED.  The kernels address x through 32-bit
+ *     offsets.  Split larger inputs along C or the image.
  *
  * Tiling (Sec. 2, region decomposition)
  *   alpha = m + 2, T = alpha^2, th = ceil(Ho/m), tw = ceil(Wo/m),
@@ -66,7 +72,7 @@ extern "C" {
 /* ---- status codes ------------------------------------------------------- */
 #define WINO_OK                0
 #define WINO_ERR_INVALID_ARG  (-1)   /* null pointer, non-positive size, Ho/Wo < 1, overflow, aliasing */
-#define WINO_ERR_UNSUPPORTED  (-2)   /* m not in {2, 4}, or an unknown flag bit */
+#define WINO_ERR_UNSUPPORTED  (-2)   /* m not in {2, 4}, an unknown flag bit, or past a size limit */
 #define WINO_ERR_WORKSPACE    (-3)   /* workspace missing or smaller than required */
 #define WINO_ERR_HIP          (-4)   /* a HIP launch or query failed */
 

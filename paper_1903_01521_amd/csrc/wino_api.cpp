@@ -152,7 +152,27 @@ double split_ns(const Geom& g, int bw) {
 
 size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeof(float); }
 
+// Offsets into x that the NCHW input kernels form (see kInvalidOffset): one
+// image for the fused and split kernels; for the staged input transforms the
+// images one 16-tile block spans, at most 16 / (th*tw) + 2.
+bool image_fits(const Geom& g) { return (int64_t)g.C * g.H * g.W * 4 < (int64_t)kInvalidOffset; }
+bool block_images_fit(const Geom& g) {
+    const int64_t span = 16 / ((int64_t)g.th * g.tw) + 2;
+    return span * ((int64_t)g.C * g.H * g.W * 4) < (int64_t)kInvalidOffset;
+}
+
+int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p);
+
+// The plan, or WINO_ERR_UNSUPPORTED where its input kernel's offsets would not fit.
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
+    const int st = make_plan_unchecked(g, flags, p);
+    if (st != WINO_OK || g.axis != 0 || g.nhwc) return st;
+    if (p->algo == WINO_ALGO_STAGED && !block_images_fit(g)) return WINO_ERR_UNSUPPORTED;
+    if ((p->algo == WINO_ALGO_FUSED || p->algo == WINO_ALGO_SPLIT) && !image_fits(g)) return WINO_ERR_UNSUPPORTED;
+    return WINO_OK;
+}
+
+int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     if (flags & ~kKnownFlags) return WINO_ERR_UNSUPPORTED;
     const unsigned algo = flags & WINO_ALGO_MASK;
     if (algo != WINO_ALGO_AUTO && algo != WINO_ALGO_FUSED && algo != WINO_ALGO_STAGED && algo != WINO_ALGO_SPLIT &&
@@ -369,6 +389,7 @@ int wino_input_transform_r(const float* x, float* V, int N, int C, int H, int W,
     if (st != WINO_OK) return st;
     if (overlap(x, (size_t)N * C * H * W * sizeof(float), V, v_elems(g) * sizeof(float)))
         return WINO_ERR_INVALID_ARG;
+    if (!block_images_fit(g)) return WINO_ERR_UNSUPPORTED;
     return hip_status(launch_input_transform(x, V, g, (hipStream_t)stream));
 }
 

@@ -7,6 +7,13 @@
 
 namespace wino {
 
+// The NCHW input kernels address x through 32-bit buffer offsets, and any
+// offset at or past this limit reads as zero: the fused and split kernels
+// within one image, the staged input transforms (fp32 and 16-bit) across the
+// images one 16-tile block spans.  The planner rejects inputs that would need
+// larger offsets.
+constexpr uint32_t kInvalidOffset = 1u << 30;
+
 // Geometry of an r x r (3x3, or 5x5 with m = 2) stride-1 layer tiled into
 // m x m output regions, and the blocked transform-domain extents (see the
 // layout notes in wino.h).

@@ -62,7 +62,7 @@ __device__ __forceinline__ TileCoord decode_tile(int p, const Geom& g) {
 // unit returns 0 for it: a padded row, column, channel or tile is read as zero
 // without a select.  The host guarantees that every valid offset is below
 // kInvalid (the images one block spans hold < 1 GiB of input).
-constexpr uint32_t kInvalid = 1u << 30;
+constexpr uint32_t kInvalid = kInvalidOffset;
 constexpr int kRsrcWord3 = 0x00020000;   // raw (unformatted) 32-bit buffer
 
 // Transformed filters as a raw buffer (the host keeps U below 2 GiB for the

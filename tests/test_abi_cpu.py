@@ -90,6 +90,10 @@ def _conv(x=FAKE, U=FAKE, y=FAKE + 0x100000, flags=0, ws=None, wsb=0, **kw):
     (dict(y=FAKE), B.WINO_ERR_INVALID_ARG),                  # y aliases x
     (dict(y=FAKE + 64), B.WINO_ERR_INVALID_ARG),             # y overlaps x
     (dict(N=1 << 20, C=1 << 10, H=1 << 10, W=1 << 10), B.WINO_ERR_INVALID_ARG),   # size overflow
+    # an image of 1 GiB of input: past the fused kernel's 32-bit offsets
+    (dict(C=256, H=1024, W=1024, K=16, y=FAKE + (1 << 42)), B.WINO_ERR_UNSUPPORTED),
+    # 512 MiB images: the staged input transform's blocks span two of them
+    (dict(C=128, H=1024, W=1024, K=16, y=FAKE + (1 << 42), flags=B.WINO_ALGO_STAGED), B.WINO_ERR_UNSUPPORTED),
 ])
 def test_conv2d_rejects(kw, status):
     assert _conv(**kw) == status
@@ -104,6 +108,8 @@ def test_stage_entry_points_reject():
     assert B.wino_input_transform(None, FAKE, 1, 4, 8, 8, 1, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_input_transform(FAKE, FAKE + 0x100000, 1, 4, 8, 8, -2, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_input_transform(FAKE, FAKE + 0x100000, 1, 4, 8, 8, 1, 7) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_input_transform(FAKE, FAKE + (1 << 42), 2, 128, 1024, 1024, 1, 4) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_workspace_bytes(2, 128, 1024, 1024, 16, 1, 4, B.WINO_ALGO_STAGED) == 2**64 - 1
     assert B.wino_batched_gemm(FAKE, None, FAKE, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_batched_gemm(FAKE, FAKE, FAKE + 8, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
     assert B.wino_output_transform(None, FAKE, 1, 4, 8, 8, 1, 4) == B.WINO_ERR_INVALID_ARG
