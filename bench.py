@@ -336,7 +336,7 @@ def main():
         else:
             wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
         wss.append((torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev), wsb))
-        if (staged or L.r != 3) and not L.axis and not L.nhwc:
+        if staged and not L.axis and not L.nhwc:
             Vs.append(torch.empty(B.wino_input_tf_bytes_r(N, L.C, L.H, L.W, L.pad, L.m, L.r) // 4,
                                   dtype=torch.float32, device=dev))
             Ms.append(torch.empty(B.wino_gemm_out_bytes_r(N, L.K, L.H, L.W, L.pad, L.m, L.r) // 4,
@@ -382,7 +382,7 @@ def main():
             else:
                 out.append((f"L{i}.filter", i, "filter",
                             (lambda sp, i=i, L=L: B.wino_filter_transform_r(hg[i], Us[i], L.C, L.K, L.m, L.r, sp))))
-            if (staged or L.r != 3) and not prec:   # 5x5 layers run the three stages
+            if staged and not prec:
                 out.append((f"L{i}.input", i, "input", (lambda sp, i=i, L=L, a=a: B.wino_input_transform_r(
                     a, Vs[i], N, L.C, L.H, L.W, L.pad, L.m, L.r, sp))))
                 out.append((f"L{i}.gemm", i, "gemm", (lambda sp, i=i, L=L: B.wino_batched_gemm_r(
@@ -392,7 +392,7 @@ def main():
             else:
                 ws, wsb = wss[i]
                 algo = flags & B.WINO_ALGO_MASK
-                lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4)
+                lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4 and L.r == 3)
                 kind = "stages16" if prec else "lowc" if lowc else "split" if wsb else "fused"
                 out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,

@@ -99,9 +99,9 @@ extern "C" {
 /* Optional overrides of the fused kernel's variant (0 = planner's choice):
  *   WINO_BLOCK_1x16 / WINO_BLOCK_4x4: a workgroup's 16 tiles are one row of 16
  *                  tiles, or a 4 x 4 square of tiles;
- *   WINO_CSPLIT(n) n in {1,2,4,8} (m = 2) or {1,2,4} (m = 4): waves of a
- *                  workgroup that split the input channels of one filter
- *                  block, reduced in a fixed order.
+ *   WINO_CSPLIT(n) n in {1,2,4,8} (F(2x2,3x3)) or {1,2,4} (F(4x4,3x3),
+ *                  F(2x2,5x5)): waves of a workgroup that split the input
+ *                  channels of one filter block, reduced in a fixed order.
  * Results of every variant agree to fp32 rounding; unsupported combinations
  * return WINO_ERR_UNSUPPORTED. */
 #define WINO_BLOCK_1x16    0x1000u
@@ -197,9 +197,11 @@ int wino_filter_transform_p(const float* g, void* U, int C, int K, int m, unsign
  *   A^T = [1 1 1 1 1 0; 0 1 -1 2 -2 1]
  *   y[n,k,i,j] = sum_c sum_{r,s<5} x[n,c,i+r-pad,j+s-pad] * g[k,c,r,s].
  * Layouts of U, V and M are the ones above with T = 36.  g is [K][C][5][5].
- * Only the three-stage algorithm runs 5x5 layers: flags may be WINO_ALGO_AUTO
- * or WINO_ALGO_STAGED (plus WINO_FLAG_RELU); the workspace is always required.
- * Errors as for the 3x3 calls; UNSUPPORTED for other (m, r) or algorithms. */
+ * 5x5 layers run the fused kernel (WINO_ALGO_AUTO or _FUSED, no workspace;
+ * WINO_BLOCK_* and WINO_CSPLIT(n), n in {1,2,4}, as for m = 4) or the three
+ * stages (WINO_ALGO_STAGED, with the workspace), plus WINO_FLAG_RELU.
+ * Errors as for the 3x3 calls; UNSUPPORTED for other (m, r), for
+ * WINO_ALGO_SPLIT and _LOWC, and for the 16-bit formats. */
 size_t wino_filter_bytes_r(int C, int K, int m, int r);
 int wino_filter_transform_r(const float* g, float* U, int C, int K, int m, int r, void* stream);
 size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsigned flags);

@@ -102,13 +102,14 @@ struct Plan {
     FusedCfg cfg;
 };
 
-// Row groups per unit of the fused kernel: m = 2 keeps all 16 positions in one
-// wave, m = 4 splits the 36 positions over two waves.
-int row_groups(int m) { return m == 2 ? 1 : 2; }
+// Row groups per unit of the fused kernel: alpha = 4 (F(2x2,3x3)) keeps all
+// 16 positions in one wave, alpha = 6 (F(4x4,3x3), F(2x2,5x5)) splits the 36
+// positions over two waves.
+int row_groups(const Geom& g) { return g.A == 4 ? 1 : 2; }
 
-bool valid_cfg(int m, FusedCfg c) {
+bool valid_cfg(const Geom& g, FusedCfg c) {
     if (c.csplit != 1 && c.csplit != 2 && c.csplit != 4 && c.csplit != 8) return false;
-    if (row_groups(m) * c.csplit > 8) return false;
+    if (row_groups(g) * c.csplit > 8) return false;
     return c.bw == 16 || c.bw == 4;
 }
 
@@ -116,8 +117,15 @@ bool valid_cfg(int m, FusedCfg c) {
 long fused_workgroups(const Geom& g, FusedCfg c) {
     const int bh = 16 / c.bw;
     const long nt = (long)g.N * ((g.th + bh - 1) / bh) * ((g.tw + c.bw - 1) / c.bw);
-    const int kgw = 8 / (row_groups(g.m) * c.csplit);
+    const int kgw = 8 / (row_groups(g) * c.csplit);
     return nt * ((g.KB + kgw - 1) / kgw);
+}
+
+// Fraction of the tiles of a grid of bw-wide tile blocks that are real tiles.
+double block_util(const Geom& g, int bw) {
+    const int bh = 16 / bw;
+    const double rows = (double)((g.th + bh - 1) / bh * bh), cols = (double)((g.tw + bw - 1) / bw * bw);
+    return (double)g.th * g.tw / (rows * cols);
 }
 
 long split_items(const Geom& g, int bw) {
@@ -135,7 +143,7 @@ constexpr double kCus = 256.0, kFlopPerClk = 256.0, kClkGHz = 2.2, kHbmBytesPerN
 double rounds(long items) { return (double)((items + (long)kCus - 1) / (long)kCus); }
 
 double fused_ns(const Geom& g, FusedCfg c) {
-    const int kgw = 8 / (row_groups(g.m) * c.csplit);
+    const int kgw = 8 / (row_groups(g) * c.csplit);
     const double eff = kgw >= 4 ? 0.58 : kgw == 2 ? 0.42 : 0.33;
     const double work = 2.0 * 16 * kgw * 16 * (4.0 * g.CQ) * g.T;      // FLOP per workgroup
     return rounds(fused_workgroups(g, c)) * work / (kFlopPerClk * eff) / kClkGHz;
@@ -180,13 +188,14 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
         return WINO_ERR_UNSUPPORTED;
     if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
-    // 5x5 and 1-D filters and channel-last tensors run the three stages
-    // (input transform, GEMMs, output transform); the one-kernel variants are
-    // written for 3x3 regions of NCHW tensors.
+    // 1-D filters, channel-last tensors and 16-bit operands run the three
+    // stages (input transform, GEMMs, output transform); of the one-kernel
+    // variants, the fused kernel also takes 5x5 filters of NCHW tensors, the
+    // split and low-channel ones only 3x3.
     const int prec = prec_of(flags);
     if (prec < 0) return WINO_ERR_UNSUPPORTED;
     if (prec && (g.r != 3 || g.axis != 0 || g.nhwc)) return WINO_ERR_UNSUPPORTED;
-    if (g.r != 3 || g.axis != 0 || g.nhwc || prec) {
+    if (g.axis != 0 || g.nhwc || prec) {
         if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->algo = WINO_ALGO_STAGED;
@@ -195,34 +204,43 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
         return WINO_OK;
     }
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
+    if (g.r != 3 && (algo == WINO_ALGO_SPLIT || algo == WINO_ALGO_LOWC)) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
     p->algo = algo == WINO_ALGO_AUTO ? WINO_ALGO_FUSED : algo;
     p->automatic = algo == WINO_ALGO_AUTO;
     // Fused variant.  Tile blocks: a row of 16 tiles when the tile grid is at
-    // least 12 wide, else 4 x 4.  Channel split: the smallest that gives the
+    // least 12 wide and those blocks waste not much more of their tiles than
+    // 4 x 4 ones (row blocks run faster per tile: measured about 15% with
+    // equal waste), else 4 x 4.  Channel split: the smallest that gives the
     // 256 CUs a workgroup each (more filter blocks per workgroup share the
-    // staged input patch), else the largest available.
+    // staged input patch) and leaves no wave without a filter block of its
+    // own, else the largest available.
     FusedCfg c;
-    c.bw = blk == WINO_BLOCK_1x16 ? 16 : blk == WINO_BLOCK_4x4 ? 4 : (g.tw >= 12 ? 16 : 4);
+    c.bw = blk == WINO_BLOCK_1x16 ? 16
+         : blk == WINO_BLOCK_4x4  ? 4
+         : (g.tw >= 12 && block_util(g, 16) >= 0.75 * block_util(g, 4) ? 16 : 4);
     if (cs_req) {
         c.csplit = cs_req;
     } else {
-        const int max_cs = 8 / row_groups(g.m);
+        const int max_cs = 8 / row_groups(g);
         c.csplit = 1;
-        while (c.csplit < max_cs && fused_workgroups(g, c) < 240) c.csplit *= 2;
+        while (c.csplit < max_cs &&
+               (fused_workgroups(g, c) < 240 || 8 / (row_groups(g) * c.csplit) > g.KB))
+            c.csplit *= 2;
     }
-    if (p->algo == WINO_ALGO_FUSED && !valid_cfg(g.m, c)) return WINO_ERR_UNSUPPORTED;
+    if (p->algo == WINO_ALGO_FUSED && !valid_cfg(g, c)) return WINO_ERR_UNSUPPORTED;
     // The fused and split kernels address U through a 32-bit buffer range.
     if (p->algo != WINO_ALGO_STAGED && (int64_t)g.KB * g.CQ * g.T * 256 > 0x7fffffffLL) return WINO_ERR_UNSUPPORTED;
     p->cfg = c;
     // Layers with at most 4 channels: the low-C kernel.
-    if (p->automatic && g.C <= 4 && !cs_req && !blk) {
+    if (p->automatic && g.r == 3 && g.C <= 4 && !cs_req && !blk) {
         p->algo = WINO_ALGO_LOWC;
         return WINO_OK;
     }
     // Split path where the estimates favour it (layers with at least a full
     // round of its workgroups).
-    if (p->automatic && !cs_req && split_items(g, c.bw) >= (long)kCus && split_ns(g, c.bw) < fused_ns(g, c))
+    if (p->automatic && g.r == 3 && !cs_req && split_items(g, c.bw) >= (long)kCus &&
+        split_ns(g, c.bw) < fused_ns(g, c))
         p->algo = WINO_ALGO_SPLIT;
     return WINO_OK;
 }

@@ -469,14 +469,14 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 // position) values; each wave then applies its row group's part of A^T M A
 // (linear in M) to its share, and the row groups' partial outputs are summed
 // through LDS once more.  Both sums run in a fixed order.
-template <int MT, int TS, int CS, int BW, int VEC>
+template <int MT, int TS, int CS, int BW, int VEC, int R = 3>
 struct FusedShape {
-    static constexpr int A = MT + 2, T = A * A, RN = A / TS, TH = RN * A;
+    static constexpr int A = MT + R - 1, T = A * A, RN = A / TS, TH = RN * A;
     static constexpr int PARTS = TS * CS, KGW = 8 / PARTS, BH = 16 / BW;
     static constexpr int QS = KGW * CS;                    // quads per step (= 8 / TS)
     static constexpr bool SHARE = KGW > 1;                 // transforms exchanged through LDS
-    static constexpr int PR = BH * MT + 2;                 // patch rows
-    static constexpr int PC = BW * MT + 2;                 // patch columns
+    static constexpr int PR = BH * MT + R - 1;             // patch rows
+    static constexpr int PC = BW * MT + R - 1;             // patch columns
     // VEC: the patch rows come as 16-byte chunks starting at the 4-aligned column
     // at or before the patch (up to 3 columns early); else one float per load.
     static constexpr int EW = VEC ? 4 : 1;                 // floats per load
@@ -541,14 +541,14 @@ __device__ __forceinline__ void with_ic(int v, F&& f, std::integer_sequence<int,
     ((v == I ? (f(IC<I>{}), 0) : 0), ...);
 }
 
-template <int MT, int TS, int CS, int BW, int VEC, int H>
+template <int MT, int TS, int CS, int BW, int VEC, int H, int RF>
 __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
-                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW, VEC>::JX],
+                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW, VEC, RF>::JX],
                                             uint32_t step_b, const float* __restrict__ U, const Geom& g,
                                             const FusedTiling& ft, int kb, int wave, int lane, int kw, int cs,
                                             int bi, int bj, float* xs0, float* xs1, float* xs2, float* vs,
-                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC>::TH], int xlo) {
-    using S = FusedShape<MT, TS, CS, BW, VEC>;
+                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC, RF>::TH], int xlo) {
+    using S = FusedShape<MT, TS, CS, BW, VEC, RF>;
     constexpr int A = S::A, RN = S::RN, X0 = H * RN, TH = S::TH, T = S::T, QS = S::QS, KGW = S::KGW;
     constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;   // this row group's position groups
     const int cl = lane >> 4;
@@ -582,7 +582,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
     };
     auto transform = [&](auto rc, float (&v)[TH]) {
         // VEC: the patch's first column sits 4 floats in (or at 0 when the
-        // chunks start on it), so region rows stay 16-byte aligned.
+        // chunks start on it), so region rows stay 16-byte aligned (8-byte
+        // aligned for m = 2).
         const float* wp = xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT + (xlo ? 4 : 0);
         float d[A][A];
 #pragma unroll
@@ -593,12 +594,15 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
                 const float2 b2 = *(const float2*)(row + 4);
                 d[u][0] = a4.x; d[u][1] = a4.y; d[u][2] = a4.z; d[u][3] = a4.w; d[u][4] = b2.x; d[u][5] = b2.y;
             } else {
-                const float2 a2 = *(const float2*)row;
-                const float2 b2 = *(const float2*)(row + 2);
-                d[u][0] = a2.x; d[u][1] = a2.y; d[u][2] = b2.x; d[u][3] = b2.y;
+#pragma unroll
+                for (int v2 = 0; v2 < A / 2; ++v2) {
+                    const float2 a2 = *(const float2*)(row + 2 * v2);
+                    d[u][2 * v2] = a2.x; d[u][2 * v2 + 1] = a2.y;
+                }
             }
         }
-        input_tf_rows<MT, X0, RN>(d, v);
+        // B^T depends only on the region side (the points): F(2x2,5x5) uses F(4x4,3x3)'s.
+        input_tf_rows<A - 2, X0, RN>(d, v);
     };
     auto mfma_quad = [&](const float (&v)[TH], const f32x4 (&ug)[NG]) {
 #pragma unroll
@@ -744,11 +748,11 @@ __device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS
     }
 }
 
-template <int MT, int TS, int CS, int BW, int VEC>
+template <int MT, int TS, int CS, int BW, int VEC, int RF = 3>
 __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, const float* __restrict__ U,
                                                float* __restrict__ y, Geom g, FusedTiling ft, int relu,
                                                int vec_ok, int nts) {
-    using S = FusedShape<MT, TS, CS, BW, VEC>;
+    using S = FusedShape<MT, TS, CS, BW, VEC, RF>;
     constexpr int PARTS = S::PARTS, KGW = S::KGW;
     __shared__ float4 xs0[S::XST / 4], xs1[S::XST / 4], xs2[S::XST / 4];   // patch stages
     __shared__ float4 vs[S::VSN / 4];                      // transform stages (SHARE)
@@ -815,13 +819,13 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     float* xs2f = (float*)xs2;
     float* vsf = (float*)vs;
     if constexpr (TS == 1) {
-        fused_steps<MT, TS, CS, BW, VEC, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
+        fused_steps<MT, TS, CS, BW, VEC, 0, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
                                        xs2f, vsf, acc, xlo);
     } else if (h == 0) {
-        fused_steps<MT, TS, CS, BW, VEC, 0>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
+        fused_steps<MT, TS, CS, BW, VEC, 0, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
                                        xs2f, vsf, acc, xlo);
     } else {
-        fused_steps<MT, TS, CS, BW, VEC, 1>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
+        fused_steps<MT, TS, CS, BW, VEC, 1, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
                                        xs2f, vsf, acc, xlo);
     }
 
@@ -911,11 +915,11 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
                 else m1[t] = msum[j * TQ + t];
             }
             if constexpr (PH == 1) {
-                output_tf_rows<MT, X0, RN>(m1, o[j]);
+                output_tf_rows<MT, X0, RN, RF>(m1, o[j]);
             } else if (ph == 0) {
-                output_tf_rows<MT, X0, RH>(m1, o[j]);
+                output_tf_rows<MT, X0, RH, RF>(m1, o[j]);
             } else {
-                output_tf_rows<MT, X0 + RH, RH>(m1, o[j]);
+                output_tf_rows<MT, X0 + RH, RH, RF>(m1, o[j]);
             }
         }
     };
@@ -2097,7 +2101,7 @@ static FastDiv make_fastdiv(uint32_t d) {
 // range: check once per instance that the compiled allocation is exactly their
 // total (no padding between them) before its first launch outside a stream
 // capture (the query is not made while a capture is being recorded).
-template <int MT, int TS, int CS, int BW, int VEC>
+template <int MT, int TS, int CS, int BW, int VEC, int R>
 static hipError_t fused_lds_check(hipStream_t s) {
     static std::atomic<int> state{0};             // 0 unchecked, 1 checked, 2 mismatch
     const int st = state.load(std::memory_order_acquire);
@@ -2105,17 +2109,17 @@ static hipError_t fused_lds_check(hipStream_t s) {
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return hipSuccess;
     hipFuncAttributes a;
-    const hipError_t e = hipFuncGetAttributes(&a, reinterpret_cast<const void*>(&k_fused<MT, TS, CS, BW, VEC>));
+    const hipError_t e = hipFuncGetAttributes(&a, reinterpret_cast<const void*>(&k_fused<MT, TS, CS, BW, VEC, R>));
     if (e != hipSuccess) return e;
-    const bool ok = a.sharedSizeBytes == (size_t)FusedShape<MT, TS, CS, BW, VEC>::LDS_BYTES;
+    const bool ok = a.sharedSizeBytes == (size_t)FusedShape<MT, TS, CS, BW, VEC, R>::LDS_BYTES;
     state.store(ok ? 1 : 2, std::memory_order_release);
     return ok ? hipSuccess : hipErrorInvalidKernelFile;
 }
 
-template <int MT, int TS, int CS, int BW>
+template <int MT, int TS, int CS, int BW, int R = 3>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
                                  hipStream_t s) {
-    using S = FusedShape<MT, TS, CS, BW, 0>;
+    using S = FusedShape<MT, TS, CS, BW, 0, R>;
     FusedTiling ft{};
     ft.nbh = (g.th + S::BH - 1) / S::BH;
     ft.nbw = (g.tw + BW - 1) / BW;
@@ -2141,25 +2145,39 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
     // 16-byte patch loads need rows of whole chunks and an aligned image base,
     // and the variant's larger stages must fit in LDS.
-    if constexpr (FusedShape<MT, TS, CS, BW, 1>::LDS_BYTES <= kMaxLdsBytes) {
+    if constexpr (FusedShape<MT, TS, CS, BW, 1, R>::LDS_BYTES <= kMaxLdsBytes) {
         if (g.W % 4 == 0 && aligned(x, 16)) {
-            const hipError_t e = fused_lds_check<MT, TS, CS, BW, 1>(s);
+            const hipError_t e = fused_lds_check<MT, TS, CS, BW, 1, R>(s);
             if (e != hipSuccess) return e;
-            hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 1>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
+            hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 1, R>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
                                stream_stores(g));
             return hipGetLastError();
         }
     }
-    const hipError_t e = fused_lds_check<MT, TS, CS, BW, 0>(s);
+    const hipError_t e = fused_lds_check<MT, TS, CS, BW, 0, R>(s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 0>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
+    hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 0, R>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
                        stream_stores(g));
     return hipGetLastError();
 }
 
 hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg c, bool relu,
                         hipStream_t s) {
-    // m = 2: all 16 positions per wave; m = 4: two row groups of 18 positions.
+    // 3x3, m = 2: all 16 positions per wave; m = 4 and 5x5 (alpha = 6): two
+    // row groups of 18 positions.
+    if (g.r == 5) {
+#define WINO_FUSED_R5(CS, BW) \
+    if (g.m == 2 && c.csplit == CS && c.bw == BW) return fused_instance<2, 2, CS, BW, 5>(x, U, y, g, relu, s);
+        WINO_FUSED_R5(1, 16)
+        WINO_FUSED_R5(2, 16)
+        WINO_FUSED_R5(4, 16)
+        WINO_FUSED_R5(1, 4)
+        WINO_FUSED_R5(2, 4)
+        WINO_FUSED_R5(4, 4)
+#undef WINO_FUSED_R5
+        return hipErrorInvalidValue;
+    }
+    if (g.r != 3) return hipErrorInvalidValue;
 #define WINO_FUSED_CASE(MT, TS, CS, BW) \
     if (g.m == MT && c.csplit == CS && c.bw == BW) return fused_instance<MT, TS, CS, BW>(x, U, y, g, relu, s);
     WINO_FUSED_CASE(2, 1, 1, 16)

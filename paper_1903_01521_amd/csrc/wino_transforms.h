@@ -182,6 +182,18 @@ template <> struct AtRows<4, 0, 3> {            // rows 0, 1, 2 of the m = 4 A^T
         r[3] = d12;
     }
 };
+template <> struct AtRows<2, 0, 3> {            // rows 0, 1, 2 of the F(2,5) A^T (2 x 6)
+    __device__ static void f(const float (&a)[3], float (&r)[2]) {
+        r[0] = a[0] + (a[1] + a[2]);
+        r[1] = a[1] - a[2];
+    }
+};
+template <> struct AtRows<2, 3, 3> {            // rows 3, 4, 5 of the F(2,5) A^T
+    __device__ static void f(const float (&a)[3], float (&r)[2]) {
+        r[0] = a[0] + a[1];
+        r[1] = __builtin_fmaf(2.0f, a[0] - a[1], a[2]);
+    }
+};
 template <> struct AtRows<4, 3, 3> {            // rows 3, 4, 5
     __device__ static void f(const float (&a)[3], float (&r)[4]) {
         const float s34 = a[0] + a[1], d34 = a[0] - a[1];
@@ -192,10 +204,11 @@ template <> struct AtRows<4, 3, 3> {            // rows 3, 4, 5
     }
 };
 
-// o = A^T M' A where M' keeps rows [X0, X0+RN) of M (mv holds just those rows).
-template <int MT, int X0, int RN>
-__device__ __forceinline__ void output_tf_rows(const float (&mv)[RN * (MT + 2)], float (&o)[MT][MT]) {
-    constexpr int A = MT + 2;
+// o = A^T M' A where M' keeps rows [X0, X0+RN) of M (mv holds just those
+// rows); A^T is m x (m + R - 1) (R = 5 only with m = 2).
+template <int MT, int X0, int RN, int R = 3>
+__device__ __forceinline__ void output_tf_rows(const float (&mv)[RN * (MT + R - 1)], float (&o)[MT][MT]) {
+    constexpr int A = MT + R - 1;
     float s[MT][A];
 #pragma unroll
     for (int j = 0; j < A; ++j) {

@@ -127,11 +127,14 @@ def test_5x5_sizes_and_rejections():
     assert B.wino_filter_bytes_r(3, 20, 4, 5) == 0                 # F(4x4,5x5): not supported
     assert B.wino_filter_bytes_r(3, 20, 2, 7) == 0
     # 35x35, pad 2 -> 35x35 output, 18x18 tiles = 324 -> 21 blocks; V + M of the staged path
-    ws = B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, 0)
+    ws = B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, B.WINO_ALGO_STAGED)
     v = 4 * 21 * 12 * 36 * 64
     assert ws == (v + 255) // 256 * 256 + 4 * 21 * 4 * 36 * 256
-    assert B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, B.WINO_ALGO_STAGED) == ws
-    for flags in (B.WINO_ALGO_FUSED, B.WINO_ALGO_SPLIT, B.WINO_ALGO_LOWC, B.WINO_BLOCK_4x4, B.WINO_CSPLIT(2)):
+    # the fused kernel (the planner's choice) needs none; two row groups of 18
+    # positions per unit, so at most 4 channel parts
+    for flags in (0, B.WINO_ALGO_FUSED, B.WINO_BLOCK_4x4, B.WINO_CSPLIT(2), B.WINO_ALGO_FUSED | B.WINO_CSPLIT(4)):
+        assert B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, flags) == 0
+    for flags in (B.WINO_ALGO_SPLIT, B.WINO_ALGO_LOWC, B.WINO_CSPLIT(8)):
         assert B.wino_workspace_bytes_r(1, 48, 35, 35, 64, 2, 2, 5, flags) == 2**64 - 1
     assert B.wino_workspace_bytes_r(1, 4, 3, 3, 4, 0, 2, 5, 0) == 2**64 - 1        # Ho < 1
     # the 3x3 calls are the r = 3 case
@@ -147,8 +150,10 @@ def test_5x5_entry_points_reject():
     conv = lambda **kw: B.wino_conv2d_r(kw.get("x", FAKE), FAKE + 0x800000, kw.get("y", y), 1, 4, 8, 8, 4,
                                         kw.get("pad", 2), kw.get("m", 2), kw.get("r", 5), kw.get("flags", 0),
                                         kw.get("ws"), kw.get("wsb", 0), None)
-    assert conv() == B.WINO_ERR_WORKSPACE                          # the three stages need V and M
-    assert conv(flags=B.WINO_ALGO_FUSED) == B.WINO_ERR_UNSUPPORTED
+    assert conv(flags=B.WINO_ALGO_STAGED) == B.WINO_ERR_WORKSPACE  # the three stages need V and M
+    assert conv(flags=B.WINO_ALGO_SPLIT) == B.WINO_ERR_UNSUPPORTED
+    assert conv(flags=B.WINO_ALGO_LOWC) == B.WINO_ERR_UNSUPPORTED
+    assert conv(flags=B.WINO_CSPLIT(8)) == B.WINO_ERR_UNSUPPORTED
     assert conv(r=7) == B.WINO_ERR_UNSUPPORTED
     assert conv(m=4) == B.WINO_ERR_UNSUPPORTED
     assert conv(pad=-1) == B.WINO_ERR_INVALID_ARG

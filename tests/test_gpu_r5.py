@@ -1,7 +1,8 @@
 """F(2x2,5x5) -- the method on 5x5 filters (the 5x5 layers of the paper's
 Table 2) -- through wino_filter_transform_r / wino_conv2d_r, against the fp64
-oracle: the filter transform, whole layers (ragged, padded, several tile and
-filter blocks, ReLU), exact integer results, and a sampled full-size layer."""
+oracle: the filter transform, whole layers on the fused and three-stage
+algorithms (ragged, padded, several tile and filter blocks, every fused
+variant, ReLU), exact integer results, and a sampled full-size layer."""
 import numpy as np
 import pytest
 import torch
@@ -103,6 +104,49 @@ def test_conv2d_5x5(shape):
         assert np.all(np.abs(y - r) <= ELEM * (bound + 1e-30))
 
 
+# The fused kernel's variants: tile block (1 x 16 or 4 x 4) x channel split.
+FUSED = [(f"b{bn}c{c}", B.WINO_ALGO_FUSED | bf | B.WINO_CSPLIT(c))
+         for bn, bf in (("16", B.WINO_BLOCK_1x16), ("4", B.WINO_BLOCK_4x4)) for c in (1, 2, 4)]
+
+
+@pytest.mark.parametrize("variant", FUSED, ids=lambda v: v[0])
+@pytest.mark.parametrize("shape", [(2, 5, 9, 11, 7, 2), (1, 16, 17, 23, 20, 2), (1, 1, 1, 1, 1, 2),
+                                   (2, 37, 14, 37, 40, 2), (1, 4, 6, 140, 8, 2), (3, 8, 5, 5, 33, 1)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_conv2d_5x5_fused_variants(shape, variant):
+    # Every variant against the oracle: several channel steps, ragged tile
+    # blocks and filter groups, odd widths (one float per patch load) and
+    # W % 4 == 0 (16-byte patch loads).
+    name, flags = variant
+    N, C, H, W, K, pad = shape
+    print(f"conv2d_r fused {name} shape={shape}", flush=True)
+    rng = np.random.default_rng(sum(shape) + 5)
+    x, g = random_layer(rng, N, C, H, W, K)
+    ref = direct.conv2d(x, g, pad)
+    bound = tile_bound(direct.conv2d(x, g, pad, absval=True))
+    U = filter_transform(g)
+    assert B.wino_workspace_bytes_r(N, C, H, W, K, pad, M_, R_, flags) == 0
+    y = h.host(conv(x, U, K, pad, flags))
+    assert np.all(np.isfinite(y))
+    assert h.normwise_err(y, ref) <= TOL
+    assert np.all(np.abs(y - ref) <= ELEM * (bound + 1e-30))
+    yr = h.host(conv(x, U, K, pad, flags | B.WINO_FLAG_RELU))
+    assert np.array_equal(yr, np.maximum(y, 0.0))
+
+
+def test_conv2d_5x5_fused_matches_staged():
+    # Same U and V arithmetic (fp32 transforms, fp32 accumulation in a different
+    # order): the two algorithms agree to rounding.
+    N, C, H, W, K, pad = 2, 48, 35, 35, 64, 2
+    rng = np.random.default_rng(35)
+    x, g = random_layer(rng, N, C, H, W, K)
+    U = filter_transform(g)
+    yf = h.host(conv(x, U, K, pad, B.WINO_ALGO_FUSED))
+    ys = h.host(conv(x, U, K, pad, B.WINO_ALGO_STAGED))
+    bound = tile_bound(direct.conv2d(x, g, pad, absval=True))
+    assert np.all(np.abs(yf - ys) <= 2 * ELEM * (bound + 1e-30))
+
+
 @pytest.mark.parametrize("shape", [(2, 4, 9, 11, 20, 2), (1, 8, 12, 12, 16, 0), (1, 3, 7, 16, 40, 1)])
 def test_conv2d_5x5_exact_on_integers(shape):
     # Integer x in {-1, 0, 1} and g a multiple of 24^2 (S*G is an integer matrix
@@ -119,8 +163,10 @@ def test_conv2d_5x5_exact_on_integers(shape):
     assert np.all(Uo == np.round(Uo)) and Mabs.max() < 2 ** 24 and np.abs(Vo).max() < 2 ** 24
     assert (np.abs(AT).sum(axis=1).max() ** 2) * Mabs.max() < 2 ** 24
     ref = direct.conv2d(x, g, pad)
-    y = h.host(conv(x, filter_transform(g), K, pad))
-    assert np.array_equal(y.astype(np.float64), ref)
+    U = filter_transform(g)
+    for flags in (B.WINO_ALGO_FUSED, B.WINO_ALGO_STAGED):
+        y = h.host(conv(x, U, K, pad, flags))
+        assert np.array_equal(y.astype(np.float64), ref)
 
 
 def test_conv2d_5x5_repeatable_and_guarded():
