@@ -445,6 +445,7 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 // ------------------------------------------------------------------ fused
 // One workgroup of 8 waves computes one tile block (16 tiles: 1 x 16 or 4 x 4)
 // for KGW 16-filter blocks, over all channels, all T positions, start to end.
+// RF is the filter side: 3, or 5 with m = 2 (6 x 6 regions like m = 4's).
 // The 8 waves are (filter block kw) x (row group h of TS) x (channel split cs
 // of CS): wave h owns transform-domain rows [h*A/TS, (h+1)*A/TS), i.e. T/TS
 // accumulators per lane.
@@ -453,11 +454,13 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 // quad j = kw*CS + cs is input-transformed by wave (kw, h, cs) for its rows --
 // every wave transforms exactly one region set per step -- and each wave then
 // multiplies the KGW quads of its channel split (j = kw'*CS + cs) with its own
-// filter block.  With KGW > 1 the transforms are exchanged through LDS, one
-// step ahead (double-buffered); with KGW = 1 they stay in registers.
+// filter block.  With KGW > 1 the transforms are exchanged through one LDS
+// stage, written for step s+1 after step s's products; with KGW = 1 they stay
+// in registers.
 //
 // The halo'd input patch of a step comes straight into LDS (buffer loads with
-// an LDS destination, no register round trip) two steps ahead, in three stages
+// an LDS destination, no register round trip) two steps ahead (three with
+// KGW > 1, whose transform runs a step early), in three stages
 // that are distinct LDS objects, so the compiler can see that reading one stage
 // never waits for loads still landing in another.  Rows, columns and channels
 // outside the image and the alignment columns are offsets past the buffer

@@ -111,7 +111,8 @@ FUSED = [(f"b{bn}c{c}", B.WINO_ALGO_FUSED | bf | B.WINO_CSPLIT(c))
 
 @pytest.mark.parametrize("variant", FUSED, ids=lambda v: v[0])
 @pytest.mark.parametrize("shape", [(2, 5, 9, 11, 7, 2), (1, 16, 17, 23, 20, 2), (1, 1, 1, 1, 1, 2),
-                                   (2, 37, 14, 37, 40, 2), (1, 4, 6, 140, 8, 2), (3, 8, 5, 5, 33, 1)],
+                                   (2, 37, 14, 37, 40, 2), (1, 4, 6, 140, 8, 2), (3, 8, 5, 5, 33, 1),
+                                   (2, 40, 20, 28, 36, 2), (1, 64, 13, 16, 80, 0)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_conv2d_5x5_fused_variants(shape, variant):
     # Every variant against the oracle: several channel steps, ragged tile
