@@ -598,6 +598,22 @@ def main():
     copy_gbs = 2 * COPY_BYTES / (e0.elapsed_time(e1) / 1e3) / 1e9
     del cs, cd
 
+    # Sustained fp32 matrix-core rate (the library's probe: 2048 waves of
+    # independent MFMA chains), best of five launches, outside every timed region.
+    probe_iters = 4096
+    probe_out = torch.empty(2048, dtype=torch.float32, device=dev)
+    B.check(B.wino_probe_mfma_f32(probe_iters, probe_out, stream), "wino_probe_mfma_f32")
+    probe_ms = []
+    for _ in range(5):
+        e0.record(stream)
+        B.check(B.wino_probe_mfma_f32(probe_iters, probe_out, stream), "wino_probe_mfma_f32")
+        e1.record(stream)
+        torch.cuda.synchronize()
+        probe_ms.append(e0.elapsed_time(e1))
+    if not bool((probe_out == 32.0 * probe_iters).all()):
+        raise RuntimeError("MFMA probe check values are wrong")
+    mfma_tflops = B.wino_probe_mfma_f32_flops(probe_iters) / (min(probe_ms) / 1e3) / 1e12
+
     direct = sum(f["direct_flops"] for f in nums)
     value = direct / (ms_step / 1e3) / 1e9
 
@@ -642,6 +658,9 @@ def main():
         "graph_ms_per_step": round(graph_ms, 6) if graph_ms is not None else None,
         "wall_ms_per_step": round((wall1 - wall0) * 1e3 / args.steps, 6),
         "copy_calibration_gbs": round(copy_gbs, 1),
+        # what this chip sustains, beside the published peaks the roofline uses
+        "measured_peaks": {"hbm_copy_gbs": round(copy_gbs, 1), "mfma_f32_tflops": round(mfma_tflops, 1),
+                           "published_hbm_gbs": HBM_PEAK / 1e9, "published_mfma_f32_tflops": FP32_MFMA_PEAK / 1e12},
     }
 
     # CPU baseline: the fp64 oracle on this host, on a bounded sample (the first

@@ -261,6 +261,17 @@ int wino_conv2d_nhwc(const float* x, const float* U, float* y,
  * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);
 
+/* Measurement aid (not part of the method): the fp32 matrix-core rate the chip
+ * sustains, to set beside the published peak when reading roofline fractions.
+ * One launch of 2048 waves (2 per SIMD of 256 CUs), each running 8 independent
+ * chains of iters v_mfma_f32_16x16x4_f32 on operands of 1.0.  out: 2048 floats
+ * (device, caller-owned); out[w] = 32 * iters exactly for every wave w (a check
+ * that the work ran).  iters in [1, 2^21], else WINO_ERR_INVALID_ARG; null out
+ * is invalid too.  wino_probe_mfma_f32_flops(iters) gives the launch's FLOPs
+ * (0 outside that range); FLOPs / elapsed time is the sustained rate. */
+int wino_probe_mfma_f32(int iters, float* out, void* stream);
+size_t wino_probe_mfma_f32_flops(int iters);
+
 #ifdef __cplusplus
 }
 #endif

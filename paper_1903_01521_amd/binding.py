@@ -63,6 +63,8 @@ _SIGS = {
     "wino_batched_gemm": ([_vp, _vp, _vp] + [_c_int] * 7 + [_vp], _c_int),
     "wino_output_transform": ([_vp, _vp] + [_c_int] * 6 + [_c_uint, _vp], _c_int),
     "wino_maxpool2x2": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
+    "wino_probe_mfma_f32": ([_c_int, _vp, _vp], _c_int),
+    "wino_probe_mfma_f32_flops": ([_c_int], _c_size),
     "wino_filter_bytes_r": ([_c_int] * 4, _c_size),
     "wino_filter_transform_r": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
     "wino_workspace_bytes_r": ([_c_int] * 8 + [_c_uint], _c_size),
@@ -186,6 +188,14 @@ def wino_output_transform(M, y, N, K, H, W, pad, m, flags=0, stream=None) -> int
 
 def wino_maxpool2x2(x, y, N, C, H, W, stream=None) -> int:
     return lib().wino_maxpool2x2(_fptr(x), _fptr(y), N, C, H, W, _stream(stream))
+
+
+def wino_probe_mfma_f32(iters, out, stream=None) -> int:
+    return lib().wino_probe_mfma_f32(iters, _fptr(out), _stream(stream))
+
+
+def wino_probe_mfma_f32_flops(iters) -> int:
+    return lib().wino_probe_mfma_f32_flops(iters)
 
 
 def wino_filter_bytes_r(C, K, m, r) -> int:

@@ -549,4 +549,14 @@ int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* 
     return hip_status(launch_maxpool2x2(x, y, N, C, H, W, (hipStream_t)stream));
 }
 
+int wino_probe_mfma_f32(int iters, float* out, void* stream) {
+    if (!out || iters < 1 || iters > kProbeMaxIters) return WINO_ERR_INVALID_ARG;
+    return hip_status(launch_mfma_probe(iters, out, (hipStream_t)stream));
+}
+
+size_t wino_probe_mfma_f32_flops(int iters) {
+    if (iters < 1 || iters > kProbeMaxIters) return 0;
+    return (size_t)kProbeWaves * (size_t)iters * 8 * (2 * 16 * 16 * 4);
+}
+
 }  // extern "C"

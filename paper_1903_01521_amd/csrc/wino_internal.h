@@ -75,6 +75,12 @@ hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, con
 // Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.
 hipError_t launch_lowc(const float* x, const float* U, float* y, const Geom& g, bool relu, hipStream_t s);
 hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, hipStream_t s);
+// Waves of the matrix-core peak probe: 256 CUs x 4 SIMDs x 2 waves.
+constexpr int kProbeWaves = 2048;
+// Up to 2^21 iterations every partial sum of the probe's check value is an
+// integer below 2^24, so the check is exact.
+constexpr int kProbeMaxIters = 1 << 21;
+hipError_t launch_mfma_probe(int iters, float* out, hipStream_t s);
 // 1-D layers (1 x r or r x 1 filters, F(1xm, 1xr, 1x8)): filter transform; the
 // input and output transforms dispatch on g.axis inside launch_input_transform
 // and launch_output_transform.

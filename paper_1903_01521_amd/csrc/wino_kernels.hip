@@ -2285,6 +2285,32 @@ hipError_t launch_maxpool2x2(const float* x, float* y, int N, int C, int H, int 
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ peak probe
+// The fp32 matrix-core rate this chip sustains: every wave runs eight
+// independent chains of v_mfma_f32_16x16x4_f32 (enough to cover the
+// instruction's latency) on operands of 1.0, so each accumulator element ends
+// at exactly 4 * iters.  Lane 0 of each wave writes the sum of its chains'
+// first elements (32 * iters) to out[wave].
+__global__ __launch_bounds__(256) void k_mfma_probe(int iters, float* __restrict__ out) {
+    f32x4 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float one = 1.0f;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(one, one, acc[j], 0, 0, 0);
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += acc[j][0];
+    if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = sum;
+}
+
+hipError_t launch_mfma_probe(int iters, float* out, hipStream_t s) {
+    hipLaunchKernelGGL(k_mfma_probe, dim3(kProbeWaves / 4), dim3(256), 0, s, iters, out);
+    return hipGetLastError();
+}
+
 size_t filter_elems(int C, int K, int m, int r) {
     const size_t T = (size_t)(m + r - 1) * (m + r - 1);
     return T * (size_t)((C + 3) / 4) * 4 * (size_t)((K + 15) / 16) * 16;

@@ -230,3 +230,14 @@ def test_16bit_operand_entry_points():
     assert B.wino_filter_transform_p(FAKE, FAKE + 8, 4, 4, 4, F16) == B.WINO_ERR_INVALID_ARG     # overlap
     assert _conv(flags=F16) == B.WINO_ERR_WORKSPACE
     assert _conv(flags=F16 | B.WINO_ALGO_FUSED) == B.WINO_ERR_UNSUPPORTED
+
+
+def test_mfma_probe_arguments():
+    assert B.wino_probe_mfma_f32(1, None) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_probe_mfma_f32(0, FAKE) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_probe_mfma_f32(2 ** 21 + 1, FAKE) == B.WINO_ERR_INVALID_ARG
+    # 2048 waves x iters x 8 chains x (2 * 16 * 16 * 4) FLOPs
+    assert B.wino_probe_mfma_f32_flops(1) == 2048 * 8 * 2048
+    assert B.wino_probe_mfma_f32_flops(1000) == 1000 * 2048 * 8 * 2048
+    assert B.wino_probe_mfma_f32_flops(0) == 0
+    assert B.wino_probe_mfma_f32_flops(2 ** 21 + 1) == 0
