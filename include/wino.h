@@ -107,6 +107,16 @@ extern "C" {
 #define WINO_BLOCK_1x16    0x1000u
 #define WINO_BLOCK_4x4     0x2000u
 #define WINO_CSPLIT(n)     (((unsigned)(n) & 0xFu) << 16)
+/* WINO_CSLICES(n), n in 1..8 and at most ceil(C/4), with WINO_ALGO_FUSED: the
+ * channels in n slices over separate workgroups (quads split as evenly as
+ * ceil(CQ/n) allows), each writing a partial output to the workspace
+ * ([slices][N][K][Ho][Wo] fp32), summed in slice order by one more launch
+ * (ReLU applied there).  WINO_ALGO_AUTO picks it for fused layers whose
+ * workgroups fill less than half of the 256 CUs with long channel loops (deep
+ * layers at batch 1), if the caller passes the workspace that
+ * wino_workspace_bytes then reports; without it the layer runs unsliced.
+ * WINO_CSLICES(1) keeps AUTO from slicing. */
+#define WINO_CSLICES(n)    (((unsigned)(n) & 0xFu) << 20)
 
 /* Human-readable text of a status code (static storage, never NULL). */
 const char* wino_status_string(int status);
@@ -144,9 +154,10 @@ int wino_filter_transform(const float* g, float* U, int C, int K, int m, void* s
  *   flags : WINO_FLAG_RELU and/or one WINO_ALGO_* value.
  *   workspace / workspace_bytes : device scratch of at least
  *       wino_workspace_bytes(N,C,H,W,K,pad,m,flags) bytes (V and M of the staged
- *       algorithm, the tile-blocked V of the split one); may be NULL/0 when that
- *       is 0.  With WINO_ALGO_AUTO the planner uses the split algorithm only if
- *       the workspace given is large enough, else the fused one.  Contents on
+ *       algorithm, the tile-blocked V of the split one, the partial outputs of
+ *       channel slices); may be NULL/0 when that is 0.  With WINO_ALGO_AUTO the
+ *       planner uses the split algorithm or channel slices only if the
+ *       workspace given is large enough, else the plain fused kernel.  Contents on
  *       return are unspecified; calls sharing one workspace must not overlap in
  *       time.
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */

@@ -41,6 +41,10 @@ def WINO_CSPLIT(n: int) -> int:
     return (n & 0xF) << 16
 
 
+def WINO_CSLICES(n: int) -> int:
+    return (n & 0xF) << 20
+
+
 class WinoError(RuntimeError):
     def __init__(self, status: int, where: str = ""):
         self.status = status

@@ -12,9 +12,9 @@ namespace {
 constexpr int64_t kMaxElems = (int64_t)1 << 40;      // per tensor, well inside size_t
 constexpr int64_t kMaxTiles = ((int64_t)1 << 31) - 64;
 
-constexpr unsigned kBlockMask = WINO_BLOCK_1x16 | WINO_BLOCK_4x4, kCsplitShift = 16;
+constexpr unsigned kBlockMask = WINO_BLOCK_1x16 | WINO_BLOCK_4x4, kCsplitShift = 16, kSliceShift = 20;
 constexpr unsigned kKnownFlags =
-    WINO_FLAG_RELU | WINO_PREC_MASK | WINO_ALGO_MASK | kBlockMask | (0xFu << kCsplitShift);
+    WINO_FLAG_RELU | WINO_PREC_MASK | WINO_ALGO_MASK | kBlockMask | (0xFu << kCsplitShift) | (0xFu << kSliceShift);
 
 // 16-bit GEMM operand format from the flags: 0 (fp32), 1 (fp16), 2 (bf16), -1 (invalid).
 int prec_of(unsigned flags) {
@@ -160,6 +160,11 @@ double split_ns(const Geom& g, int bw) {
 
 size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeof(float); }
 
+// Partial outputs of the channel slices: [slices used][N][K][Ho][Wo].
+size_t slice_workspace(const Geom& g, int nsl) {
+    return (size_t)slices_used(g, nsl) * g.N * g.K * g.Ho * g.Wo * sizeof(float);
+}
+
 // Offsets into x that the NCHW input kernels form (see kInvalidOffset): one
 // image for the fused and split kernels; for the staged input transforms the
 // images one 16-tile block spans, at most 16 / (th*tw) + 2.
@@ -196,14 +201,17 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     if (prec < 0) return WINO_ERR_UNSUPPORTED;
     if (prec && (g.r != 3 || g.axis != 0 || g.nhwc)) return WINO_ERR_UNSUPPORTED;
     if (g.axis != 0 || g.nhwc || prec) {
-        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF)
+        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF ||
+            (flags >> kSliceShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->algo = WINO_ALGO_STAGED;
         p->automatic = algo == WINO_ALGO_AUTO;
-        p->cfg = FusedCfg{1, 16};
+        p->cfg = FusedCfg{1, 16, 1};
         return WINO_OK;
     }
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
+    const int sl_req = (int)((flags >> kSliceShift) & 0xF);
+    if (sl_req > 8 || (sl_req > 1 && (algo != WINO_ALGO_FUSED || sl_req > g.CQ))) return WINO_ERR_UNSUPPORTED;
     if (g.r != 3 && (algo == WINO_ALGO_SPLIT || algo == WINO_ALGO_LOWC)) return WINO_ERR_UNSUPPORTED;
     const int cs_req = (int)((flags >> kCsplitShift) & 0xF);
     p->algo = algo == WINO_ALGO_AUTO ? WINO_ALGO_FUSED : algo;
@@ -216,6 +224,7 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     // staged input patch) and leaves no wave without a filter block of its
     // own, else the largest available.
     FusedCfg c;
+    c.nsl = 1;
     c.bw = blk == WINO_BLOCK_1x16 ? 16
          : blk == WINO_BLOCK_4x4  ? 4
          : (g.tw >= 12 && block_util(g, 16) >= 0.75 * block_util(g, 4) ? 16 : 4);
@@ -242,6 +251,21 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     if (p->automatic && g.r == 3 && !cs_req && split_items(g, c.bw) >= (long)kCus &&
         split_ns(g, c.bw) < fused_ns(g, c))
         p->algo = WINO_ALGO_SPLIT;
+    // Channel slices over workgroups for fused layers that leave CUs idle with
+    // a long channel loop each (deep layers at small batch): double the slices
+    // while the workgroups still fit one round on the 256 CUs and every slice
+    // keeps at least 4 channel steps.  Partial outputs go to the workspace and
+    // one more launch sums them in slice order.
+    if (p->algo == WINO_ALGO_FUSED && sl_req > 1) {
+        p->cfg.nsl = sl_req;
+    } else if (p->algo == WINO_ALGO_FUSED && p->automatic && !sl_req) {
+        const long wgs = fused_workgroups(g, c);
+        const int qs = 8 / row_groups(g);                   // quads per channel step
+        const int steps = (g.CQ + qs - 1) / qs;
+        int nsl = 1;
+        while (nsl < 8 && wgs * nsl * 2 <= (long)kCus && steps / (nsl * 2) >= 4) nsl *= 2;
+        p->cfg.nsl = nsl;
+    }
     return WINO_OK;
 }
 
@@ -310,6 +334,7 @@ size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m,
     if (make_geom_r(N, C, H, W, K, pad, m, r, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
     if (prec_of(flags)) return round_up(vh_bytes(g), 256) + m_elems(g) * sizeof(float);
+    if (p.algo == WINO_ALGO_FUSED && p.cfg.nsl > 1) return slice_workspace(g, p.cfg.nsl);
     if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
     if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
@@ -375,6 +400,17 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
             if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
                 return WINO_ERR_INVALID_ARG;
             return hip_status(launch_split(x, U, y, (float*)workspace, g, p.cfg.bw, relu, s));
+        }
+    }
+    if (p.algo == WINO_ALGO_FUSED && p.cfg.nsl > 1) {
+        const size_t need = slice_workspace(g, p.cfg.nsl);
+        if (!workspace || workspace_bytes < need) {
+            if (!p.automatic) return WINO_ERR_WORKSPACE;
+            p.cfg.nsl = 1;                      // no room for the partial outputs: unsliced
+        } else {
+            if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+                return WINO_ERR_INVALID_ARG;
+            return hip_status(launch_fused(x, U, y, g, p.cfg, relu, s, (float*)workspace));
         }
     }
     if (p.algo == WINO_ALGO_FUSED) return hip_status(launch_fused(x, U, y, g, p.cfg, relu, s));

@@ -32,6 +32,7 @@ struct Geom {
 struct FusedCfg {
     int csplit;     // waves of one workgroup splitting the channel quads of a unit
     int bw;         // tile-block width: 16 (1 x 16 tiles) or 4 (4 x 4 tiles)
+    int nsl;        // channel slices over workgroups (1: none), summed by k_slice_sum
 };
 
 // Division of n < 2^31 by a fixed d >= 1 as ((mulhi(n, m) + n) >> l), with
@@ -54,6 +55,10 @@ struct FusedTiling {
     FastDiv d_item; // fused path: item -> (quotient, remainder) by nkg (kfast) or nt
     FastDiv d_img;  // by nbh * nbw (tile blocks per image)
     FastDiv d_nbw;  // by nbw
+    int nsl;        // channel slices: workgroup items nt * nkg per slice
+    int qsl;        // channel quads per slice
+    FastDiv d_sl;   // by nt * nkg
+    long long ysz;  // N*K*Ho*Wo: floats of one slice's partial output
 };
 
 size_t filter_elems(int C, int K, int m, int r);         // T*Cp*Kp
@@ -64,8 +69,13 @@ hipError_t launch_filter_transform(const float* g, float* U, int C, int K, int m
 hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s);
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s);
 hipError_t launch_output_transform(const float* M, float* y, const Geom& g, bool relu, hipStream_t s);
+// cfg.nsl > 1: the channels in cfg.nsl slices over workgroups, partial outputs
+// to part ([nsl][N][K][Ho][Wo]), then summed in slice order into y.
 hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg cfg,
-                        bool relu, hipStream_t s);
+                        bool relu, hipStream_t s, float* part = nullptr);
+// Channel quads per slice, and the slices that hold any, for a requested count.
+int slice_quads(const Geom& g, int nsl);
+int slices_used(const Geom& g, int nsl);
 // Split path: input transform into a tile-blocked workspace, then the GEMMs
 // with the output transform in their epilogue.
 long split_blocks(const Geom& g, int bw);

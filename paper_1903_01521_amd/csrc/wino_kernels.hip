@@ -550,7 +550,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
                                             uint32_t step_b, const float* __restrict__ U, const Geom& g,
                                             const FusedTiling& ft, int kb, int wave, int lane, int kw, int cs,
                                             int bi, int bj, float* xs0, float* xs1, float* xs2, float* vs,
-                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC, RF>::TH], int xlo) {
+                                            f32x4 (&acc)[FusedShape<MT, TS, CS, BW, VEC, RF>::TH], int xlo,
+                                            int cq0, int cqn, int nsteps) {
     using S = FusedShape<MT, TS, CS, BW, VEC, RF>;
     constexpr int A = S::A, RN = S::RN, X0 = H * RN, TH = S::TH, T = S::T, QS = S::QS, KGW = S::KGW;
     constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;   // this row group's position groups
@@ -573,12 +574,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + xlo + (i * 512 + wave * 64) * S::EW, 4 * S::EW,
                                                      xoff[i] + cbase, 0, 0, 0);
     };
-    // Filters of (step j, quad slot q): a quad past CQ repeats a valid block (it
-    // meets zero regions); past the last step it repeats the last step.
+    // Filters of (step j, quad slot q) of the channel slice [cq0, cq0 + cqn): a
+    // quad past the slice repeats a valid block (it meets zero regions, the
+    // patch buffer ending at the slice); past the last step it repeats the last.
     const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
     const uint32_t ulane = (uint32_t)lane * 16u;
     auto load_u = [&](int j, int q, f32x4 (&ug)[NG]) {
-        const int cq = min(min(j, ft.nsteps - 1) * QS + q, g.CQ - 1);
+        const int cq = cq0 + min(min(j, nsteps - 1) * QS + q, cqn - 1);
         const uint32_t go = __builtin_amdgcn_readfirstlane((uint32_t)(((kb * g.CQ + cq) * (T / 4) + G0) * 1024));
 #pragma unroll
         for (int i = 0; i < NG; ++i) ug[i] = u_load(ur, ulane, go + i * 1024u);
@@ -644,13 +646,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             mfma_quad(v, uring(IC<R>{}));
         };
         int s = 0;
-        for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
+        for (; s + 3 <= nsteps; s += 3) {   // straight-line body: exact wait analysis
             step(IC<0>{}, s);
             step(IC<1>{}, s + 1);
             step(IC<2>{}, s + 2);
         }
-        if (s < ft.nsteps) step(IC<0>{}, s);
-        if (s + 1 < ft.nsteps) step(IC<1>{}, s + 1);
+        if (s < nsteps) step(IC<0>{}, s);
+        if (s + 1 < nsteps) step(IC<1>{}, s + 1);
     } else {
         // Step s: for each filter-block slot kw' the MFMAs of quad kw'*CS + cs
         // from the V stage, then (after every wave has read it) the transform of
@@ -716,7 +718,7 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
 #pragma unroll
                 for (int i = 0; i < NG; ++i) ua[i] = ub[i];
             }
-            if (s + 1 < ft.nsteps) {
+            if (s + 1 < nsteps) {
                 wait_vm_lds<WAITT>();      // patch s+1 has landed and V(s) is read (this wave)
                 wg_barrier();              // ... every wave
                 float v[TH];
@@ -726,13 +728,13 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             issue_x(IC<R>{}, s + 3);       // stage R held patch s, transformed at the end of step s-1
         };
         int s = 0;
-        for (; s + 3 <= ft.nsteps; s += 3) {   // straight-line body: exact wait analysis
+        for (; s + 3 <= nsteps; s += 3) {   // straight-line body: exact wait analysis
             step(IC<0>{}, s);
             step(IC<1>{}, s + 1);
             step(IC<2>{}, s + 2);
         }
-        if (s < ft.nsteps) step(IC<0>{}, s);
-        if (s + 1 < ft.nsteps) step(IC<1>{}, s + 1);
+        if (s < nsteps) step(IC<0>{}, s);
+        if (s + 1 < nsteps) step(IC<1>{}, s + 1);
     }
     __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
 }
@@ -754,7 +756,7 @@ __device__ __forceinline__ void fused_share(const f32x4 (&acc)[FusedShape<MT, TS
 template <int MT, int TS, int CS, int BW, int VEC, int RF = 3>
 __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, const float* __restrict__ U,
                                                float* __restrict__ y, Geom g, FusedTiling ft, int relu,
-                                               int vec_ok, int nts) {
+                                               int vec_ok, int nts, float* __restrict__ ypart) {
     using S = FusedShape<MT, TS, CS, BW, VEC, RF>;
     constexpr int PARTS = S::PARTS, KGW = S::KGW;
     __shared__ float4 xs0[S::XST / 4], xs1[S::XST / 4], xs2[S::XST / 4];   // patch stages
@@ -765,9 +767,13 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     // Filter-group-major order keeps one or two groups' filters in an XCD's L2;
     // tile-major order (kfast) keeps the XCD's input patches there instead, and
     // every filter group of a patch reads it from L2.
+    // With channel slices the slice is the slowest index of the item.
     const int b = blockIdx.x;
-    const int item = (b & 7) * ft.per + (b >> 3);
-    if (item >= ft.nt * ft.nkg) return;
+    const int per_sl = ft.nt * ft.nkg;
+    const int item0 = (b & 7) * ft.per + (b >> 3);
+    if (item0 >= per_sl * ft.nsl) return;
+    const int sl = ft.nsl > 1 ? (int)fdiv((uint32_t)item0, ft.d_sl) : 0;
+    const int item = item0 - sl * per_sl;
     const int iq = (int)fdiv((uint32_t)item, ft.d_item), ir = item - iq * (ft.kfast ? ft.nkg : ft.nt);
     const int kgi = ft.kfast ? ir : iq;
     const int tb = ft.kfast ? iq : ir;
@@ -791,10 +797,16 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     // row).  VEC: loads are 16-byte chunks from column col0, which is the patch's
     // first column moved back by xsh to a multiple of 4; with W % 4 == 0 every
     // chunk lies wholly inside or wholly outside the row.
+    // The buffer covers this slice's channels of image n only: channels past
+    // the slice (or past C) read as zeros.
+    const int cq0 = sl * ft.qsl, cqn = min(ft.qsl, g.CQ - cq0);
+    const int c0 = cq0 * 4, cn = min(g.C - c0, cqn * 4);
+    const int nsteps = (cqn + S::QS - 1) / S::QS;
     const size_t img = (size_t)g.C * g.H * g.W;
-    const size_t img_b = img * 4;
+    const size_t sl_b = (size_t)cn * g.H * g.W * 4;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(x + (size_t)n * img), (short)0, (int)(img_b < kInvalid ? img_b : kInvalid), kRsrcWord3);
+        (void*)(x + (size_t)n * img + (size_t)c0 * g.H * g.W), (short)0, (int)(sl_b < kInvalid ? sl_b : kInvalid),
+        kRsrcWord3);
     const uint32_t plane_b = (uint32_t)g.H * g.W * 4;
     // In LDS the chunks start xlo floats past the stage base, which puts the
     // patch's first column (xsh floats into its chunk) on a 16-byte boundary.
@@ -823,13 +835,13 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     float* vsf = (float*)vs;
     if constexpr (TS == 1) {
         fused_steps<MT, TS, CS, BW, VEC, 0, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
-                                       xs2f, vsf, acc, xlo);
+                                       xs2f, vsf, acc, xlo, cq0, cqn, nsteps);
     } else if (h == 0) {
         fused_steps<MT, TS, CS, BW, VEC, 0, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
-                                       xs2f, vsf, acc, xlo);
+                                       xs2f, vsf, acc, xlo, cq0, cqn, nsteps);
     } else {
         fused_steps<MT, TS, CS, BW, VEC, 1, RF>(xr, xoff, step_b, U, g, ft, kb, wave, lane, kw, cs, bi, bj, xs0f, xs1f,
-                                       xs2f, vsf, acc, xlo);
+                                       xs2f, vsf, acc, xlo, cq0, cqn, nsteps);
     }
 
     // ---- epilogue.  Every load has landed (fused_steps ends with a full
@@ -994,12 +1006,14 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     }
 #undef WINO_O
     const int kset = (kgi * KGW + kw) * 16 + 4 * cl + fset * NF;   // first filter of this wave's set
-    const bool rl = relu != 0, vo = vec_ok != 0;
+    // A slice's partial output goes to its own plane of part, without ReLU.
+    float* const yo = ft.nsl > 1 ? ypart + (size_t)sl * (size_t)ft.ysz : y;
+    const bool rl = relu != 0 && ft.nsl == 1, vo = vec_ok != 0;
 #pragma unroll
     for (int rr = 0; rr < NR2; ++rr) {
         const int rho = q * NR2 + rr;
-        if (nts) store_row<MT, true>(y, g, tc, kset + rho / MT, rho % MT, fin[rr], rl, vo);
-        else store_row<MT, false>(y, g, tc, kset + rho / MT, rho % MT, fin[rr], rl, vo);
+        if (nts) store_row<MT, true>(yo, g, tc, kset + rho / MT, rho % MT, fin[rr], rl, vo);
+        else store_row<MT, false>(yo, g, tc, kset + rho / MT, rho % MT, fin[rr], rl, vo);
     }
 }
 
@@ -2119,16 +2133,36 @@ static hipError_t fused_lds_check(hipStream_t s) {
     return ok ? hipSuccess : hipErrorInvalidKernelFile;
 }
 
+// y[i] = max?(sum over slices s = 0, 1, ... of part[s][i]), in that order.
+__global__ __launch_bounds__(256) void k_slice_sum(const float* __restrict__ part, float* __restrict__ y,
+                                                   long long count, int nsl, int relu) {
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= count) return;
+    float v = part[i];
+    for (int k = 1; k < nsl; ++k) v += part[(size_t)k * (size_t)count + (size_t)i];
+    y[i] = relu ? fmaxf(v, 0.0f) : v;
+}
+
+int slice_quads(const Geom& g, int nsl) { return (g.CQ + nsl - 1) / nsl; }
+int slices_used(const Geom& g, int nsl) {
+    const int q = slice_quads(g, nsl);
+    return (g.CQ + q - 1) / q;
+}
+
 template <int MT, int TS, int CS, int BW, int R = 3>
 static hipError_t fused_instance(const float* x, const float* U, float* y, const Geom& g, bool relu,
-                                 hipStream_t s) {
+                                 hipStream_t s, int nsl_req, float* part) {
     using S = FusedShape<MT, TS, CS, BW, 0, R>;
     FusedTiling ft{};
     ft.nbh = (g.th + S::BH - 1) / S::BH;
     ft.nbw = (g.tw + BW - 1) / BW;
     ft.nt = g.N * ft.nbh * ft.nbw;
     ft.nkg = (g.KB + S::KGW - 1) / S::KGW;
-    ft.per = (int)(((long)ft.nt * ft.nkg + 7) / 8);
+    ft.nsl = part && nsl_req > 1 ? slices_used(g, nsl_req) : 1;
+    ft.qsl = ft.nsl > 1 ? slice_quads(g, nsl_req) : g.CQ;
+    ft.ysz = (long long)g.N * g.K * g.Ho * g.Wo;
+    ft.d_sl = make_fastdiv((uint32_t)(ft.nt * ft.nkg));
+    ft.per = (int)(((long)ft.nt * ft.nkg * ft.nsl + 7) / 8);
     ft.nsteps = (g.CQ + S::QS - 1) / S::QS;
     // Item order: estimate the bytes an XCD fetches past its L2 for each order,
     // with one workgroup per CU (32 per XCD) resident at a time.  Filter-group
@@ -2145,7 +2179,18 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
     ft.d_img = make_fastdiv((uint32_t)(ft.nbh * ft.nbw));
     ft.d_nbw = make_fastdiv((uint32_t)ft.nbw);
     const dim3 grid((unsigned)(8 * ft.per)), block(512);
-    const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
+    float* const pp = ft.nsl > 1 ? part : nullptr;
+    const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT) && (!pp || aligned(pp, 4 * MT));
+    // Partial outputs are read back at once: plain stores keep them in L2.
+    const int nts = pp ? 0 : stream_stores(g);
+    auto finish = [&]() -> hipError_t {
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || !pp) return e;
+        const long long cnt = ft.ysz;
+        hipLaunchKernelGGL(k_slice_sum, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, s, pp, y, cnt, ft.nsl,
+                           (int)relu);
+        return hipGetLastError();
+    };
     // 16-byte patch loads need rows of whole chunks and an aligned image base,
     // and the variant's larger stages must fit in LDS.
     if constexpr (FusedShape<MT, TS, CS, BW, 1, R>::LDS_BYTES <= kMaxLdsBytes) {
@@ -2153,24 +2198,24 @@ static hipError_t fused_instance(const float* x, const float* U, float* y, const
             const hipError_t e = fused_lds_check<MT, TS, CS, BW, 1, R>(s);
             if (e != hipSuccess) return e;
             hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 1, R>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
-                               stream_stores(g));
-            return hipGetLastError();
+                               nts, pp);
+            return finish();
         }
     }
     const hipError_t e = fused_lds_check<MT, TS, CS, BW, 0, R>(s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_fused<MT, TS, CS, BW, 0, R>), grid, block, 0, s, x, U, y, g, ft, (int)relu, vec_ok,
-                       stream_stores(g));
-    return hipGetLastError();
+                       nts, pp);
+    return finish();
 }
 
 hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g, FusedCfg c, bool relu,
-                        hipStream_t s) {
+                        hipStream_t s, float* part) {
     // 3x3, m = 2: all 16 positions per wave; m = 4 and 5x5 (alpha = 6): two
     // row groups of 18 positions.
     if (g.r == 5) {
 #define WINO_FUSED_R5(CS, BW) \
-    if (g.m == 2 && c.csplit == CS && c.bw == BW) return fused_instance<2, 2, CS, BW, 5>(x, U, y, g, relu, s);
+    if (g.m == 2 && c.csplit == CS && c.bw == BW) return fused_instance<2, 2, CS, BW, 5>(x, U, y, g, relu, s, c.nsl, part);
         WINO_FUSED_R5(1, 16)
         WINO_FUSED_R5(2, 16)
         WINO_FUSED_R5(4, 16)
@@ -2182,7 +2227,7 @@ hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g,
     }
     if (g.r != 3) return hipErrorInvalidValue;
 #define WINO_FUSED_CASE(MT, TS, CS, BW) \
-    if (g.m == MT && c.csplit == CS && c.bw == BW) return fused_instance<MT, TS, CS, BW>(x, U, y, g, relu, s);
+    if (g.m == MT && c.csplit == CS && c.bw == BW) return fused_instance<MT, TS, CS, BW>(x, U, y, g, relu, s, c.nsl, part);
     WINO_FUSED_CASE(2, 1, 1, 16)
     WINO_FUSED_CASE(2, 1, 2, 16)
     WINO_FUSED_CASE(2, 1, 4, 16)

@@ -241,3 +241,28 @@ def test_mfma_probe_arguments():
     assert B.wino_probe_mfma_f32_flops(1000) == 1000 * 2048 * 8 * 2048
     assert B.wino_probe_mfma_f32_flops(0) == 0
     assert B.wino_probe_mfma_f32_flops(2 ** 21 + 1) == 0
+
+
+def test_channel_slice_sizes_and_rejections():
+    F = B.WINO_ALGO_FUSED
+    # 64 channels = 16 quads in 3 slices of 6 quads: 3 partial outputs
+    assert B.wino_workspace_bytes(1, 64, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(3)) == 3 * 16 * 20 * 20 * 4
+    # 20 quads in 8 slices of 3: 7 slices hold channels
+    assert B.wino_workspace_bytes(1, 80, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(8)) == 7 * 16 * 20 * 20 * 4
+    assert B.wino_workspace_bytes(1, 64, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(1)) == 0
+    for flags in (B.WINO_CSLICES(2),                          # only with an explicit WINO_ALGO_FUSED
+                  B.WINO_ALGO_STAGED | B.WINO_CSLICES(2), B.WINO_ALGO_SPLIT | B.WINO_CSLICES(2),
+                  F | B.WINO_CSLICES(9)):
+        assert B.wino_workspace_bytes(1, 64, 20, 20, 16, 1, 4, flags) == 2**64 - 1
+    assert B.wino_workspace_bytes(1, 8, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(3)) == 2**64 - 1   # 2 quads
+    assert B.wino_workspace_bytes_1d(1, 64, 17, 17, 16, 3, 2, 7, B.WINO_AXIS_W, B.WINO_CSLICES(2)) == 2**64 - 1
+    # the planner: VGG-16's 512-channel 28x28 layer at batch 1 gets two slices;
+    # the bench layer (224 workgroups) and batch-8 ResNet layers get none
+    assert B.wino_workspace_bytes(1, 512, 28, 28, 512, 1, 4, 0) == 2 * 512 * 28 * 28 * 4
+    assert B.wino_workspace_bytes(1, 512, 14, 14, 512, 1, 2, 0) == 2 * 512 * 14 * 14 * 4
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, 0) == 0
+    assert B.wino_workspace_bytes(8, 128, 28, 28, 128, 1, 4, 0) == 0
+    # missing workspace with explicit slices
+    y = FAKE + 0x1000000
+    assert B.wino_conv2d(FAKE, FAKE + 0x800000, y, 1, 64, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(2), None, 0) == \
+        B.WINO_ERR_WORKSPACE
