@@ -54,7 +54,9 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
                 "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
                 # the split path's call: the input transform, then the GEMMs with the output transform
-                "split": ("void wino::k_vblk", "void wino::k_gemm_out")}
+                "split": ("void wino::k_vblk", "void wino::k_gemm_out"),
+                # the fused kernel over channel slices, then the sum of the slices
+                "fused_sliced": ("void wino::k_fused", "void wino::k_slice_sum")}
 
 
 def kernel_label(kind: str) -> str:
@@ -98,6 +100,7 @@ def layer_numbers(N, L):
     f["bytes"] = {
         "filter": 4 * L.K * L.C * taps + u_b,
         "fused": x_b + u_b + y_b,
+        "fused_sliced": x_b + u_b + y_b,
         "split": x_b + u_b + y_b,
         "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
@@ -109,7 +112,8 @@ def layer_numbers(N, L):
         # the same with 16-bit V and U (fp16 / bf16 GEMM operands)
         "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
     }
-    f["flops"] = {"fused": f["gemm_flops"], "split": f["gemm_flops"], "gemm": f["gemm_flops"],
+    f["flops"] = {"fused": f["gemm_flops"], "fused_sliced": f["gemm_flops"], "split": f["gemm_flops"],
+                  "gemm": f["gemm_flops"],
                   "stages": f["gemm_flops"],
                   "stages16": f["gemm_flops"]}
     return f
@@ -135,7 +139,7 @@ def roofline(kind, nums, seconds):
 def traffic_file(workload: str, kind: str) -> str:
     """Counter summary of a workload's convolution kernel (fused, low-C), or of
     one stage of its staged path (input, gemm, output)."""
-    if kind in ("fused", "split", "lowc"):
+    if kind in ("fused", "fused_sliced", "split", "lowc"):
         return os.path.join(PROFILES, f"traffic_{workload}.txt")
     return os.path.join(PROFILES, f"traffic_{workload}_{kind}.txt")
 
@@ -391,9 +395,10 @@ def main():
                     Ms[i], ys[i], N, L.K, L.H, L.W, L.pad, L.m, L.r, relu, sp))))
             else:
                 ws, wsb = wss[i]
-                algo = flags & B.WINO_ALGO_MASK
-                lowc = algo == B.WINO_ALGO_LOWC or (algo == B.WINO_ALGO_AUTO and L.C <= 4 and L.r == 3)
-                kind = "stages16" if prec else "lowc" if lowc else "split" if wsb else "fused"
+                st, algo, nsl = B.wino_plan_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags | relu)
+                B.check(st, "wino_plan_r")
+                kind = "stages16" if prec else {B.WINO_ALGO_LOWC: "lowc", B.WINO_ALGO_SPLIT: "split"}.get(
+                    algo, "fused_sliced" if nsl > 1 else "fused")
                 out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                        L.pad, L.m, L.r, flags | relu,

@@ -147,6 +147,15 @@ size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, u
  * Errors: INVALID_ARG (null, C/K <= 0, overflow), UNSUPPORTED (m), HIP. */
 int wino_filter_transform(const float* g, float* U, int C, int K, int m, void* stream);
 
+/* The planner's choice for a layer (r = 3, or 5 with m = 2), for callers that
+ * pass the workspace wino_workspace_bytes(_r) reports: *algo = the
+ * WINO_ALGO_* value that runs (FUSED, SPLIT, STAGED or LOWC), *slices = the
+ * fused kernel's channel slices (1 when unsliced or not fused).  Errors as for
+ * wino_workspace_bytes_r's arguments (INVALID_ARG, UNSUPPORTED); null outputs
+ * are INVALID_ARG. */
+int wino_plan_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsigned flags, unsigned* algo,
+                int* slices);
+
 /* One 3x3 stride-1 convolution layer (Eq. 1 over all regions; Sec. 2).
  *   x : [N][C][H][W] fp32 (NCHW), read only.
  *   U : output of wino_filter_transform with the same (C, K, m), read only.

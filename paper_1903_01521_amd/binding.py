@@ -68,6 +68,7 @@ _SIGS = {
     "wino_output_transform": ([_vp, _vp] + [_c_int] * 6 + [_c_uint, _vp], _c_int),
     "wino_maxpool2x2": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
     "wino_probe_mfma_f32": ([_c_int, _vp, _vp], _c_int),
+    "wino_plan_r": ([_c_int] * 8 + [_c_uint, _vp, _vp], _c_int),
     "wino_probe_mfma_f32_flops": ([_c_int], _c_size),
     "wino_filter_bytes_r": ([_c_int] * 4, _c_size),
     "wino_filter_transform_r": ([_vp, _vp] + [_c_int] * 4 + [_vp], _c_int),
@@ -192,6 +193,13 @@ def wino_output_transform(M, y, N, K, H, W, pad, m, flags=0, stream=None) -> int
 
 def wino_maxpool2x2(x, y, N, C, H, W, stream=None) -> int:
     return lib().wino_maxpool2x2(_fptr(x), _fptr(y), N, C, H, W, _stream(stream))
+
+
+def wino_plan_r(N, C, H, W, K, pad, m, r, flags=0):
+    """(status, algo, slices): the planner's choice, given the workspace it asks for."""
+    algo, slices = ctypes.c_uint(0), ctypes.c_int(0)
+    st = lib().wino_plan_r(N, C, H, W, K, pad, m, r, flags, ctypes.byref(algo), ctypes.byref(slices))
+    return st, algo.value, slices.value
 
 
 def wino_probe_mfma_f32(iters, out, stream=None) -> int:

@@ -340,6 +340,20 @@ size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m,
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
 
+int wino_plan_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsigned flags, unsigned* algo,
+                int* slices) {
+    if (!algo || !slices) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    int st = make_geom_r(N, C, H, W, K, pad, m, r, &g);
+    if (st != WINO_OK) return st;
+    Plan p;
+    st = make_plan(g, flags, &p);
+    if (st != WINO_OK) return st;
+    *algo = p.algo;
+    *slices = p.algo == WINO_ALGO_FUSED && p.cfg.nsl > 1 ? slices_used(g, p.cfg.nsl) : 1;
+    return WINO_OK;
+}
+
 size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags) {
     return wino_workspace_bytes_r(N, C, H, W, K, pad, m, 3, flags);
 }

@@ -266,3 +266,17 @@ def test_channel_slice_sizes_and_rejections():
     y = FAKE + 0x1000000
     assert B.wino_conv2d(FAKE, FAKE + 0x800000, y, 1, 64, 20, 20, 16, 1, 4, F | B.WINO_CSLICES(2), None, 0) == \
         B.WINO_ERR_WORKSPACE
+
+
+def test_plan_query():
+    F = B.WINO_ALGO_FUSED
+    assert B.wino_plan_r(1, 64, 112, 112, 64, 1, 4, 3, 0) == (B.WINO_OK, F, 1)
+    assert B.wino_plan_r(1, 512, 28, 28, 512, 1, 4, 3, 0) == (B.WINO_OK, F, 2)
+    assert B.wino_plan_r(1, 3, 224, 224, 64, 1, 4, 3, 0) == (B.WINO_OK, B.WINO_ALGO_LOWC, 1)
+    assert B.wino_plan_r(64, 256, 56, 56, 256, 1, 4, 3, 0) == (B.WINO_OK, B.WINO_ALGO_SPLIT, 1)
+    assert B.wino_plan_r(1, 64, 20, 20, 16, 1, 4, 3, B.WINO_ALGO_STAGED) == (B.WINO_OK, B.WINO_ALGO_STAGED, 1)
+    assert B.wino_plan_r(1, 80, 20, 20, 16, 1, 4, 3, F | B.WINO_CSLICES(8)) == (B.WINO_OK, F, 7)
+    assert B.wino_plan_r(32, 48, 35, 35, 64, 2, 2, 5, 0) == (B.WINO_OK, F, 1)
+    assert B.wino_plan_r(1, 64, 20, 20, 16, 1, 3, 3, 0)[0] == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_plan_r(0, 64, 20, 20, 16, 1, 4, 3, 0)[0] == B.WINO_ERR_INVALID_ARG
+    assert B.lib().wino_plan_r(1, 64, 20, 20, 16, 1, 4, 3, 0, None, None) == B.WINO_ERR_INVALID_ARG

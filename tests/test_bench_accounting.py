@@ -57,3 +57,14 @@ def test_roofline_bound(name, kind, bound):
         assert r["achieved"] == pytest.approx(f["flops"][kind] / 1e-3 / 1e12, rel=1e-3)
     else:
         assert r["achieved"] == pytest.approx(f["bytes"][kind] / 1e-3 / 1e9, rel=1e-3)
+
+
+def test_sliced_fused_accounting_equals_fused():
+    # Channel slices change how the fused kernel runs, not the layer's
+    # algorithmic work: the same bytes and FLOPs as the unsliced kernel.
+    L = wl.WORKLOADS["vgg16_stack_n1"].layers[8]            # 512 -> 512 at 28 x 28
+    f = bench.layer_numbers(1, L)
+    assert f["bytes"]["fused_sliced"] == f["bytes"]["fused"]
+    assert f["flops"]["fused_sliced"] == f["flops"]["fused"]
+    assert bench.kernel_label("fused_sliced") == "wino::k_fused + wino::k_slice_sum"
+    assert bench.traffic_file("vgg16_stack_n1", "fused_sliced").endswith("traffic_vgg16_stack_n1.txt")
