@@ -182,6 +182,75 @@ def kernel_is(name: str, prefix: str) -> bool:
     return n.startswith(base) and n[len(base):len(base) + 1] in ("<", "(")
 
 
+MFMA_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE")
+
+
+def mfma_summary(args):
+    """Matrix-core work of a kind of launch from one rocprofv3 PMC run of this
+    script with MFMA_COUNTERS.  On MI355X SQ_VALU_MFMA_BUSY_CYCLES reads 32 per
+    v_mfma_f32_16x16x4_f32 (its issue cycles), so it measures work, not time;
+    GRBM_GUI_ACTIVE is summed over the 8 XCDs.  Busy cycles over the active
+    cycles of 1024 SIMDs give the utilisation while the launch ran (under the
+    profiler, whose per-dispatch overhead weighs on short launches); the MFMA
+    probe in the same run calibrates it (its value is its measured share of the
+    published peak).  The instruction count checks the launch does exactly the
+    MFMA work the algorithm needs, plus the padding of partial tile blocks."""
+    from paper_1903_01521_amd import workloads as wl
+    name = args.workload or wl.DEFAULT_BENCH
+    w = wl.WORKLOADS[name]
+    nums = [layer_numbers(w.N, L) for L in w.layers]
+    kind = args.kind
+    prefixes = KERNEL_NAMES[kind]
+    prefixes = (prefixes,) if isinstance(prefixes, str) else prefixes
+    rows = pmc_rows(args.mfma_summary)
+
+    def mean(counter, pref):
+        v = [float(r["Counter_Value"]) for r in rows if r["Counter_Name"] == counter and kernel_is(r["Kernel_Name"], pref)]
+        if not v:
+            raise SystemExit(f"no {counter} rows for {pref} under {args.mfma_summary}")
+        return float(np.mean(v)), len(v)
+
+    simds = 256 * 4
+    util = lambda busy, active: busy / (active / 8 * simds)
+    pb, pn = mean("SQ_VALU_MFMA_BUSY_CYCLES", "void wino::k_mfma_probe")
+    pg, _ = mean("GRBM_GUI_ACTIVE", "void wino::k_mfma_probe")
+    kb = sum(mean("SQ_VALU_MFMA_BUSY_CYCLES", p)[0] for p in prefixes)
+    kg = sum(mean("GRBM_GUI_ACTIVE", p)[0] for p in prefixes)
+    ki = sum(mean("SQ_INSTS_MFMA", p)[0] for p in prefixes)
+    kn = min(mean("SQ_INSTS_MFMA", p)[1] for p in prefixes)
+    need = sum(f["flops"].get(kind, 0) for f in nums) / len(nums) / (2 * 16 * 16 * 4)
+    fl = f" --flags {args.flags:#x}" if args.flags is not None else ""
+    lines = [
+        f"# MFMA work and utilisation of the {kind} launch on workload {name}, from one",
+        "# rocprofv3 PMC run of bench.py on one MI355X (command below).",
+        "#   mfma_insts: v_mfma_f32_16x16x4_f32 per launch, all waves (SQ_INSTS_MFMA);",
+        "#   mfma_insts_algorithmic: the launch's algorithmic FLOPs / 2048;",
+        "#   busy_cycles_per_inst: SQ_VALU_MFMA_BUSY_CYCLES / SQ_INSTS_MFMA;",
+        "#   util_active: busy cycles / (GRBM_GUI_ACTIVE / 8 XCDs * 1024 SIMDs), and the",
+        "#   same for the MFMA probe in this run (its share of the published peak).",
+        "#   cd /tmp && export TMPDIR=/tmp",
+        f"#   timeout -s KILL 90 rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d <out>/mfma "
+        f"-o run -- python3 <repo>/bench.py --workload {name}{fl} --steps 5 --warmup 1 --cpu-seconds 0 --no-graphs",
+        f"#   python3 bench.py --workload {name}{fl} --kind {kind} --mfma-summary <out>/mfma",
+        f"workload: {name}",
+        f"kind: {kind}",
+        f"kernels: {kernel_label(kind)}",
+        f"sources_sha256: {sources_hash()}",
+        f"dispatches: {kn}",
+        f"mfma_insts: {ki:.0f}",
+        f"mfma_insts_algorithmic: {need:.0f}",
+        f"mfma_insts_over_algorithmic: {ki / need:.4f}",
+        f"busy_cycles_per_inst: {kb / ki:.2f}",
+        f"util_active: {util(kb, kg):.3f}",
+        f"probe_util_active: {util(pb, pg):.3f} ({pn} dispatches)",
+    ]
+    text = "\n".join(lines) + "\n"
+    if args.write_summary:
+        with open(os.path.join(PROFILES, f"mfma_{name}_{kind}.txt"), "w") as fh:
+            fh.write(text)
+    print(text, end="")
+
+
 def pmc_summary(args):
     """Summarise a FETCH_SIZE run and a WRITE_SIZE run of this script."""
     from paper_1903_01521_amd import workloads as wl
@@ -279,6 +348,8 @@ def main():
                     help="CPU time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc csv runs (no GPU needed)")
+    ap.add_argument("--mfma-summary", metavar="DIR",
+                    help="summarise a rocprofv3 --pmc run with the MFMA counters (matrix-core utilisation)")
     ap.add_argument("--kind", default="fused", help="kernel kind the --pmc-summary covers")
     ap.add_argument("--write-summary", action="store_true",
                     help="with --pmc-summary: also write it to profiles/traffic_<workload>.txt")
@@ -286,6 +357,9 @@ def main():
 
     if args.pmc_summary:
         pmc_summary(args)
+        return
+    if args.mfma_summary:
+        mfma_summary(args)
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

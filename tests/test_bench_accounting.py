@@ -68,3 +68,30 @@ def test_sliced_fused_accounting_equals_fused():
     assert f["flops"]["fused_sliced"] == f["flops"]["fused"]
     assert bench.kernel_label("fused_sliced") == "wino::k_fused + wino::k_slice_sum"
     assert bench.traffic_file("vgg16_stack_n1", "fused_sliced").endswith("traffic_vgg16_stack_n1.txt")
+
+
+def test_mfma_summary_from_counter_rows(tmp_path, capsys):
+    # Synthetic counter rows: the probe busy 0.85 of 1024 SIMDs over its active
+    # cycles (summed over 8 XCDs), the bench layer's fused launch with the
+    # padded instruction count of 1 x 16 blocks on a 28-tile-wide grid.
+    import argparse
+    w = wl.WORKLOADS["f4_n1_c64_k64_112x112"]
+    need = bench.layer_numbers(w.N, w.first)["flops"]["fused"] / 2048
+    insts = need * 32 / 28
+    rows = [("void wino::k_mfma_probe(int, float*)", "SQ_VALU_MFMA_BUSY_CYCLES", 0.85 * 1024 * 1000),
+            ("void wino::k_mfma_probe(int, float*)", "GRBM_GUI_ACTIVE", 8 * 1000),
+            ("void wino::k_fused<4, 2, 4, 16, 1, 3>(float const*)", "SQ_INSTS_MFMA", insts),
+            ("void wino::k_fused<4, 2, 4, 16, 1, 3>(float const*)", "SQ_VALU_MFMA_BUSY_CYCLES", 32 * insts),
+            ("void wino::k_fused<4, 2, 4, 16, 1, 3>(float const*)", "GRBM_GUI_ACTIVE", 8 * 32 * insts / 1024 / 0.25)]
+    with open(tmp_path / "run_counter_collection.csv", "w") as f:
+        f.write("Kernel_Name,Counter_Name,Counter_Value\n")
+        for k, c, v in rows:
+            f.write(f'"{k}",{c},{v}\n')
+    args = argparse.Namespace(workload="f4_n1_c64_k64_112x112", kind="fused", mfma_summary=str(tmp_path),
+                              flags=None, write_summary=False)
+    bench.mfma_summary(args)
+    out = dict(l.split(": ", 1) for l in capsys.readouterr().out.splitlines() if not l.startswith("#"))
+    assert float(out["mfma_insts_over_algorithmic"]) == pytest.approx(32 / 28, rel=1e-4)
+    assert float(out["busy_cycles_per_inst"]) == pytest.approx(32.0)
+    assert float(out["util_active"]) == pytest.approx(0.25, abs=1e-3)
+    assert out["probe_util_active"].startswith("0.850")
