@@ -31,12 +31,20 @@
  *     with x read as zero outside [0,H) x [0,W).
  *   - Floating point is IEEE fp32 storage and fp32 arithmetic (the paper's
  *     precision, Sec. 3); FMA contraction is allowed; the GEMMs run on fp32 MFMA.
- *   - Size limit of the NCHW (channel-first) paths: one image's input,
- *     C*H*W*4 bytes, must be below 1 GiB for the fused and split algorithms,
- *     and (16 / (th*tw) + 2) such images below 1 GiB for the staged input
- *     transform (the images one 16-tile block spans); otherwise the call
- *     returns WINO_ERR_UNSUPPORTED.  The kernels address x through 32-bit
- *     offsets.  Split larger inputs along C or the image.
+ *   - Size limits of the NCHW (channel-first) paths, from the kernels' 32-bit
+ *     offsets into x: one image's input, C*H*W*4 bytes, must be below 1 GiB for
+ *     the fused and split algorithms, and (16 / (th*tw) + 2) such images below
+ *     1 GiB for the staged input transform (the images one 16-tile block
+ *     spans).  The fused and split kernels also read the channels past C (up
+ *     to whole channel steps) as zeros through offsets past the image, so
+ *     1 GiB + P*H*W*4 must stay below 4 GiB, with P = S * (steps + 3) for the
+ *     fused kernel (S = 32 channels a step for m = 2 and 3x3, 16 otherwise;
+ *     steps = ceil(channels of one slice / S)) and P = 16 * ceil(C/16) for
+ *     the split one.  A layer past a limit of an
+ *     explicitly chosen algorithm returns WINO_ERR_UNSUPPORTED; WINO_ALGO_AUTO
+ *     moves on to one that fits (fused, then split, then staged) and returns
+ *     WINO_ERR_UNSUPPORTED only when none does.  Split larger inputs along C
+ *     or the image.
  *
  * Tiling (Sec. 2, region decomposition)
  *   alpha = m + 2, T = alpha^2, th = ceil(Ho/m), tw = ceil(Wo/m),
@@ -133,10 +141,13 @@ size_t wino_filter_bytes(int C, int K, int m);
 size_t wino_input_tf_bytes(int N, int C, int H, int W, int pad, int m);
 size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m);
 
-/* Workspace bytes wino_conv2d needs for this layer and algorithm choice
- * (flags as for wino_conv2d; only the WINO_ALGO_* bits matter).  0 means the
- * chosen plan needs none (workspace may then be NULL).  Returns (size_t)-1 on
- * invalid arguments. */
+/* Workspace bytes wino_conv2d needs for this layer and flags word.  The
+ * result depends on the whole word as wino_conv2d reads it: the algorithm
+ * (and, for WINO_ALGO_AUTO, the planner's choice of split, channel slices or
+ * staged), WINO_PREC_* (16-bit V plus fp32 M), WINO_CSLICES(n) (the partial
+ * outputs) and the variant overrides.  0 means the plan needs none (workspace
+ * may then be NULL).  Returns (size_t)-1 for invalid arguments and for flag
+ * sets or layers that wino_conv2d would reject as WINO_ERR_UNSUPPORTED. */
 size_t wino_workspace_bytes(int N, int C, int H, int W, int K, int pad, int m, unsigned flags);
 
 /* Offline filter transform (Eq. 1's W w W^T; Sec. 2, the GEMM step's 'B'
@@ -166,7 +177,9 @@ int wino_plan_r(int N, int C, int H, int W, int K, int pad, int m, int r, unsign
  *       algorithm, the tile-blocked V of the split one, the partial outputs of
  *       channel slices); may be NULL/0 when that is 0.  With WINO_ALGO_AUTO the
  *       planner uses the split algorithm or channel slices only if the
- *       workspace given is large enough, else the plain fused kernel.  Contents on
+ *       workspace given is large enough, else the plain fused kernel (or
+ *       WINO_ERR_WORKSPACE where the fused kernel's offsets would not fit, see
+ *       the size limits above).  Contents on
  *       return are unspecified; calls sharing one workspace must not overlap in
  *       time.
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */

@@ -174,15 +174,58 @@ bool block_images_fit(const Geom& g) {
     return span * ((int64_t)g.C * g.H * g.W * 4) < (int64_t)kInvalidOffset;
 }
 
+// The fused and split kernels read channels past the slice (or past C) as
+// zeros: such a load's offset lies past the buffer's record count.  That holds
+// only while no 32-bit offset wraps round: the largest one a kernel forms must
+// stay below 2^32.
+constexpr int64_t kOffsetLimit = (int64_t)1 << 32;
+
+// Fused kernel: a step loads 4*QS channel planes (QS = 8 / row groups quads),
+// the prefetch runs up to three steps past a slice's last, and a load outside
+// the image adds its step's offset to kInvalidOffset.
+bool fused_offsets_fit(const Geom& g, const FusedCfg& c) {
+    const int64_t plane_b = (int64_t)g.H * g.W * 4, qs = 8 / row_groups(g);
+    const int64_t qsl = c.nsl > 1 ? (g.CQ + c.nsl - 1) / c.nsl : g.CQ;
+    const int64_t steps = (qsl + qs - 1) / qs;
+    return (int64_t)kInvalidOffset + (steps + 3) * 4 * qs * plane_b < kOffsetLimit;
+}
+
+// Split path's input transform: a workgroup loads 16 channel planes from the
+// offset of its group of 4 quads, over CQ rounded up to whole groups.
+bool split_offsets_fit(const Geom& g) {
+    const int64_t plane_b = (int64_t)g.H * g.W * 4, ncq4 = (g.CQ + 3) / 4;
+    return (int64_t)kInvalidOffset + ncq4 * 16 * plane_b < kOffsetLimit;
+}
+
+bool plan_fits(const Geom& g, const Plan& p) {
+    if (p.algo == WINO_ALGO_STAGED) return block_images_fit(g);
+    if (p.algo == WINO_ALGO_FUSED) return image_fits(g) && fused_offsets_fit(g, p.cfg);
+    if (p.algo == WINO_ALGO_SPLIT) return image_fits(g) && split_offsets_fit(g);
+    return true;
+}
+
 int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p);
 
-// The plan, or WINO_ERR_UNSUPPORTED where its input kernel's offsets would not fit.
+// The plan, or WINO_ERR_UNSUPPORTED where its input kernels' offsets would not
+// fit.  AUTO moves on to the next algorithm that fits: an unsliced fused plan
+// to split, then to the three stages.
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
     const int st = make_plan_unchecked(g, flags, p);
     if (st != WINO_OK || g.axis != 0 || g.nhwc) return st;
-    if (p->algo == WINO_ALGO_STAGED && !block_images_fit(g)) return WINO_ERR_UNSUPPORTED;
-    if ((p->algo == WINO_ALGO_FUSED || p->algo == WINO_ALGO_SPLIT) && !image_fits(g)) return WINO_ERR_UNSUPPORTED;
-    return WINO_OK;
+    if (plan_fits(g, *p)) return WINO_OK;
+    if (!p->automatic) return WINO_ERR_UNSUPPORTED;
+    if (p->algo == WINO_ALGO_FUSED && g.r == 3) {
+        Plan q = *p;
+        q.algo = WINO_ALGO_SPLIT;
+        q.cfg.nsl = 1;
+        if (plan_fits(g, q)) {
+            *p = q;
+            return WINO_OK;
+        }
+    }
+    p->algo = WINO_ALGO_STAGED;
+    p->cfg.nsl = 1;
+    return plan_fits(g, *p) ? WINO_OK : WINO_ERR_UNSUPPORTED;
 }
 
 int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
@@ -409,7 +452,8 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
         const size_t need = split_workspace(g, p.cfg.bw);
         if (!workspace || workspace_bytes < need) {
             if (!p.automatic) return WINO_ERR_WORKSPACE;
-            p.algo = WINO_ALGO_FUSED;
+            p.algo = WINO_ALGO_FUSED;          // no room for V: the fused kernel, where its offsets fit
+            if (!plan_fits(g, p)) return WINO_ERR_WORKSPACE;
         } else {
             if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
                 return WINO_ERR_INVALID_ARG;
@@ -421,6 +465,7 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
         if (!workspace || workspace_bytes < need) {
             if (!p.automatic) return WINO_ERR_WORKSPACE;
             p.cfg.nsl = 1;                      // no room for the partial outputs: unsliced
+            if (!plan_fits(g, p)) return WINO_ERR_WORKSPACE;
         } else {
             if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
                 return WINO_ERR_INVALID_ARG;

@@ -280,3 +280,33 @@ def test_plan_query():
     assert B.wino_plan_r(1, 64, 20, 20, 16, 1, 3, 3, 0)[0] == B.WINO_ERR_UNSUPPORTED
     assert B.wino_plan_r(0, 64, 20, 20, 16, 1, 4, 3, 0)[0] == B.WINO_ERR_INVALID_ARG
     assert B.lib().wino_plan_r(1, 64, 20, 20, 16, 1, 4, 3, 0, None, None) == B.WINO_ERR_INVALID_ARG
+
+
+def test_input_offsets_stay_below_2_32():
+    """The fused and split kernels read channels past C (or past a slice) as
+    zeros because their 32-bit offsets land past the buffer; layers where the
+    largest such offset would reach 2^32 (and wrap back inside the image) are
+    rejected, or AUTO moves to an algorithm whose offsets fit."""
+    F, S, A = B.WINO_ALGO_FUSED, B.WINO_ALGO_SPLIT, B.WINO_ALGO_AUTO
+    # fused, m = 4 (16 channels a step): 2^30 + (1 + 3) * 16 * H*W*4 < 2^32  <=>  H*W < 3 * 2^22
+    assert B.wino_workspace_bytes(1, 16, 3071, 4096, 16, 1, 4, F) == 0
+    assert B.wino_workspace_bytes(1, 16, 3072, 4096, 16, 1, 4, F) == 2**64 - 1
+    # fused, m = 2 (32 channels a step): H*W < 3 * 2^21
+    assert B.wino_workspace_bytes(1, 16, 2047, 3072, 16, 1, 2, F) == 0
+    assert B.wino_workspace_bytes(1, 16, 2048, 3072, 16, 1, 2, F) == 2**64 - 1
+    # split (16 channels per input-transform workgroup): 2^30 + 16 * H*W*4 < 2^32
+    assert B.wino_workspace_bytes(1, 5, 6143, 8192, 16, 1, 4, S) > 0
+    assert B.wino_workspace_bytes(1, 5, 6144, 8192, 16, 1, 4, S) == 2**64 - 1
+    assert B.wino_plan_r(1, 3, 9220, 9220, 64, 1, 4, 3, S)[0] == B.WINO_ERR_UNSUPPORTED
+    # N=1, C=5, 6400 x 6400, m = 2: the fused kernel's offsets would wrap; AUTO
+    # takes split, whose offsets fit, and needs its workspace (no fused fallback)
+    assert B.wino_plan_r(1, 5, 6400, 6400, 64, 1, 2, 3, F)[0] == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_plan_r(1, 5, 6400, 6400, 64, 1, 2, 3, A) == (B.WINO_OK, S, 1)
+    y = FAKE + (1 << 34)
+    assert B.wino_conv2d(FAKE, FAKE + (1 << 33), y, 1, 5, 6400, 6400, 64, 1, 2, A, None, 0) == \
+        B.WINO_ERR_WORKSPACE
+    # 5x5 layers have no split path: AUTO takes the three stages where their
+    # offsets fit (two images per block: 2 * 5 * 4000^2 * 4 < 2^30), else rejects
+    assert B.wino_plan_r(1, 5, 4000, 4000, 64, 2, 2, 5, F)[0] == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_plan_r(1, 5, 4000, 4000, 64, 2, 2, 5, A) == (B.WINO_OK, B.WINO_ALGO_STAGED, 1)
+    assert B.wino_plan_r(1, 5, 6400, 6400, 64, 2, 2, 5, A)[0] == B.WINO_ERR_UNSUPPORTED
