@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the Winograd hot path on one MI355X.
 
-One step = one pass of the whole path over one batch: the weight transform and
-the convolution (input transform -> T GEMMs -> output transform) of every 3x3
-layer in the workload (plus the 2x2 pools of a stack).  Prints one JSON line.
+One step = one pass of the per-inference path over one batch: the
+convolution (input transform -> T GEMMs -> output transform) of every layer in
+the workload, plus the 2x2 pools of a stack.  The weight transform is done once
+per weight set (offline in the method); it runs before the timed region and
+is timed and reported on its own, and also as part of a second, full-step
+figure.  Prints one JSON line.
 
 Metric: effective GFLOP/s = direct-convolution FLOPs (2*N*K*C*9*Ho*Wo per layer)
 divided by the step time, with eager launches (``--graph`` replays a HIP graph
 of 10 steps instead; the eager and the other figure are both reported).  Also
 reported:
 
-* ``roofline``: the dominant kernel's algorithmic bytes (or FLOPs) per launch
-  over its average launch duration, timed with HIP events around a graph of
-  back-to-back launches of that kernel on its own stream; ``traffic`` is the HBM
+* ``roofline``: the dominant launch's algorithmic bytes (or FLOPs) over its
+  duration: primarily the cold median (after evicting L2 and the last-level
+  cache), also the warm one from HIP events around a graph of back-to-back
+  launches on its own stream; ``traffic`` is the HBM
   bytes per launch that rocprofv3's FETCH_SIZE / WRITE_SIZE counters measured
   for it (scaled by what they read for a plain device copy of known size), read
   from the committed counter summary under profiles/ -- or null when that
@@ -314,6 +318,47 @@ def pmc_summary(args):
     print(text, end="")
 
 
+def trace_summary(args):
+    """Turn a rocprofv3 --kernel-trace --stats csv run of this script into the
+    committed kernel-trace summary (per-kernel calls and durations)."""
+    import re
+    from paper_1903_01521_amd import workloads as wl
+    name = args.workload or wl.DEFAULT_BENCH
+    files = glob.glob(os.path.join(args.trace_summary, "**", "*kernel_stats.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one kernel_stats.csv under {args.trace_summary}, found {len(files)}")
+    rows = list(csv.DictReader(open(files[0])))
+
+    def short(n):
+        n = re.sub(r"^void ", "", n)
+        n = re.sub(r"\(.*$", "", n) if n.startswith("wino::") else n
+        return n[:60] + ("..." if len(n) > 60 else "")
+    fl = f" --flags {args.flags:#x}" if args.flags is not None else ""
+    extra = f" {args.trace_args}" if args.trace_args else ""
+    tag = f"_{args.tag}" if args.tag else ""
+    lines = [f"# rocprofv3 kernel-trace summary: workload {name}{fl}",
+             "# one MI355X; commands (on the GPU host; <repo> is the repository root):",
+             "#   cd /tmp && export TMPDIR=/tmp",
+             f"#   rocprofv3 --kernel-trace --stats --output-format csv -d <out>/prof -o run -- "
+             f"python3 <repo>/bench.py --workload {name}{fl}{extra}",
+             f"#   python3 <repo>/bench.py --workload {name}{fl} --trace-summary <out>/prof"
+             + (f" --trace-args '{args.trace_args}'" if args.trace_args else "")
+             + (f" --tag {args.tag}" if args.tag else ""),
+             "# durations in ns; the calls include the warm-up, the timed steps and the",
+             "# per-launch (warm, in-sequence and cold) timing runs of bench.py.",
+             f"sources_sha256: {sources_hash()}",
+             "",
+             f"{'kernel':<64}{'calls':>7}{'avg_ns':>13}{'stddev':>11}{'min_ns':>9}{'max_ns':>9}"]
+    for r in rows:
+        lines.append(f"{short(r['Name']):<64}{int(r['Calls']):>7}{float(r['AverageNs']):>13.1f}"
+                     f"{float(r['StdDev']):>11.1f}{int(r['MinNs']):>9}{int(r['MaxNs']):>9}")
+    text = "\n".join(lines) + "\n"
+    if args.write_summary:
+        with open(os.path.join(PROFILES, f"kernel_trace_{name}{tag}.txt"), "w") as fh:
+            fh.write(text)
+    print(text, end="")
+
+
 def sleep_calibration(stream) -> float:
     """GPU cycles per millisecond of torch's spin kernel (torch.cuda._sleep)."""
     import torch
@@ -350,6 +395,10 @@ def main():
                     help="summarise two rocprofv3 --pmc csv runs (no GPU needed)")
     ap.add_argument("--mfma-summary", metavar="DIR",
                     help="summarise a rocprofv3 --pmc run with the MFMA counters (matrix-core utilisation)")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="summarise a rocprofv3 --kernel-trace --stats csv run (no GPU needed)")
+    ap.add_argument("--trace-args", default="", help="with --trace-summary: the profiled run's other arguments")
+    ap.add_argument("--tag", default="", help="with --trace-summary: suffix of the summary's file name")
     ap.add_argument("--kind", default="fused", help="kernel kind the --pmc-summary covers")
     ap.add_argument("--write-summary", action="store_true",
                     help="with --pmc-summary: also write it to profiles/traffic_<workload>.txt")
@@ -360,6 +409,9 @@ def main():
         return
     if args.mfma_summary:
         mfma_summary(args)
+        return
+    if args.trace_summary:
+        trace_summary(args)
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -413,6 +465,9 @@ def main():
             wsb = B.wino_workspace_bytes_1d(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, AXIS[L.axis], flags)
         else:
             wsb = B.wino_workspace_bytes_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags)
+        if wsb == 2**64 - 1:
+            raise SystemExit(f"{name} layer {len(wss)} ({L.C}->{L.K} at {L.H}x{L.W}, m={L.m}, r={L.r}): "
+                             f"the library rejects flags {flags:#x} for it (workspace size query failed)")
         wss.append((torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev), wsb))
         if staged and not L.axis and not L.nhwc:
             Vs.append(torch.empty(B.wino_input_tf_bytes_r(N, L.C, L.H, L.W, L.pad, L.m, L.r) // 4,
@@ -493,7 +548,11 @@ def main():
             if st != 0:
                 raise RuntimeError(f"{label}: {B.wino_status_string(st)}")
 
-    step_fns = [(label, fn) for label, _, _, fn in step]
+    # The timed step: every launch but the weight transforms, which run once
+    # before it (and in a second, full-step timing below).
+    step_fns = [(label, fn) for label, _, kind, fn in step if kind != "filter"]
+    filter_fns = [(label, fn) for label, _, kind, fn in step if kind == "filter"]
+    full_fns = [(label, fn) for label, _, _, fn in step]
 
     def capture(fns, reps=1):
         g = torch.cuda.CUDAGraph()
@@ -516,6 +575,7 @@ def main():
         raise SystemExit(f"--graph needs --steps to be a multiple of {GS}")
     graph = capture(step_fns, reps=GS) if use_graph else None
 
+    run(filter_fns)                      # U of every layer, once per weight set
     for _ in range(args.warmup):
         run(step_fns)
     torch.cuda.synchronize()
@@ -535,6 +595,17 @@ def main():
     torch.cuda.synchronize()
     wall1 = time.perf_counter()
     ms_step = e0.elapsed_time(e1) / args.steps
+
+    # The full step with the weight transforms, eager, for reference (outside
+    # the timed region above).
+    full_steps = max(1, min(args.steps, 200))
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(full_steps):
+        run(full_fns)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    full_ms = e0.elapsed_time(e1) / full_steps
 
     # The other launch mode of the same step, for reference (outside the timed region).
     ref_steps = 20 * GS
@@ -654,11 +725,18 @@ def main():
     total_by = {}
     for (label, li, kind, _), t in zip(step, per_launch):
         total_by[kind] = total_by.get(kind, 0.0) + t
-    dom = int(np.argmax(per_launch))
+    # the dominant launch of the timed step (weight transforms excluded)
+    dom = max((i for i, (_, _, k, _) in enumerate(step) if k != "filter"), key=lambda i: per_launch[i])
     dlabel, dlayer, dkind, _ = step[dom]
-    roof = roofline(dkind, nums[dlayer], per_launch[dom] / 1e3)
+    cold_med = [float(np.median(c)) for c in cold]
+    # primary: the cold median (inputs from HBM, not from a cache a repeated
+    # launch warmed); the warm back-to-back figure beside it
+    roof = roofline(dkind, nums[dlayer], cold_med[dom] / 1e3)
     roof["kernel"] = f"{dlabel} ({kernel_label(dkind)})"
-    roof["avg_us"] = round(per_launch[dom] * 1e3, 3)
+    roof["avg_us"] = round(cold_med[dom] * 1e3, 3)
+    roof["timing"] = "cold median (L2 and last-level cache evicted before each launch)"
+    roof["avg_us_warm"] = round(per_launch[dom] * 1e3, 3)
+    roof["frac_warm"] = roofline(dkind, nums[dlayer], per_launch[dom] / 1e3)["frac"]
     traffic, src = read_traffic(name, dkind) if len(w.layers) == 1 else (None, "multi-layer workload")
     roof["traffic"] = traffic
     roof["traffic_source"] = os.path.relpath(src, HERE) if traffic is not None else src
@@ -695,6 +773,7 @@ def main():
 
     direct = sum(f["direct_flops"] for f in nums)
     value = direct / (ms_step / 1e3) / 1e9
+    filter_us = [t * 1e3 for (_, _, k, _), t in zip(step, per_launch) if k == "filter"]
 
     result = {
         "metric": "effective GFLOP/s (direct-conv FLOPs) per 3x3 layer + % of HBM/MFMA roofline",
@@ -731,8 +810,13 @@ def main():
         # every launch against the roof that bounds it (algorithmic work / duration)
         "per_launch_roofline": {lbl: (lambda r: f"{r['bound']} {r['frac']:.3f}")(
             roofline(kind, nums[li], t / 1e3)) for (lbl, li, kind, _), t in zip(step, per_launch)},
-        "conv_only_gflops": round(direct / (sum(t for (_, _, k, _), t in zip(step, per_launch)
-                                                 if k != "filter") / 1e3) / 1e9, 1),
+        "per_launch_roofline_cold": {lbl: (lambda r: f"{r['bound']} {r['frac']:.3f}")(
+            roofline(kind, nums[li], t / 1e3)) for (lbl, li, kind, _), t in zip(step, cold_med)},
+        # the weight transform (offline in the method): per-launch durations,
+        # and the step with it included (eager, outside the timed region)
+        "filter_transform_us": round(sum(filter_us), 3),
+        "ms_per_step_with_filter_transform": round(full_ms, 6),
+        "value_with_filter_transform": round(direct / (full_ms / 1e3) / 1e9, 1),
         "eager_ms_per_step": round(eager_ms, 6),
         "graph_ms_per_step": round(graph_ms, 6) if graph_ms is not None else None,
         "wall_ms_per_step": round((wall1 - wall0) * 1e3 / args.steps, 6),

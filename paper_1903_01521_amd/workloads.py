@@ -92,8 +92,9 @@ WORKLOADS = {w.name: w for w in [
              note="7x1 layer shaped like Inception-v3's 17x17 blocks, F(2x1,7x1,8x1)"),
 ]}
 
-# The single-layer workload the benchmark times by default.
-DEFAULT_BENCH = "f4_n1_c64_k64_112x112"
+# The single-layer workload the benchmark times by default: the largest
+# single-GPU layer (N=64, C=K=256, 56x56, F(4x4,3x3)).
+DEFAULT_BENCH = "f4_n64_c256_k256_56x56"
 
 
 def generate(w: Workload, seed: int = 0, N: int | None = None):

@@ -95,3 +95,17 @@ def test_mfma_summary_from_counter_rows(tmp_path, capsys):
     assert float(out["busy_cycles_per_inst"]) == pytest.approx(32.0)
     assert float(out["util_active"]) == pytest.approx(0.25, abs=1e-3)
     assert out["probe_util_active"].startswith("0.850")
+
+
+def test_default_workload_is_the_large_layer():
+    # N=64, C=K=256, 56x56, pad 1, F(4x4,3x3): 14 x 14 tiles per image
+    assert wl.DEFAULT_BENCH == "f4_n64_c256_k256_56x56"
+    w = wl.WORKLOADS[wl.DEFAULT_BENCH]
+    f = bench.layer_numbers(w.N, w.first)
+    assert (f["P"], f["T"]) == (64 * 14 * 14, 36)
+    assert f["direct_flops"] == 2 * 64 * 256 * 256 * 9 * 56 * 56          # 236.76 GFLOP
+    assert f["gemm_flops"] * 4 == f["direct_flops"]
+    # the split call: x read, U read, y written
+    assert f["bytes"]["split"] == 4 * (64 * 256 * 56 * 56 * 2 + 36 * 256 * 256)
+    r = bench.roofline("split", f, 1e-3)
+    assert r["bound"] == "mfma" and r["achieved"] == pytest.approx(f["gemm_flops"] / 1e-3 / 1e12, rel=1e-3)

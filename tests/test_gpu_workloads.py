@@ -78,14 +78,21 @@ def test_single_layer_whole(name):
     assert err <= TOL[L.m]
 
 
-@pytest.mark.parametrize("name", ["f4_n64_c256_k256_56x56", "f4_lowc_n64_c3_k64_224x224"])
-def test_large_batch_sampled(name):
+@pytest.mark.parametrize("name,algo", [("f4_n64_c256_k256_56x56", B.WINO_ALGO_AUTO),
+                                       ("f4_n64_c256_k256_56x56", B.WINO_ALGO_STAGED),
+                                       ("f4_n64_c256_k256_56x56", B.WINO_ALGO_FUSED),
+                                       ("f4_lowc_n64_c3_k64_224x224", B.WINO_ALGO_AUTO)])
+def test_large_batch_sampled(name, algo):
+    """The whole batch on the GPU (AUTO: the split path for the 256-channel
+    layer, low-C for the first layer; the staged and fused paths too), checked
+    on sampled images."""
     w = wl.WORKLOADS[name]
     L = w.first
     x, (g,) = wl.generate(w)
     sample = [0, w.N // 2, w.N - 1]
-    print(f"{name} sample {sample}", flush=True)
-    y = h.host(_layer(h.dev(x), g, L))[sample]
+    print(f"{name} algo {algo:#x} sample {sample}", flush=True)
+    U = h.filter_transform(g, L.m)
+    y = h.host(h.conv2d(h.dev(x), U, L.K, L.pad, L.m, algo | (B.WINO_FLAG_RELU if L.relu else 0)))[sample]
     ref = direct.conv2d(x[sample], g, L.pad)
     err = h.normwise_err(y, ref)
     print(f"  normwise err {err:.2e}", flush=True)
