@@ -290,6 +290,30 @@ int wino_conv2d_nhwc(const float* x, const float* U, float* y,
                      int N, int C, int H, int W, int K, int pad, int m,
                      unsigned flags, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- allocation-free variant ------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the layer of
+ * wino_conv2d with the same arguments and flags, its workspace taken from a
+ * static device array of WINO_NOALLOC_SCRATCH_BYTES bytes that the library
+ * holds on every GPU it runs on until the process ends (no hipMalloc, hipFree
+ * or other allocation; the caller passes x, U and y as before).
+ *   - WINO_ALGO_AUTO plans as wino_conv2d does with a workspace of that size:
+ *     the split algorithm, channel slices or the staged one where their
+ *     workspace fits, else the fused kernel (WINO_ERR_WORKSPACE only when no
+ *     algorithm that fits is left, see the size limits above).
+ *   - An explicit algorithm or WINO_CSLICES(n) whose workspace
+ *     (wino_workspace_bytes with the same flags) exceeds the array returns
+ *     WINO_ERR_WORKSPACE before any HIP call.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (every algorithm writes all the workspace it reads):
+ *     calls that overlap in time on one GPU, from any stream or thread, race
+ *     and must be serialised by the caller.
+ * Errors: as for wino_conv2d. */
+#define WINO_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int wino_conv2d_noalloc(const float* x, const float* U, float* y,
+                        int N, int C, int H, int W, int K, int pad, int m,
+                        unsigned flags, void* stream);
+
 /* Glue between the blocks of a VGG-style stack (not part of the method):
  * 2x2 window, stride 2 max-pool, y: [N][C][H/2][W/2] (floor). */
 int wino_maxpool2x2(const float* x, float* y, int N, int C, int H, int W, void* stream);

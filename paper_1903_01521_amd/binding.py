@@ -87,7 +87,10 @@ _SIGS = {
     "wino_filter_bytes_p": ([_c_int] * 3 + [_c_uint], _c_size),
     "wino_filter_transform_p": ([_vp, _vp] + [_c_int] * 3 + [_c_uint, _vp], _c_int),
     "wino_conv2d_nhwc": ([_vp, _vp, _vp] + [_c_int] * 7 + [_c_uint, _vp, _c_size, _vp], _c_int),
+    "wino_conv2d_noalloc": ([_vp, _vp, _vp] + [_c_int] * 7 + [_c_uint, _vp], _c_int),
 }
+
+WINO_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def lib() -> ctypes.CDLL:
@@ -177,6 +180,11 @@ def wino_conv2d(x, U, y, N, C, H, W, K, pad, m, flags=0, workspace=None, workspa
                 stream=None) -> int:
     return lib().wino_conv2d(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, flags,
                              _ptr(workspace), workspace_bytes, _stream(stream))
+
+
+def wino_conv2d_noalloc(x, U, y, N, C, H, W, K, pad, m, flags=0, stream=None) -> int:
+    return lib().wino_conv2d_noalloc(_fptr(x), _fptr(U), _fptr(y), N, C, H, W, K, pad, m, flags,
+                                     _stream(stream))
 
 
 def wino_input_transform(x, V, N, C, H, W, pad, m, stream=None) -> int:

@@ -494,6 +494,33 @@ int wino_conv2d(const float* x, const float* U, float* y, int N, int C, int H, i
     return wino_conv2d_r(x, U, y, N, C, H, W, K, pad, m, 3, flags, workspace, workspace_bytes, stream);
 }
 
+int wino_conv2d_noalloc(const float* x, const float* U, float* y, int N, int C, int H, int W, int K, int pad,
+                        int m, unsigned flags, void* stream) {
+    if (!x || !U || !y) return WINO_ERR_INVALID_ARG;
+    Geom g;
+    int st = make_geom(N, C, H, W, K, pad, m, &g);
+    if (st != WINO_OK) return st;
+    Plan p;
+    st = make_plan(g, flags, &p);
+    if (st != WINO_OK) return st;
+    const size_t need = wino_workspace_bytes(N, C, H, W, K, pad, m, flags);
+    if (need == (size_t)-1) return WINO_ERR_UNSUPPORTED;
+    // AUTO falls back to a plan whose workspace fits (wino_conv2d_r decides,
+    // given the array's size); explicit choices must fit as asked.
+    if (need > kNoAllocScratchBytes && !p.automatic) return WINO_ERR_WORKSPACE;
+    // the aliasing checks of wino_conv2d, before the scratch lookup (a HIP call)
+    const size_t xb = (size_t)N * C * H * W * sizeof(float);
+    const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
+    const size_t ub = prec_of(flags) ? wino_filter_bytes_p(C, K, m, flags & WINO_PREC_MASK) : wino_filter_bytes(C, K, m);
+    if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
+    void* ws = nullptr;
+    if (need > 0) {
+        st = hip_status(noalloc_scratch(&ws));
+        if (st != WINO_OK) return st;
+    }
+    return wino_conv2d_r(x, U, y, N, C, H, W, K, pad, m, 3, flags, ws, ws ? kNoAllocScratchBytes : 0, stream);
+}
+
 int wino_input_transform_r(const float* x, float* V, int N, int C, int H, int W, int pad, int m, int r,
                            void* stream) {
     if (!x || !V) return WINO_ERR_INVALID_ARG;

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "wino.h"
+
 namespace wino {
 
 // The NCHW input kernels address x through 32-bit buffer offsets, and any
@@ -91,6 +93,11 @@ constexpr int kProbeWaves = 2048;
 // integer below 2^24, so the check is exact.
 constexpr int kProbeMaxIters = 1 << 21;
 hipError_t launch_mfma_probe(int iters, float* out, hipStream_t s);
+// Scratch of wino_conv2d_noalloc: a static device array of this many bytes
+// per GPU; *out = its address on the current device (looked up once per
+// device and kept).
+constexpr size_t kNoAllocScratchBytes = WINO_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch(void** out);
 // 1-D layers (1 x r or r x 1 filters, F(1xm, 1xr, 1x8)): filter transform; the
 // input and output transforms dispatch on g.axis inside launch_input_transform
 // and launch_output_transform.

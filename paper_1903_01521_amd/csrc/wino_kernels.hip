@@ -22,6 +22,7 @@
 // tile l%16 for output channels 4*(l/16) .. 4*(l/16)+3 -- everything the output
 // transform of those four (tile, channel) pairs needs, in its own registers.
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "wino_internal.h"
@@ -2354,6 +2355,35 @@ __global__ __launch_bounds__(256) void k_mfma_probe(int iters, float* __restrict
 hipError_t launch_mfma_probe(int iters, float* out, hipStream_t s) {
     hipLaunchKernelGGL(k_mfma_probe, dim3(kProbeWaves / 4), dim3(256), 0, s, iters, out);
     return hipGetLastError();
+}
+
+// ---- scratch of the allocation-free entry point ---------------------------
+// One array per GPU the library runs on, resident until the process ends.  In
+// host code `scratch` names a host-side stand-in, not device memory: its
+// device address comes from hipGetSymbolAddress, once per device with that
+// device current, and only that address is ever passed on.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+hipError_t noalloc_scratch(void** out) {
+    *out = nullptr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    static std::mutex mu;
+    static void* addr[kMaxDevices];
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 size_t filter_elems(int C, int K, int m, int r) {

@@ -310,3 +310,25 @@ def test_input_offsets_stay_below_2_32():
     assert B.wino_plan_r(1, 5, 4000, 4000, 64, 2, 2, 5, F)[0] == B.WINO_ERR_UNSUPPORTED
     assert B.wino_plan_r(1, 5, 4000, 4000, 64, 2, 2, 5, A) == (B.WINO_OK, B.WINO_ALGO_STAGED, 1)
     assert B.wino_plan_r(1, 5, 6400, 6400, 64, 2, 2, 5, A)[0] == B.WINO_ERR_UNSUPPORTED
+
+
+def test_noalloc_entry_point_rejects():
+    """The allocation-free variant validates like wino_conv2d and rejects
+    explicit plans whose workspace exceeds its static scratch, before any HIP
+    call (CPU only)."""
+    y = FAKE + (1 << 33)
+    cap = B.WINO_NOALLOC_SCRATCH_BYTES
+    assert "WINO_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)" in open(B.HEADER).read()
+    # N=64, C=K=256, 56x56, m=4: V and M of the staged path, or the split path's
+    # tile-blocked V, are far past the scratch
+    for algo in (B.WINO_ALGO_STAGED, B.WINO_ALGO_SPLIT):
+        assert B.wino_workspace_bytes(64, 256, 56, 56, 256, 1, 4, algo) > cap
+        assert B.wino_conv2d_noalloc(FAKE, FAKE + (1 << 32), y, 64, 256, 56, 56, 256, 1, 4, algo) == \
+            B.WINO_ERR_WORKSPACE
+    # invalid arguments as for wino_conv2d
+    assert B.wino_conv2d_noalloc(None, FAKE, y, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_conv2d_noalloc(FAKE, FAKE + 0x1000, y, 0, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
+    assert B.wino_conv2d_noalloc(FAKE, FAKE + 0x1000, y, 1, 4, 8, 8, 4, 1, 3) == B.WINO_ERR_UNSUPPORTED
+    assert B.wino_conv2d_noalloc(FAKE, FAKE + 0x1000, y, 1, 4, 8, 8, 4, 1, 4, 0x500) == B.WINO_ERR_UNSUPPORTED
+    # x aliasing y
+    assert B.wino_conv2d_noalloc(FAKE, FAKE + (1 << 32), FAKE, 1, 4, 8, 8, 4, 1, 4) == B.WINO_ERR_INVALID_ARG
