@@ -128,10 +128,7 @@ double block_util(const Geom& g, int bw) {
     return (double)g.th * g.tw / (rows * cols);
 }
 
-long split_items(const Geom& g, int bw) {
-    const int kgw = g.m == 4 ? 4 : 8;
-    return (split_blocks(g, bw) + 1) / 2 * ((g.KB + kgw - 1) / kgw);
-}
+long split_items(const Geom& g) { return split_tail(g).items; }
 
 // Estimated time (ns) of the fused and split algorithms: both kernels run one
 // workgroup per CU, so a launch takes ceil(items/256) rounds of one
@@ -149,16 +146,19 @@ double fused_ns(const Geom& g, FusedCfg c) {
     return rounds(fused_workgroups(g, c)) * work / (kFlopPerClk * eff) / kClkGHz;
 }
 
-double split_ns(const Geom& g, int bw) {
+double split_ns(const Geom& g) {
     const int kgw = g.m == 4 ? 4 : 8;
     const double cq4 = (g.CQ + 3) / 4 * 4;
-    const double work = 2.0 * 2 * 16 * kgw * 16 * (4.0 * cq4) * g.T;    // FLOP per workgroup
-    const double gemm = rounds(split_items(g, bw)) * work / (kFlopPerClk * 0.74) / kClkGHz;
-    const double bytes = 1.5 * 4.0 * g.N * g.C * g.H * g.W + 4.0 * (double)split_blocks(g, bw) * cq4 * g.T * 64;
+    const double work = 2.0 * 2 * 16 * kgw * 16 * (4.0 * cq4) * g.T;    // FLOP per item
+    // the tail's units run in one round of about a quarter of an item's time
+    const SplitTail t = split_tail(g);
+    const double item_rounds = rounds(t.items - t.tail) + (t.tail ? 0.25 : 0.0);
+    const double gemm = item_rounds * work / (kFlopPerClk * 0.74) / kClkGHz;
+    const double bytes = 1.5 * 4.0 * g.N * g.C * g.H * g.W + 4.0 * (double)split_blocks(g) * cq4 * g.T * 64;
     return gemm + bytes / kHbmBytesPerNs;
 }
 
-size_t split_workspace(const Geom& g, int bw) { return vblk_elems(g, bw) * sizeof(float); }
+size_t split_workspace(const Geom& g) { return vblk_elems(g) * sizeof(float); }
 
 // Partial outputs of the channel slices: [slices used][N][K][Ho][Wo].
 size_t slice_workspace(const Geom& g, int nsl) {
@@ -291,8 +291,7 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     }
     // Split path where the estimates favour it (layers with at least a full
     // round of its workgroups).
-    if (p->automatic && g.r == 3 && !cs_req && split_items(g, c.bw) >= (long)kCus &&
-        split_ns(g, c.bw) < fused_ns(g, c))
+    if (p->automatic && g.r == 3 && !cs_req && split_items(g) >= (long)kCus && split_ns(g) < fused_ns(g, c))
         p->algo = WINO_ALGO_SPLIT;
     // Channel slices over workgroups for fused layers that leave CUs idle with
     // a long channel loop each (deep layers at small batch): double the slices
@@ -379,7 +378,7 @@ size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m,
     if (prec_of(flags)) return round_up(vh_bytes(g), 256) + m_elems(g) * sizeof(float);
     if (p.algo == WINO_ALGO_FUSED && p.cfg.nsl > 1) return slice_workspace(g, p.cfg.nsl);
     if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
-    if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g, p.cfg.bw);
+    if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
 
@@ -449,7 +448,7 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
         return hip_status(launch_staged16(x, U, y, workspace, (float*)((char*)workspace + vb), g, prec, relu, s));
     }
     if (p.algo == WINO_ALGO_SPLIT) {
-        const size_t need = split_workspace(g, p.cfg.bw);
+        const size_t need = split_workspace(g);
         if (!workspace || workspace_bytes < need) {
             if (!p.automatic) return WINO_ERR_WORKSPACE;
             p.algo = WINO_ALGO_FUSED;          // no room for V: the fused kernel, where its offsets fit

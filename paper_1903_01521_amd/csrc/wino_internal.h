@@ -78,10 +78,21 @@ hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g,
 // Channel quads per slice, and the slices that hold any, for a requested count.
 int slice_quads(const Geom& g, int nsl);
 int slices_used(const Geom& g, int nsl);
-// Split path: input transform into a tile-blocked workspace, then the GEMMs
-// with the output transform in their epilogue.
-long split_blocks(const Geom& g, int bw);
-size_t vblk_elems(const Geom& g, int bw);
+// Split path: input transform into a workspace of 16-tile blocks, then the
+// GEMMs with the output transform in their epilogue.
+long split_blocks(const Geom& g);            // ceil(P / 16)
+size_t vblk_elems(const Geom& g);
+// Work items of the GEMM kernel: (pair of tile blocks, filter group).  When
+// the last round of items would leave most CUs idle (items % 256, at most
+// 256 / units of them), those items run as units of one tile block and one
+// filter block each.
+constexpr long kSplitCus = 256;
+struct SplitTail {
+    long items;     // (tile-block pair, filter group) items
+    long tail;      // of them, run as units
+    int units;      // units per item: 2 tile blocks x filter blocks per group
+};
+SplitTail split_tail(const Geom& g);
 hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
                         hipStream_t s);
 // Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.

@@ -1026,10 +1026,14 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
 // MFMAs and LDS reads only -- on gfx950 vector ALU work does not overlap the
 // MFMAs of its SIMD, so it costs its full time inside a GEMM loop.
 //
-// Tile-blocked V: Vb[tb][CQ4][T/4][64][4], tb = (n*nbh + bh)*nbw + bw a spatial
-// block of 16 tiles (BH x BW), CQ4 = CQ rounded up to a multiple of 4 (the
-// padding quads hold zeros); element (t, c, tile (bh*BH + bi, bw*BW + bj)) at
-// lane (c%4)*16 + bi*BW + bj, slot t%4 of group t/4.
+// Blocked V: Vb[tb][CQ4][T/4][64][4], tb = p / 16 a block of 16 consecutive
+// tiles (in the order n, ti, tj, so only the batch's last block has slots past
+// the last tile), CQ4 = CQ rounded up to a multiple of 4 (the padding quads
+// hold zeros); element (t, c, tile p) at lane (c%4)*16 + p%16, slot t%4 of
+// group t/4.  The input transform still works on rectangular patches of
+// 16 tiles (BH x BW, sharing the halo in LDS); each lane stores its tile to
+// that tile's block and slot, and a patch's columns or rows past the tile grid
+// store nothing.
 
 // Patch byte offsets of one image for load e = j*NT + tid of
 // [4*NQ channels][PR rows][NE loads] (kInvalid outside the image or past the
@@ -1075,9 +1079,11 @@ struct VblkShape {
     static constexpr int XSP = JX * 256 * EW;
 };
 
-// One workgroup per (tile block, 4 channel quads): the halo'd patch comes into
-// LDS by DMA, each wave transforms one quad for the block's 16 tiles and
-// stores its 9 (m = 4) or 4 (m = 2) 1 KiB groups.
+// One workgroup per (16-tile patch, 4 channel quads): the halo'd patch comes
+// into LDS by DMA, each wave transforms one quad for the patch's 16 tiles and
+// stores its 9 (m = 4) or 4 (m = 2) groups of 16 bytes per lane into the
+// blocks of those tiles.  The workgroup of the batch's last patch also writes
+// zeros to the last block's slots past the last tile.
 template <int MT, int BW, int VEC>
 __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
                                               int nbh, int nbw, int ncq4) {
@@ -1124,7 +1130,23 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
     }
     float v[T];
     input_tf<MT>(d, v);
-    store_t4<T, false>(Vb + ((size_t)tb * (ncq4 * 4) + cq) * T * 64, lane, v);
+    // this lane's tile, and its block and slot in Vb
+    const int ti = ti0 + bi, tj = tj0 + bj;
+    const size_t qstride = (size_t)ncq4 * 4 * T * 64;              // floats of one block
+    const int hi = lane & 0x30;                                     // (c % 4) * 16
+    if (ti < g.th && tj < g.tw) {
+        const int p = (n * g.th + ti) * g.tw + tj;
+        float* dst = Vb + (size_t)(p >> 4) * qstride + (size_t)cq * T * 64 + (hi | (p & 15)) * 4;
+#pragma unroll
+        for (int g4 = 0; g4 < T / 4; ++g4)
+            store_out<false>(dst + g4 * 256, v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
+    }
+    const int tail = g.P & 15;
+    if (tail && tb == g.N * nbh * nbw - 1 && l16 >= tail) {
+        float* dst = Vb + (size_t)(g.P >> 4) * qstride + (size_t)cq * T * 64 + (hi | l16) * 4;
+#pragma unroll
+        for (int g4 = 0; g4 < T / 4; ++g4) store_out<false>(dst + g4 * 256, 0.f, 0.f, 0.f, 0.f);
+    }
 }
 
 // GEMMs + output transform from Vb.  A workgroup of 8 waves computes two tile
@@ -1184,7 +1206,7 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
         for (int i = 0; i < NG; ++i) ug[i] = u_load(ur, ulane, go + i * 1024u);
     };
     // quad q of the stage: 2 blocks x TH MFMAs, V read group by group; after
-    // group gi, between(gi) (the next step's V DMA is spread over quad 0)
+    // group gi, between(gi) (the reload of that group's filter registers)
     auto quad = [&](const float* vs, int q, const f32x4 (&ug)[NG], auto&& between) {
 #pragma unroll
         for (int gi = 0; gi < NG; ++gi) {
@@ -1202,17 +1224,22 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
             between(gi);
         }
     };
-    f32x4 ua[NG], ub[NG];
-    // Loads of quad q of step s, in order: the filters of the next quad, then
-    // (q < 3) part q of the next step's V DMA, JP loads -- spread so that no
-    // wave stalls behind the whole burst.  Waiting for a quad's filters only
-    // forces DMA parts issued two quads earlier; at the start of step s+1 all of
-    // its V must have landed: the NG filter loads of quad 3 came after it.
-    constexpr int WAITN = NG;
+    f32x4 ubuf[2][NG];                           // filter register sets of even and odd quads
     constexpr int JV = S::JV, JP = (JV + 2) / 3;
+    // Filters come two quads ahead: after the MFMAs of position group gi of
+    // quad q, group gi of quad q+2 is loaded into the registers they used (one
+    // quad ahead, the loads that miss L2 -- the whole U does not fit one XCD's
+    // L2 -- stalled the MFMAs: 680 against 649 us on the N=64 256-channel
+    // layer).  Part q < 3 of the next step's V DMA (JP loads, spread so that
+    // no wave stalls behind the whole burst) is issued at the start of quad q,
+    // so at the start of step s+1 the 2*NG filter loads of quads 2 and 3 came
+    // after the last part: all of its V has landed when at most those remain.
+    constexpr int WAITN = 2 * NG;
     issue_v(IC<0>{}, 0, IC<0>{}, IC<JV>{});
-    load_u(0, ua);
-    wait_vm_lds<NG>();                // V of step 0 has landed (for this wave)
+    load_u(0, ubuf[0]);
+    load_u(1, ubuf[1]);
+    wait_vm_lds<WAITN>();             // V of step 0 has landed (for this wave)
+    const uint32_t uq = (uint32_t)(kb * g.CQ) * (T / 4) + G0;
     auto step = [&](auto rc, int s) {  // s % 2 == R
         constexpr int R = decltype(rc)::value;
         wait_vm_lds<WAITN>();          // V of step s has landed (this wave)
@@ -1220,9 +1247,7 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
         const float* vs = stage(IC<R>{});
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            f32x4 (&cur)[NG] = (q & 1) ? ub : ua;
-            f32x4 (&nxt)[NG] = (q & 1) ? ua : ub;
-            load_u(s * NQ + q + 1, nxt);
+            f32x4 (&cur)[NG] = ubuf[q & 1];
             auto part = [&](auto pc) {
                 constexpr int P = decltype(pc)::value;
                 constexpr int A0 = P * JP < JV ? P * JP : JV, A1 = (P + 1) * JP < JV ? (P + 1) * JP : JV;
@@ -1232,7 +1257,9 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
             part(IC<1>{});
             part(IC<2>{});
             __builtin_amdgcn_sched_barrier(0);
-            quad(vs, q, cur, [](int) {});
+            const uint32_t go2 = __builtin_amdgcn_readfirstlane(
+                (uint32_t)((uq + (uint32_t)min(s * NQ + q + 2, g.CQ - 1) * (T / 4)) * 1024u));
+            quad(vs, q, cur, [&](int gi) { cur[gi] = u_load(ur, ulane, go2 + (uint32_t)gi * 1024u); });
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -1245,29 +1272,163 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
     __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
 }
 
+// The tile of lane l16 in block tb (16 consecutive tiles).
+__device__ __forceinline__ TileCoord block_tile(int tb, int l16, const Geom& g) {
+    return decode_tile(tb * 16 + l16, g);
+}
+
+// A GEMM + output-transform unit of a tail item: one tile block tb and one
+// filter block kb over all channels.  The 8 waves are (row group h of TS) x
+// (channel part cp of 8/TS); each multiplies its quads for its row group's
+// positions, with U and V straight from memory to registers (no operand is
+// shared between waves), one quad ahead.  Each wave then applies its row
+// group's part of A^T M A to its accumulators, and the 8 partial outputs are
+// summed through LDS in wave order: wave w adds and stores 1/8 of the values.
+template <int MT, int H>
+__device__ __forceinline__ void unit_steps(const __amdgpu_buffer_rsrc_t vr, const __amdgpu_buffer_rsrc_t ur,
+                                           const Geom& g, int kb, int q0, int q1, int lane,
+                                           f32x4 (&acc)[GoShape<MT>::TH]) {
+    using S = GoShape<MT>;
+    constexpr int A = S::A, X0 = H * S::RN, TH = S::TH, T = S::T;
+    constexpr int G0 = X0 * A / 4, NG = (X0 * A + TH - 1) / 4 - G0 + 1;
+    const uint32_t l16b = (uint32_t)lane * 16u;
+    auto load = [&](int q, f32x4 (&ug)[NG], f32x4 (&vg)[NG]) {
+        const int c = min(q, g.CQ - 1);    // quads past CQ: zero V, any filters
+        const uint32_t go = __builtin_amdgcn_readfirstlane((uint32_t)(((kb * g.CQ + c) * (T / 4) + G0) * 1024));
+        const uint32_t vo = __builtin_amdgcn_readfirstlane((uint32_t)((q * (T / 4) + G0) * 1024));
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+            ug[i] = u_load(ur, l16b, go + i * 1024u);
+            vg[i] = u_load(vr, l16b, vo + i * 1024u);
+        }
+    };
+    auto mma = [&](const f32x4 (&ug)[NG], const f32x4 (&vg)[NG]) {
+#pragma unroll
+        for (int t = 0; t < TH; ++t) {
+            const int idx = X0 * A + t;
+            acc[t] = mfma16x16x4(ug[idx / 4 - G0][idx % 4], vg[idx / 4 - G0][idx % 4], acc[t]);
+        }
+    };
+    f32x4 ua[NG], va[NG], ub[NG], vb[NG];
+    if (q0 < q1) load(q0, ua, va);
+    for (int q = q0; q < q1; q += 2) {
+        if (q + 1 < q1) load(q + 1, ub, vb);
+        mma(ua, va);
+        if (q + 2 < q1) load(q + 2, ua, va);
+        if (q + 1 < q1) mma(ub, vb);
+    }
+}
+
+template <int MT>
+__device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, const float* __restrict__ U,
+                                              float* __restrict__ y, const Geom& g, int tb, int kb, int ncq4,
+                                              bool relu, bool vec_ok, float4* vs0, float4* vs1, int wave,
+                                              int lane) {
+    using S = GoShape<MT>;
+    constexpr int TS = S::TS, TH = S::TH, T = S::T, CP = 8 / TS, NV = S::NV, VPW = NV / 8;
+    static_assert(4 * NV * 64 <= S::VST, "four partial-output slots per LDS stage");
+    static_assert(VPW % MT == 0, "whole output rows per wave");
+    const int h = wave % TS, cp = wave / TS;
+    const int nq = ncq4 * 4;
+    const int qpp = (nq + CP - 1) / CP;
+    const int q0 = min(cp * qpp, nq), q1 = min(nq, q0 + qpp);
+    const size_t blk_b = (size_t)nq * T * 256;
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)((const char*)Vb + (size_t)tb * blk_b), (short)0, (int)(blk_b < kInvalid ? blk_b : kInvalid),
+        kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
+    f32x4 acc[TH];
+#pragma unroll
+    for (int t = 0; t < TH; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float o[4][MT][MT];
+    if constexpr (TS == 1) {
+        unit_steps<MT, 0>(vr, ur, g, kb, q0, q1, lane, acc);
+        fused_share<MT, 1, 1, 16, 0, 0>(acc, o);
+    } else {
+        if (h == 0) {
+            unit_steps<MT, 0>(vr, ur, g, kb, q0, q1, lane, acc);
+            fused_share<MT, 2, 1, 16, 0, 0>(acc, o);
+        } else {
+            unit_steps<MT, 1>(vr, ur, g, kb, q0, q1, lane, acc);
+            fused_share<MT, 2, 1, 16, 0, 1>(acc, o);
+        }
+    }
+    // Slot w of NV*64 floats: w < 4 in vs0, else vs1 (each branch names its
+    // array, so the accesses stay LDS accesses).
+    auto with_slot = [&](int w, auto&& f) {
+        if (w < 4) f((float*)vs0 + (size_t)w * NV * 64 + lane);
+        else f((float*)vs1 + (size_t)(w - 4) * NV * 64 + lane);
+    };
+    with_slot(wave, [&](float* slot) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int j = 0; j < MT; ++j) slot[((r * MT + i) * MT + j) * 64] = o[r][i][j];
+    });
+    __syncthreads();
+    float sum[VPW];
+#pragma unroll
+    for (int e = 0; e < VPW; ++e) sum[e] = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        with_slot(w, [&](float* slot) {
+#pragma unroll
+            for (int e = 0; e < VPW; ++e) sum[e] += slot[(wave * VPW + e) * 64];
+        });
+    }
+    const int f0 = wave * VPW, r = f0 / (MT * MT), i0 = (f0 % (MT * MT)) / MT;
+    const TileCoord tc = block_tile(tb, lane & 15, g);
+    const int k = kb * 16 + 4 * (lane >> 4) + r;
+#pragma unroll
+    for (int ii = 0; ii < VPW / MT; ++ii) {
+        float row[MT];
+#pragma unroll
+        for (int j = 0; j < MT; ++j) row[j] = sum[ii * MT + j];
+        store_row<MT>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
+    }
+}
+
 template <int MT>
 __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, const float* __restrict__ U,
-                                                  float* __restrict__ y, Geom g, FusedTiling ft, int ntb,
-                                                  int relu, int vec_ok) {
+                                                  float* __restrict__ y, Geom g, FusedTiling ft, int nb,
+                                                  int relu, int vec_ok, int ntail) {
     using S = GoShape<MT>;
     constexpr int TS = S::TS, KGW = S::KGW, TH = S::TH, NV = S::NV;
     __shared__ float4 vs0[S::VST / 4], vs1[S::VST / 4];
 
-    // item = (tile-block pair, filter group), XCD-aware as in k_fused
+    // item = (tile-block pair, filter group), XCD-aware as in k_fused; the
+    // last ntail items run as 2*KGW units each after the others
     const int b = blockIdx.x;
-    const int item = (b & 7) * ft.per + (b >> 3);
-    if (item >= ft.nt * ft.nkg) return;
-    const int kgi = ft.kfast ? item % ft.nkg : item / ft.nt;
-    const int tp = ft.kfast ? item / ft.nkg : item - kgi * ft.nt;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nmain = ft.nt * ft.nkg - ntail;
+    auto decode = [&](int it, int& kgi, int& tp) {
+        kgi = ft.kfast ? it % ft.nkg : it / ft.nt;
+        tp = ft.kfast ? it / ft.nkg : it - kgi * ft.nt;
+    };
+    if (b >= 8 * ft.per) {
+        const int u = b - 8 * ft.per;
+        const int it = nmain + u / (2 * KGW), sub = u % (2 * KGW);
+        int kgi, tp;
+        decode(it, kgi, tp);
+        const int tb = 2 * tp + sub / KGW, kb = kgi * KGW + sub % KGW;
+        if (tb >= nb || kb >= g.KB) return;
+        gemm_out_unit<MT>(Vb, U, y, g, tb, kb, (g.CQ + 3) / 4, relu != 0, vec_ok != 0, vs0, vs1, wave, lane);
+        return;
+    }
+    const int item = (b & 7) * ft.per + (b >> 3);
+    if (item >= nmain) return;
+    int kgi, tp;
+    decode(item, kgi, tp);
     const int kw = wave / TS, h = wave % TS;
     const int kb = min(kgi * KGW + kw, g.KB - 1);
     const int cl = lane >> 4;
 
     // Vb as a buffer: a block past the last reads zeros
     const size_t blk_b = (size_t)((g.CQ + 3) / 4 * 4) * g.T * 256;   // bytes of one tile block
-    const size_t tot_b = (size_t)ntb * blk_b;
+    const size_t tot_b = (size_t)nb * blk_b;
     const size_t first = (size_t)(2 * tp) * blk_b;
     const size_t left = tot_b - first;
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
@@ -1302,19 +1463,7 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
         }
     }
     const int kbase = (kgi * KGW + kw) * 16 + 4 * cl;
-    const int per_img = ft.nbh * ft.nbw;
-    auto tile_of = [&](int bb) {
-        const int tb = 2 * tp + bb;
-        const int n = tb / per_img, r2 = tb - n * per_img;
-        const int bh = 16 / ft.bw;
-        const int l16 = lane & 15;
-        TileCoord tc;
-        tc.n = n;
-        tc.ti = (r2 / ft.nbw) * bh + l16 / ft.bw;
-        tc.tj = (r2 % ft.nbw) * ft.bw + l16 % ft.bw;
-        tc.valid = tb < ntb && tc.ti < g.th && tc.tj < g.tw;
-        return tc;
-    };
+    auto tile_of = [&](int bb) { return block_tile(2 * tp + bb, lane & 15, g); };
     const bool rl = relu != 0, vo = vec_ok != 0;
     if constexpr (TS == 1) {
 #pragma unroll
@@ -2248,11 +2397,18 @@ hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g,
 }
 
 // Tile blocks of the split path's workspace for block width bw.
-long split_blocks(const Geom& g, int bw) {
-    const int bh = 16 / bw;
-    return (long)g.N * ((g.th + bh - 1) / bh) * ((g.tw + bw - 1) / bw);
+long split_blocks(const Geom& g) { return ((long)g.P + 15) / 16; }
+size_t vblk_elems(const Geom& g) { return (size_t)split_blocks(g) * ((g.CQ + 3) / 4 * 4) * g.T * 64; }
+
+SplitTail split_tail(const Geom& g) {
+    const int kgw = g.m == 4 ? GoShape<4>::KGW : GoShape<2>::KGW;
+    SplitTail t;
+    t.items = (split_blocks(g) + 1) / 2 * ((g.KB + kgw - 1) / kgw);
+    const long rem = t.items % kSplitCus;
+    t.units = 2 * kgw;
+    t.tail = (t.items > kSplitCus && rem > 0 && rem * t.units <= kSplitCus) ? rem : 0;
+    return t;
 }
-size_t vblk_elems(const Geom& g, int bw) { return (size_t)split_blocks(g, bw) * ((g.CQ + 3) / 4 * 4) * g.T * 64; }
 
 template <int MT, int BW>
 static hipError_t split_instance(const float* x, const float* U, float* y, float* Vb, const Geom& g, bool relu,
@@ -2262,7 +2418,8 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
     ft.bw = BW;
     ft.nbh = (g.th + 16 / BW - 1) / (16 / BW);
     ft.nbw = (g.tw + BW - 1) / BW;
-    const int ntb = g.N * ft.nbh * ft.nbw;
+    const int ntb = g.N * ft.nbh * ft.nbw;      // 16-tile patches of the input transform
+    const int nb = (int)split_blocks(g);        // 16-tile blocks of Vb and the GEMMs
     const int ncq4 = (g.CQ + 3) / 4;
     {
         const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
@@ -2274,20 +2431,22 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    ft.nt = (ntb + 1) / 2;
+    const SplitTail st = split_tail(g);
+    ft.nt = (nb + 1) / 2;
     ft.nkg = (g.KB + GS::KGW - 1) / GS::KGW;
-    ft.per = (int)(((long)ft.nt * ft.nkg + 7) / 8);
+    ft.per = (int)(((long)ft.nt * ft.nkg - st.tail + 7) / 8);
     ft.nsteps = (g.CQ + GS::NQ - 1) / GS::NQ;
     {   // item order: V of a tile pair is read by every filter group
-        const double vb = 4.0 * vblk_elems(g, BW), ub = 4.0 * g.T * g.CQ * 4 * g.KB * 16;
+        const double vb = 4.0 * vblk_elems(g), ub = 4.0 * g.T * g.CQ * 4 * g.KB * 16;
         const double sets = (double)ft.nt * ft.nkg / 32.0;
         const double group_major = vb * ft.nkg + ub * sets / ft.nkg;
         const double tile_major = vb + ub * sets * (ft.nkg < 32 ? 1.0 : 32.0 / ft.nkg);
         ft.kfast = tile_major < group_major ? 1 : 0;
     }
-    const dim3 grid((unsigned)(8 * ft.per)), block(512);
+    const dim3 grid((unsigned)(8 * ft.per + st.tail * st.units)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
-    hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, ntb, (int)relu, vec_ok);
+    hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, nb, (int)relu, vec_ok,
+                       (int)st.tail);
     return hipGetLastError();
 }
 

@@ -48,8 +48,10 @@ def test_workspace_bytes():
     staged = B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_STAGED)
     assert staged >= B.wino_input_tf_bytes(1, 64, 112, 112, 1, 4) + B.wino_gemm_out_bytes(1, 64, 112, 112, 1, 4)
     assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 3, 0) == 2**64 - 1
-    # split: the tile-blocked V, 16-tile blocks (1 x 16 here: 28 x 28 tiles -> 28 x 2 blocks)
-    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_SPLIT) == 4 * 56 * 16 * 36 * 64
+    # split: the blocked V, blocks of 16 consecutive tiles (28 x 28 tiles -> 49 blocks),
+    # channel quads rounded up to a multiple of 4 (16 here; C = 20: 5 -> 8 quads, 2 x 15 x 15 tiles -> 29 blocks)
+    assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_SPLIT) == 4 * 49 * 16 * 36 * 64
+    assert B.wino_workspace_bytes(2, 20, 30, 30, 64, 1, 2, B.WINO_ALGO_SPLIT) == 4 * 29 * 8 * 16 * 64
     assert B.wino_workspace_bytes(1, 3, 112, 112, 64, 1, 4, B.WINO_ALGO_LOWC) == 0
     assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_LOWC) == 2**64 - 1   # C > 4
     assert B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, 0x500) == 2**64 - 1
