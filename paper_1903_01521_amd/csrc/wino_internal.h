@@ -93,6 +93,15 @@ struct SplitTail {
     int units;      // units per item: 2 tile blocks x filter blocks per group
 };
 SplitTail split_tail(const Geom& g);
+// The split path's input transform by whole tile rows: R rows of the batch
+// per workgroup (0: the 16-tile patch kernel instead), LDS row pitch in
+// floats, dynamic LDS bytes.
+constexpr size_t kVrowsLds = 64 << 10;
+struct VrowsPlan {
+    int R, pitch;
+    size_t lds;
+};
+VrowsPlan vrows_plan(const Geom& g, int vec);
 hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
                         hipStream_t s);
 // Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.

@@ -1149,6 +1149,91 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
     }
 }
 
+// Input transform of the split path by whole tile rows: one workgroup per
+// (R consecutive tile rows of the batch, channel quad).  The rows' halo'd
+// patches (A image rows each, all columns) come into LDS by DMA; wave w then
+// transforms tile blocks w, w+4, ... of the rows' tiles, lane = (channel,
+// tile), and stores each block's 9 (m = 4) or 4 (m = 2) groups as whole 1 KiB
+// runs.  The host picks R so that R*tw is a multiple of 16 where LDS allows:
+// every block is then written by one workgroup (a block the row range only
+// partly covers is completed by the neighbouring workgroup).  VEC: 16-byte
+// loads of column chunks starting xsh columns before the patch.
+// LDS: [row r][channel][A rows][pitch] floats, shifted so that a tile's first
+// column sits at a multiple of 4.
+template <int MT, int VEC>
+__global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
+                                               int R, int pitch, int ncq4) {
+    constexpr int A = MT + 2, T = A * A, EW = VEC ? 4 : 1;
+    extern __shared__ float4 xs4[];
+    float* xs = (float*)xs4;
+    const int nrows = g.N * g.th;                        // tile rows of the batch
+    const int ngr = (nrows + R - 1) / R;
+    const int b = blockIdx.x;
+    const int cq = b / ngr, gr0 = (b - cq * ngr) * R;    // quad, first tile row
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n0 = gr0 / g.th;
+    const size_t img = (size_t)g.C * g.H * g.W;
+    const size_t left = ((size_t)g.N - n0) * img * 4;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + (size_t)n0 * img), (short)0, (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
+    const int xsh = VEC ? (4 - g.pad % 4) % 4 : 0, xlo = (4 - xsh) % 4;
+    const int cs = -g.pad - xsh;                         // image column of a patch row's first unit
+    const int ne = pitch / EW;                           // units per patch row
+    const int units = R * 4 * A * ne;
+    const uint32_t plane_b = (uint32_t)g.H * g.W * 4;
+    for (int e = tid; e < units; e += 256) {             // e = ((r*4 + c)*A + u)*ne + k
+        const int k = e % ne, q1 = e / ne;
+        const int u = q1 % A, q2 = q1 / A;
+        const int c = q2 & 3, r = q2 >> 2;
+        const int gr = gr0 + r, n = gr / g.th, ti = gr - n * g.th;
+        const int row = ti * MT - g.pad + u, col = cs + k * EW, ch = cq * 4 + c;
+        const bool ok = gr < nrows && ch < g.C && (unsigned)row < (unsigned)g.H && col >= 0 &&
+                        col + EW <= g.W;
+        const uint32_t off = ok ? (uint32_t)(n - n0) * (uint32_t)(img * 4) + (uint32_t)ch * plane_b +
+                                      ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u
+                                : kInvalid;
+        // the wave's 64 units are consecutive in LDS (lane order)
+        lds_dma<4 * EW>(xr, xs + xlo + (e - lane) * EW, off);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const int l16 = lane & 15, cl = lane >> 4;
+    const int t0 = gr0 * g.tw, t1 = min(gr0 + R, nrows) * g.tw;   // this workgroup's tiles [t0, t1)
+    const size_t qstride = (size_t)ncq4 * 4 * T * 64;             // floats of one block
+    const int last_tail = (t1 == g.P && (g.P & 15)) ? 1 : 0;      // the batch's last block is partial
+    for (int blk = t0 / 16 + wave; blk <= (t1 - 1) / 16; blk += 4) {
+        const int p = blk * 16 + l16;
+        float* dst = Vb + (size_t)blk * qstride + (size_t)cq * T * 64 + lane * 4;
+        if (p >= t0 && p < t1) {
+            const int r = p / g.tw - gr0, tj = p % g.tw;
+            const float* wp = xs + ((r * 4 + cl) * A) * pitch + tj * MT + (xlo ? 4 : 0);
+            float d[A][A];
+#pragma unroll
+            for (int u = 0; u < A; ++u) {
+                const float* rowp = wp + u * pitch;
+                if constexpr (MT == 4) {
+                    const float4 a4 = *(const float4*)rowp;
+                    const float2 b2 = *(const float2*)(rowp + 4);
+                    d[u][0] = a4.x; d[u][1] = a4.y; d[u][2] = a4.z; d[u][3] = a4.w; d[u][4] = b2.x; d[u][5] = b2.y;
+                } else {
+                    const float2 a2 = *(const float2*)rowp;
+                    const float2 b2 = *(const float2*)(rowp + 2);
+                    d[u][0] = a2.x; d[u][1] = a2.y; d[u][2] = b2.x; d[u][3] = b2.y;
+                }
+            }
+            float v[T];
+            input_tf<MT>(d, v);
+#pragma unroll
+            for (int g4 = 0; g4 < T / 4; ++g4)
+                store_out<false>(dst + g4 * 256, v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
+        } else if (last_tail && p >= g.P) {
+#pragma unroll
+            for (int g4 = 0; g4 < T / 4; ++g4) store_out<false>(dst + g4 * 256, 0.f, 0.f, 0.f, 0.f);
+        }
+    }
+}
+
 // GEMMs + output transform from Vb.  A workgroup of 8 waves computes two tile
 // blocks for KGW = 8/TS filter blocks over all channels; wave (kw, h) owns
 // filter block kw and transform rows [h*A/TS, (h+1)*A/TS) of both tile blocks
@@ -2400,6 +2485,31 @@ hipError_t launch_fused(const float* x, const float* U, float* y, const Geom& g,
 long split_blocks(const Geom& g) { return ((long)g.P + 15) / 16; }
 size_t vblk_elems(const Geom& g) { return (size_t)split_blocks(g) * ((g.CQ + 3) / 4 * 4) * g.T * 64; }
 
+// Rows per workgroup of the row-wise input transform: R*tw a multiple of
+// 16 (whole blocks) where that fits 64 KB of LDS, else fewer; R = 0 (the
+// patch kernel) when one tile row's patch does not fit, or the images a row
+// range spans do not fit the 32-bit load offsets.
+VrowsPlan vrows_plan(const Geom& g, int vec) {
+    VrowsPlan p{0, 0, 0};
+    const int xsh = vec ? (4 - g.pad % 4) % 4 : 0;
+    p.pitch = (xsh + g.tw * g.m + 2 + 3) / 4 * 4;
+    const size_t row_b = (size_t)4 * g.A * p.pitch * sizeof(float);    // one tile row, 4 channels
+    int gcd = 16, t = g.tw;
+    while (t) {
+        const int r = gcd % t;
+        gcd = t;
+        t = r;
+    }
+    int R = 16 / gcd;
+    while (R > 1 && (size_t)R * row_b > kVrowsLds) --R;
+    const size_t img_b = (size_t)g.C * g.H * g.W * sizeof(float);
+    while (R > 1 && (size_t)(R / g.th + 2) * img_b >= (size_t)kInvalid) --R;
+    if ((size_t)R * row_b > kVrowsLds || (size_t)(R / g.th + 2) * img_b >= (size_t)kInvalid) return p;
+    p.R = R;
+    p.lds = R * row_b + 16;
+    return p;
+}
+
 SplitTail split_tail(const Geom& g) {
     const int kgw = g.m == 4 ? GoShape<4>::KGW : GoShape<2>::KGW;
     SplitTail t;
@@ -2422,11 +2532,17 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
     const int nb = (int)split_blocks(g);        // 16-tile blocks of Vb and the GEMMs
     const int ncq4 = (g.CQ + 3) / 4;
     {
-        const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
-        if (g.W % 4 == 0 && aligned(x, 16)) {
-            hipLaunchKernelGGL((k_vblk<MT, BW, 1>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
+        const int vec = g.W % 4 == 0 && aligned(x, 16);
+        const VrowsPlan vp = vrows_plan(g, vec);
+        if (vp.R > 0) {
+            const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
+            const dim3 grid((unsigned)(ngr * ncq4 * 4)), block(256);
+            if (vec) hipLaunchKernelGGL((k_vrows<MT, 1>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, ncq4);
+            else hipLaunchKernelGGL((k_vrows<MT, 0>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, ncq4);
         } else {
-            hipLaunchKernelGGL((k_vblk<MT, BW, 0>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
+            const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
+            if (vec) hipLaunchKernelGGL((k_vblk<MT, BW, 1>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
+            else hipLaunchKernelGGL((k_vblk<MT, BW, 0>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
