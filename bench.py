@@ -57,8 +57,9 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
                 "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
-                # the split path's call: the input transform, then the GEMMs with the output transform
-                "split": ("void wino::k_vblk", "void wino::k_gemm_out"),
+                # the split path's call: the input transform (by tile rows, or by 16-tile
+                # patches for very wide images), then the GEMMs with the output transform
+                "split": ("void wino::k_vrows|void wino::k_vblk", "void wino::k_gemm_out"),
                 # the fused kernel over channel slices, then the sum of the slices
                 "fused_sliced": ("void wino::k_fused", "void wino::k_slice_sum")}
 
@@ -66,7 +67,8 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
 def kernel_label(kind: str) -> str:
     names = KERNEL_NAMES[kind]
     names = (names,) if isinstance(names, str) else names
-    return " + ".join(n[5:] if n.startswith("void ") else n for n in names)
+    strip = lambda n: n[5:] if n.startswith("void ") else n
+    return " + ".join(" or ".join(strip(a) for a in n.split("|")) for n in names)
 
 
 def log(*a):
@@ -179,11 +181,13 @@ def pmc_rows(d: str):
 def kernel_is(name: str, prefix: str) -> bool:
     """Whether a profiler kernel name is of the given kind: template instances
     carry their return type ("void wino::k_fused<...>(...)"), plain functions
-    do not ("wino::k_gemm(...)")."""
+    do not ("wino::k_gemm(...)").  A prefix "a|b" matches either kernel."""
     strip = lambda n: n[5:] if n.startswith("void ") else n
-    base = strip(prefix)
     n = strip(name)
-    return n.startswith(base) and n[len(base):len(base) + 1] in ("<", "(")
+    for base in (strip(p) for p in prefix.split("|")):
+        if n.startswith(base) and n[len(base):len(base) + 1] in ("<", "("):
+            return True
+    return False
 
 
 MFMA_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE")

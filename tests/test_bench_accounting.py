@@ -109,3 +109,14 @@ def test_default_workload_is_the_large_layer():
     assert f["bytes"]["split"] == 4 * (64 * 256 * 56 * 56 * 2 + 36 * 256 * 256)
     r = bench.roofline("split", f, 1e-3)
     assert r["bound"] == "mfma" and r["achieved"] == pytest.approx(f["gemm_flops"] / 1e-3 / 1e12, rel=1e-3)
+
+
+def test_split_kernel_names():
+    # The split call's input transform runs as k_vrows (by tile rows) or, for
+    # very wide images, k_vblk (by 16-tile patches): either counts for it.
+    assert bench.kernel_label("split") == "wino::k_vrows or wino::k_vblk + wino::k_gemm_out"
+    pre = bench.KERNEL_NAMES["split"][0]
+    assert bench.kernel_is("void wino::k_vrows<4, 1>(float const*, float*, wino::Geom, int, int, int)", pre)
+    assert bench.kernel_is("void wino::k_vblk<4, 16, 1>(float const*, float*, wino::Geom, int, int, int)", pre)
+    assert not bench.kernel_is("void wino::k_vrowsx<4>(float const*)", pre)
+    assert not bench.kernel_is("void wino::k_gemm_out<4>(float const*)", pre)
