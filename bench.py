@@ -57,6 +57,7 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 "input": "void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
                 "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
+                "gemm16": "void wino::k_gemm16",
                 # the split path's call: the input transform (by tile rows, or by 16-tile
                 # patches for very wide images), then the GEMMs with the output transform
                 "split": ("void wino::k_vrows|void wino::k_vblk", "void wino::k_gemm_out"),
@@ -117,18 +118,20 @@ def layer_numbers(N, L):
         "stages": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
         # the same with 16-bit V and U (fp16 / bf16 GEMM operands)
         "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
+        # the 16-bit GEMM stage alone: 16-bit V and U read, fp32 M written
+        "gemm16": v_b // 2 + u_b // 2 + m_b,
     }
     f["flops"] = {"fused": f["gemm_flops"], "fused_sliced": f["gemm_flops"], "split": f["gemm_flops"],
                   "gemm": f["gemm_flops"],
                   "stages": f["gemm_flops"],
-                  "stages16": f["gemm_flops"]}
+                  "stages16": f["gemm_flops"], "gemm16": f["gemm_flops"]}
     return f
 
 
 def roofline(kind, nums, seconds):
     b = nums["bytes"].get(kind, 0)
     fl = nums["flops"].get(kind, 0)
-    peak = FP16_MFMA_PEAK if kind == "stages16" else FP32_MFMA_PEAK   # the GEMM's own operand type
+    peak = FP16_MFMA_PEAK if kind in ("stages16", "gemm16") else FP32_MFMA_PEAK   # the GEMM's own operand type
     t_hbm = b / HBM_PEAK
     t_mfma = fl / peak
     if t_mfma >= t_hbm and fl > 0:

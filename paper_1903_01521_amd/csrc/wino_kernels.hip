@@ -1061,10 +1061,10 @@ __device__ __forceinline__ void patch_offsets(uint32_t (&xoff)[JX], const Geom& 
 // One direct-to-LDS buffer load of BYTES per lane (a device function: the
 // host pass rejects the 16-byte form written directly in a kernel body).
 template <int BYTES>
-__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, uint32_t off) {
+__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, uint32_t off, uint32_t soff = 0) {
     static_assert(BYTES == 4 || BYTES == 16, "dword or 16-byte loads");
-    if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
-    else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 4, off, 0, 0, 0);
+    if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, soff, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 4, off, soff, 0, 0);
 }
 
 template <int MT, int BW, int VEC>
@@ -1711,15 +1711,16 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
 // ------------------------------------------------------------------ 16-bit operands
 // Reduced-precision three-stage path: U and V are rounded to fp16 (PREC 1) or
 // bf16 (PREC 2), to nearest with ties to even, and the T per-position GEMMs run
-// on v_mfma_f32_16x16x16_{f16,bf16} with fp32 accumulation; M and the output
-// transform stay fp32.  MFMA lane layout (16 x 16 x 16): lane l holds A[l%16]
-// [4*(l/16) .. +3] and B[4*(l/16) .. +3][l%16]; D as for the fp32 MFMA.  So a
-// lane carries four consecutive channels, and the 16-bit layouts are
+// on v_mfma_f32_16x16x32_{f16,bf16} with fp32 accumulation; M and the output
+// transform stay fp32.  The 16-bit layouts hold 16-channel groups, a lane
+// carrying four consecutive channels of its group:
 //   UH[KB][C16][T][64][4]: element (t, c, k) at lane ((c%16)/4)*16 + k%16, half c%4
 //   VH[PB][C16][T][64][4]: element (t, c, p) at lane ((c%16)/4)*16 + p%16, half c%4
 // (C16 = ceil(C/16), padding zero): one 8-byte word per lane and position.
-typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
+// The MFMA's 16-byte operand of lane l holds A[l%16] (or B[.][l%16]) at eight
+// reduction slots, here two such words: groups 2j and 2j+1.
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 template <int PREC>
 __device__ __forceinline__ uint32_t to16(float v) {
@@ -1738,13 +1739,13 @@ __device__ __forceinline__ uint2 pack16(float a, float b, float c, float d) {
 }
 
 template <int PREC>
-__device__ __forceinline__ f32x4 mfma16x16x16(uint2 a, uint2 b, f32x4 c) {
+__device__ __forceinline__ f32x4 mfma16x16x32(uint4 a, uint4 b, f32x4 c) {
     if constexpr (PREC == 1)
-        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b),
-                                                      c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b),
+                                                       c, 0, 0, 0);
     else
-        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
-                                                          __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                        __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
 // One wave per (16-filter block, 16-channel group): lane = (k%16, channel
@@ -1833,82 +1834,119 @@ __global__ __launch_bounds__(256) void k_input16(const float* __restrict__ x, ui
     for (int t = 0; t < T; ++t) dst[t * 64] = make_uint2(ph[t][0], ph[t][1]);
 }
 
-// The T GEMMs on 16-bit operands: workgroup = 4 positions x 4 k-blocks x 4
-// p-blocks as in k_gemm (same XCD-contiguous item order), 16 channels per
-// chunk through an LDS double buffer, 16 MFMAs per wave and chunk.
-template <int PREC>
-__global__ __launch_bounds__(256) void k_gemm16(const uint2* __restrict__ UH, const uint2* __restrict__ VH,
+// The T GEMMs on 16-bit operands, on v_mfma_f32_16x16x32_{f16,bf16}: one
+// instruction takes two 16-channel groups, the lane's words of groups 2j and
+// 2j+1 side by side in its 16-byte operand (A and B place the same channel in
+// the same operand slot, so the instruction's reduction covers all 32).
+// Workgroup = NP positions x 8 k-blocks x 8 p-blocks, 8 waves of NP x 4
+// k-blocks x 2 p-blocks each (XCD-contiguous item order).  A chunk of 32
+// channels is 16*NP pairs (U of position x k-block, then V of position x
+// p-block) of two 512-byte group blocks and comes into one of three LDS stages
+// by DMA two chunks ahead: one 16-byte load per lane moves one pair (lanes
+// 0-31 the first group, 32-63 the second).  Blocks and groups past the last
+// read zero.
+template <int PREC, int NP>
+__global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, const uint2* __restrict__ VH,
                                                 float* __restrict__ M, Geom g, int C16) {
-    __shared__ uint2 As[2][4][4][64];    // [buf][position][k-block][lane]
-    __shared__ uint2 Bs[2][4][4][64];    // [buf][position][p-block][lane]
-    const int T = g.T, TG = g.T / 4;
-    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
-    const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
+    constexpr int NPAIR = 16 * NP, PPW = NPAIR / 8;       // pairs per chunk, per wave
+    __shared__ uint4 st0[NPAIR * 64], st1[NPAIR * 64], st2[NPAIR * 64];   // three stages of pairs x 1 KB
+    const int T = g.T, TN = g.T / NP;
+    const int KB8 = (g.KB + 7) >> 3, PB8 = (g.PB + 7) >> 3;
+    const long nitems = (long)TN * PB8 * KB8, per = (nitems + 7) / 8;
     const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (item >= nitems) return;
-    const int kb0 = (int)(item % KB4) * 4;
-    const long rest = item / KB4;
-    const int pb0 = (int)(rest % PB4) * 4;
-    const int tg = (int)(rest / PB4);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wk = wave >> 1, wp = wave & 1;
-
-    // Loader: a chunk is 16 A and 16 B blocks (position x block) of 64 words;
-    // thread tid moves word (tid & 63) of blocks (tid >> 6) + 4*i, i < 4.
-    uint2 ra[4], rb[4];
-    auto fetch = [&](int c16) {
+    const int kb0 = (int)(item % KB8) * 8;
+    const long rest = item / KB8;
+    const int pb0 = (int)(rest % PB8) * 8;
+    const int t0 = (int)(rest / PB8) * NP;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wk = wave >> 2, wp = wave & 3;              // k-blocks 4*wk .. +3, p-blocks 2*wp, +1
+    const int NC = (C16 + 1) / 2;
+    const uint32_t gstride = (uint32_t)T * 512;          // bytes between groups of one block
+    const uint32_t bstride = (uint32_t)C16 * gstride;    // bytes between blocks
+    // U and V of this item's blocks as buffers: a block past the last reads zeros
+    const size_t ub = (size_t)min(g.KB - kb0, 8) * bstride, vb = (size_t)min(g.PB - pb0, 8) * bstride;
+    const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)((const char*)UH + (size_t)kb0 * bstride), (short)0, (int)ub, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)((const char*)VH + (size_t)pb0 * bstride), (short)0, (int)vb, kRsrcWord3);
+    auto stage = [&](auto sc) -> uint4* {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S == 0) return st0;
+        else if constexpr (S == 1) return st1;
+        else return st2;
+    };
+    // DMA of chunk c into stage sc: wave w moves pairs PPW*w .. PPW*w+PPW-1.
+    const uint32_t lane_off = (uint32_t)(lane >> 5) * gstride + (uint32_t)(lane & 31) * 16u;
+    auto issue = [&](auto sc, int c) {
+        uint4* s = stage(sc);
+        const bool g1ok = 2 * c + 1 < C16;
+        const uint32_t voff = lane_off + ((lane >> 5) && !g1ok ? kInvalid : 0u);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int blk = (tid >> 6) + 4 * i, t4 = blk >> 2, bi = blk & 3;
-            const int kb = kb0 + bi, pb = pb0 + bi, t = 4 * tg + t4;
-            ra[i] = make_uint2(0u, 0u);
-            rb[i] = ra[i];
-            if (kb < g.KB) ra[i] = UH[(((size_t)kb * C16 + c16) * T + t) * 64 + lane];
-            if (pb < g.PB) rb[i] = VH[(((size_t)pb * C16 + c16) * T + t) * 64 + lane];
+        for (int i = 0; i < PPW; ++i) {
+            const int q = wave * PPW + i, qq = q < 8 * NP ? q : q - 8 * NP, pos = qq >> 3, blk = qq & 7;
+            const uint32_t soff = (uint32_t)blk * bstride + (uint32_t)(2 * c) * gstride + (uint32_t)(t0 + pos) * 512u;
+            if (q < 8 * NP) lds_dma<16>(ur, (float*)(s + q * 64), voff, __builtin_amdgcn_readfirstlane(soff));
+            else lds_dma<16>(vr, (float*)(s + q * 64), voff, __builtin_amdgcn_readfirstlane(soff));
         }
     };
-    auto stage = [&](int buf) {
+    f32x4 acc[NP][4][2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int blk = (tid >> 6) + 4 * i;
-            As[buf][blk >> 2][blk & 3][lane] = ra[i];
-            Bs[buf][blk >> 2][blk & 3][lane] = rb[i];
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[p][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // operand of lane l from pair q: its words of both groups
+    auto operand = [&](const uint4* s, int q) {
+        const uint2* w = (const uint2*)(s + q * 64);
+        const uint2 a = w[lane], b = w[64 + lane];
+        return make_uint4(a.x, a.y, b.x, b.y);
+    };
+    issue(IC<0>{}, 0);
+    if (NC > 1) issue(IC<1>{}, 1);
+    // Chunk ch (stage ch % 3): at its start the PPW DMA loads of chunk ch+1
+    // may still be in flight, not those of chunk ch; the barrier then tells
+    // every wave that chunk ch is in LDS and chunk ch-1's stage is free for
+    // chunk ch+2.
+    auto chunk = [&](auto sc, int ch) {
+        constexpr int S = decltype(sc)::value;
+        if (ch + 1 < NC) wait_vm_lds<PPW>();
+        else wait_vm_lds<0>();
+        wg_barrier();
+        if (ch + 2 < NC) issue(IC<(S + 2) % 3>{}, ch + 2);
+        const uint4* s = stage(sc);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            uint4 a[4], b[2];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = operand(s, p * 8 + wk * 4 + i);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) b[j] = operand(s, 8 * NP + p * 8 + wp * 2 + j);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[p][i][j] = mfma16x16x32<PREC>(a[i], b[j], acc[p][i][j]);
         }
     };
-    f32x4 acc[4][2][2];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    fetch(0);
-    stage(0);
-    __syncthreads();
-    for (int ch = 0; ch < C16; ++ch) {
-        const int buf = ch & 1;
-        if (ch + 1 < C16) fetch(ch + 1);
-#pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4) {
-            const uint2 a0 = As[buf][t4][wk * 2 + 0][lane], a1 = As[buf][t4][wk * 2 + 1][lane];
-            const uint2 b0 = Bs[buf][t4][wp * 2 + 0][lane], b1 = Bs[buf][t4][wp * 2 + 1][lane];
-            acc[t4][0][0] = mfma16x16x16<PREC>(a0, b0, acc[t4][0][0]);
-            acc[t4][0][1] = mfma16x16x16<PREC>(a0, b1, acc[t4][0][1]);
-            acc[t4][1][0] = mfma16x16x16<PREC>(a1, b0, acc[t4][1][0]);
-            acc[t4][1][1] = mfma16x16x16<PREC>(a1, b1, acc[t4][1][1]);
-        }
-        if (ch + 1 < C16) stage(buf ^ 1);
-        __syncthreads();
+    int ch = 0;
+    for (; ch + 3 <= NC; ch += 3) {
+        chunk(IC<0>{}, ch);
+        chunk(IC<1>{}, ch + 1);
+        chunk(IC<2>{}, ch + 2);
     }
+    if (ch < NC) chunk(IC<0>{}, ch);
+    if (ch + 1 < NC) chunk(IC<1>{}, ch + 1);
 #pragma unroll
-    for (int t4 = 0; t4 < 4; ++t4)
+    for (int p = 0; p < NP; ++p)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
+                const int kb = kb0 + wk * 4 + i, pb = pb0 + wp * 2 + j;
                 if (kb < g.KB && pb < g.PB)
-                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
+                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + t0 + p) * 256 + lane * 4) = acc[p][i][j];
             }
 }
 
@@ -1938,11 +1976,17 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
     else hipLaunchKernelGGL((k_input16<4, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
+    // one position per workgroup: 48 KB of LDS, so up to three workgroups share a CU
+    constexpr int NP = 1;
+    if ((size_t)8 * C16 * g.T * 512 >= (size_t)kInvalid) return hipErrorInvalidConfiguration;   // 32-bit offsets
+    const long nitems = (long)((g.PB + 7) / 8) * ((g.KB + 7) / 8) * (g.T / NP);
     const long wgs = (nitems + 7) / 8 * 8;
     if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
-    if (prec == 1) hipLaunchKernelGGL((k_gemm16<1>), dim3((unsigned)wgs), block, 0, s, (const uint2*)UH, vh, M, g, C16);
-    else hipLaunchKernelGGL((k_gemm16<2>), dim3((unsigned)wgs), block, 0, s, (const uint2*)UH, vh, M, g, C16);
+    const dim3 b512(512);
+    if (prec == 1)
+        hipLaunchKernelGGL((k_gemm16<1, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C16);
+    else
+        hipLaunchKernelGGL((k_gemm16<2, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C16);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_output_transform(M, y, g, relu, s);

@@ -120,3 +120,14 @@ def test_split_kernel_names():
     assert bench.kernel_is("void wino::k_vblk<4, 16, 1>(float const*, float*, wino::Geom, int, int, int)", pre)
     assert not bench.kernel_is("void wino::k_vrowsx<4>(float const*)", pre)
     assert not bench.kernel_is("void wino::k_gemm_out<4>(float const*)", pre)
+
+
+def test_gemm16_accounting():
+    # The 16-bit GEMM stage reads 16-bit V and U and writes fp32 M; its roof is
+    # HBM at every shape here (the 16-bit matrix peak is 16x the fp32 one).
+    L = wl.WORKLOADS["f4_n64_c256_k256_56x56"].first
+    f = bench.layer_numbers(64, L)
+    P = 64 * 14 * 14
+    assert f["bytes"]["gemm16"] == 2 * 36 * P * 256 + 2 * 36 * 256 * 256 + 4 * 36 * P * 256
+    r = bench.roofline("gemm16", f, 150e-6)
+    assert r["bound"] == "hbm" and r["peak"] == 8000.0
