@@ -1149,8 +1149,9 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
     }
 }
 
-// Input transform of the split path by whole tile rows: one workgroup per
-// (R consecutive tile rows of the batch, channel quad).  The rows' halo'd
+// Input transform by whole tile rows (the split path's Vb with nq = CQ
+// rounded up to a multiple of 4, the staged path's V with nq = CQ): one
+// workgroup per (R consecutive tile rows of the batch, channel quad).  The rows' halo'd
 // patches (A image rows each, all columns) come into LDS by DMA; wave w then
 // transforms tile blocks w, w+4, ... of the rows' tiles, lane = (channel,
 // tile), and stores each block's 9 (m = 4) or 4 (m = 2) groups as whole 1 KiB
@@ -1162,7 +1163,7 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
 // column sits at a multiple of 4.
 template <int MT, int VEC>
 __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
-                                               int R, int pitch, int ncq4) {
+                                               int R, int pitch, int nq) {
     constexpr int A = MT + 2, T = A * A, EW = VEC ? 4 : 1;
     extern __shared__ float4 xs4[];
     float* xs = (float*)xs4;
@@ -1200,7 +1201,7 @@ __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, floa
     __syncthreads();
     const int l16 = lane & 15, cl = lane >> 4;
     const int t0 = gr0 * g.tw, t1 = min(gr0 + R, nrows) * g.tw;   // this workgroup's tiles [t0, t1)
-    const size_t qstride = (size_t)ncq4 * 4 * T * 64;             // floats of one block
+    const size_t qstride = (size_t)nq * T * 64;                   // floats of one block
     const int last_tail = (t1 == g.P && (g.P & 15)) ? 1 : 0;      // the batch's last block is partial
     for (int blk = t0 / 16 + wave; blk <= (t1 - 1) / 16; blk += 4) {
         const int p = blk * 16 + l16;
@@ -2332,6 +2333,26 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
         }
         return hipGetLastError();
     }
+    if (g.r == 3) {
+        // by whole tile rows where the rows' patches fit LDS (the split path's kernel)
+        const int vec = g.W % 4 == 0 && aligned(x, 16);
+        const VrowsPlan vp = vrows_plan(g, vec);
+        if (vp.R > 0) {
+            const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
+            const dim3 gr((unsigned)(ngr * g.CQ)), b256(256);
+#define WINO_VROWS(MT, VEC) \
+    hipLaunchKernelGGL((k_vrows<MT, VEC>), gr, b256, vp.lds, s, x, V, g, vp.R, vp.pitch, g.CQ)
+            if (g.m == 2) {
+                if (vec) WINO_VROWS(2, 1);
+                else WINO_VROWS(2, 0);
+            } else {
+                if (vec) WINO_VROWS(4, 1);
+                else WINO_VROWS(4, 0);
+            }
+#undef WINO_VROWS
+            return hipGetLastError();
+        }
+    }
     if (g.r == 5)
         hipLaunchKernelGGL((k_input<2, 5>), grid, block, 0, s, x, V, g, nwg);
     else if (g.m == 2)
@@ -2581,8 +2602,8 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
         if (vp.R > 0) {
             const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
             const dim3 grid((unsigned)(ngr * ncq4 * 4)), block(256);
-            if (vec) hipLaunchKernelGGL((k_vrows<MT, 1>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, ncq4);
-            else hipLaunchKernelGGL((k_vrows<MT, 0>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, ncq4);
+            if (vec) hipLaunchKernelGGL((k_vrows<MT, 1>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, 4 * ncq4);
+            else hipLaunchKernelGGL((k_vrows<MT, 0>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, 4 * ncq4);
         } else {
             const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
             if (vec) hipLaunchKernelGGL((k_vblk<MT, BW, 1>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
