@@ -1149,6 +1149,18 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
     }
 }
 
+// fp16 (PREC 1) or bf16 (PREC 2) bits of v, to nearest with ties to even.
+template <int PREC>
+__device__ __forceinline__ uint32_t to16(float v) {
+    if constexpr (PREC == 1) {
+        return (uint32_t)__builtin_bit_cast(unsigned short, (_Float16)v);
+    } else {
+        const uint32_t u = __builtin_bit_cast(uint32_t, v);
+        if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;        // NaN stays NaN
+        return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;               // nearest, ties to even
+    }
+}
+
 // Input transform by whole tile rows (the split path's Vb with nq = CQ
 // rounded up to a multiple of 4, the staged path's V with nq = CQ): one
 // workgroup per (R consecutive tile rows of the batch, channel quad).  The rows' halo'd
@@ -1160,8 +1172,11 @@ __global__ __launch_bounds__(256) void k_vblk(const float* __restrict__ x, float
 // partly covers is completed by the neighbouring workgroup).  VEC: 16-byte
 // loads of column chunks starting xsh columns before the patch.
 // LDS: [row r][channel][A rows][pitch] floats, shifted so that a tile's first
-// column sits at a multiple of 4.
-template <int MT, int VEC>
+// column sits at a multiple of 4.  OUT = 1 / 2: the 16-bit three-stage path's
+// VH (fp16 / bf16, 16-channel groups, a lane's word holding four channels):
+// the lane stores its channel's 16 bits, and a wave's store covers its quad's
+// 128 contiguous bytes of a group's position block; nq = 4 * C16.
+template <int MT, int VEC, int OUT = 0>
 __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
                                                int R, int pitch, int nq) {
     constexpr int A = MT + 2, T = A * A, EW = VEC ? 4 : 1;
@@ -1203,6 +1218,12 @@ __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, floa
     const int t0 = gr0 * g.tw, t1 = min(gr0 + R, nrows) * g.tw;   // this workgroup's tiles [t0, t1)
     const size_t qstride = (size_t)nq * T * 64;                   // floats of one block
     const int last_tail = (t1 == g.P && (g.P & 15)) ? 1 : 0;      // the batch's last block is partial
+    // 16-bit VH: the half of (channel cq*4 + cl, tile l16) in block blk,
+    // position t at [t * 256] (halves: [blk][C16][T][64 lanes][4])
+    auto vh_dst = [&](int blk) {
+        const int c16 = cq >> 2, q = cq & 3;
+        return (unsigned short*)Vb + (((size_t)blk * (nq >> 2) + c16) * T * 64 + q * 16 + l16) * 4 + cl;
+    };
     for (int blk = t0 / 16 + wave; blk <= (t1 - 1) / 16; blk += 4) {
         const int p = blk * 16 + l16;
         float* dst = Vb + (size_t)blk * qstride + (size_t)cq * T * 64 + lane * 4;
@@ -1225,12 +1246,24 @@ __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, floa
             }
             float v[T];
             input_tf<MT>(d, v);
+            if constexpr (OUT == 0) {
 #pragma unroll
-            for (int g4 = 0; g4 < T / 4; ++g4)
-                store_out<false>(dst + g4 * 256, v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
+                for (int g4 = 0; g4 < T / 4; ++g4)
+                    store_out<false>(dst + g4 * 256, v[4 * g4], v[4 * g4 + 1], v[4 * g4 + 2], v[4 * g4 + 3]);
+            } else {
+                unsigned short* h = vh_dst(blk);
+#pragma unroll
+                for (int t = 0; t < T; ++t) h[t * 256] = (unsigned short)to16<OUT>(v[t]);
+            }
         } else if (last_tail && p >= g.P) {
+            if constexpr (OUT == 0) {
 #pragma unroll
-            for (int g4 = 0; g4 < T / 4; ++g4) store_out<false>(dst + g4 * 256, 0.f, 0.f, 0.f, 0.f);
+                for (int g4 = 0; g4 < T / 4; ++g4) store_out<false>(dst + g4 * 256, 0.f, 0.f, 0.f, 0.f);
+            } else {
+                unsigned short* h = vh_dst(blk);
+#pragma unroll
+                for (int t = 0; t < T; ++t) h[t * 256] = 0;
+            }
         }
     }
 }
@@ -1723,16 +1756,6 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <int PREC>
-__device__ __forceinline__ uint32_t to16(float v) {
-    if constexpr (PREC == 1) {
-        return (uint32_t)__builtin_bit_cast(unsigned short, (_Float16)v);
-    } else {
-        const uint32_t u = __builtin_bit_cast(uint32_t, v);
-        if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;        // NaN stays NaN
-        return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;               // nearest, ties to even
-    }
-}
 
 template <int PREC>
 __device__ __forceinline__ uint2 pack16(float a, float b, float c, float d) {
@@ -1951,6 +1974,8 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
             }
 }
 
+static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
 hipError_t launch_filter_transform16(const float* gw, void* UH, int C, int K, int m, int prec, hipStream_t s) {
     const int C16 = (C + 15) / 16, KB = (K + 15) / 16;
     const long waves = (long)KB * C16;
@@ -1971,7 +1996,30 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 gi((unsigned)((nwg + 7) / 8 * 8)), block(256);
     uint2* vh = (uint2*)VH;
-    if (g.m == 2 && prec == 1) hipLaunchKernelGGL((k_input16<2, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
+    const int vec = g.W % 4 == 0 && aligned(x, 16);
+    const VrowsPlan vp = vrows_plan(g, vec);
+    if (vp.R > 0) {
+        // by whole tile rows, the lanes of a quad storing their channels' 16 bits
+        const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
+        const dim3 gr((unsigned)(ngr * 4 * C16)), b256(256);
+        float* vf = (float*)VH;
+#define WINO_VROWS16(MT, VEC, P) \
+    hipLaunchKernelGGL((k_vrows<MT, VEC, P>), gr, b256, vp.lds, s, x, vf, g, vp.R, vp.pitch, 4 * C16)
+        if (g.m == 2 && prec == 1) {
+            if (vec) WINO_VROWS16(2, 1, 1);
+            else WINO_VROWS16(2, 0, 1);
+        } else if (g.m == 2) {
+            if (vec) WINO_VROWS16(2, 1, 2);
+            else WINO_VROWS16(2, 0, 2);
+        } else if (prec == 1) {
+            if (vec) WINO_VROWS16(4, 1, 1);
+            else WINO_VROWS16(4, 0, 1);
+        } else {
+            if (vec) WINO_VROWS16(4, 1, 2);
+            else WINO_VROWS16(4, 0, 2);
+        }
+#undef WINO_VROWS16
+    } else if (g.m == 2 && prec == 1) hipLaunchKernelGGL((k_input16<2, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
     else if (g.m == 2) hipLaunchKernelGGL((k_input16<2, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
     else if (prec == 1) hipLaunchKernelGGL((k_input16<4, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
     else hipLaunchKernelGGL((k_input16<4, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
@@ -2276,7 +2324,6 @@ __global__ __launch_bounds__(256) void k_maxpool2x2(const float* __restrict__ x,
 
 // ------------------------------------------------------------------ launchers
 
-static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // Streaming (non-temporal) stores of y pay off once y outgrows one XCD's 4 MB
 // L2 (measured: plain stores 2-6% slower at 6-13 MB of output, 10% slower at
