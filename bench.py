@@ -366,6 +366,134 @@ def trace_summary(args):
     print(text, end="")
 
 
+# Layers whose algorithm choice the planner table records: the single 3x3
+# layers, one layer of the ResNet stage, and the VGG-16 layers at N=1 and N=32.
+PLANNER_WORKLOADS = ("f2_n1_c32_k32_56x56", "f4_n1_c64_k64_112x112", "f4_n1_c48_k48_57x57",
+                     "f4_resnet_stage_n8_c128_28x28", "vgg16_stack_n1", "vgg16_stack_n32",
+                     "f4_n64_c256_k256_56x56", "f4_lowc_n64_c3_k64_224x224", "f4_lowc_n1_c3_k64_224x224")
+PLANNER_TABLE = os.path.join(PROFILES, "planner_table.txt")
+
+
+def planner_layers():
+    """Unique (N, C, H, W, K, pad, m) of the layers PLANNER_WORKLOADS run."""
+    from paper_1903_01521_amd import workloads as wl
+    seen, out = set(), []
+    for name in PLANNER_WORKLOADS:
+        w = wl.WORKLOADS[name]
+        for L in w.layers:
+            key = (w.N, L.C, L.H, L.W, L.K, L.pad, L.m)
+            if key not in seen:
+                seen.add(key)
+                out.append(key)
+    return out
+
+
+def read_planner_table(path=PLANNER_TABLE):
+    """Rows of the committed planner table: dict per layer with the shape, the
+    measured time (us) of every algorithm the library accepted for it, and
+    AUTO's choice when the table was taken."""
+    rows = []
+    for line in open(path):
+        if line.startswith("#") or not line.strip() or line.startswith("N ") or ":" in line.split()[0]:
+            continue
+        f = line.split()
+        shape = tuple(int(v) for v in f[:7])
+        times = {}
+        for kv in f[7:-2]:
+            k, v = kv.split("=")
+            times[k] = float(v)
+        rows.append(dict(shape=shape, times=times, best=f[-2], auto=f[-1]))
+    return rows
+
+
+def planner_candidate_name(algo: int, nsl: int) -> str:
+    from paper_1903_01521_amd import binding as B
+    base = {B.WINO_ALGO_FUSED: "fused", B.WINO_ALGO_SPLIT: "split", B.WINO_ALGO_STAGED: "staged",
+            B.WINO_ALGO_LOWC: "lowc"}[algo]
+    return f"{base}_s{nsl}" if nsl > 1 else base
+
+
+def planner_table(args):
+    """Time every algorithm the library accepts on each planner layer (graph
+    of back-to-back calls, median of replays) and record AUTO's choice."""
+    import torch
+    from paper_1903_01521_amd import binding as B
+    B.lib()
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(0)
+    lines = ["# Planner table: per-layer time (us, one wino_conv2d call, HIP graph of 10 back-to-back",
+             "# calls, median of 5 replays) of every algorithm the library accepts for the layer",
+             "# (fused: the planner's fused variant without channel slices; fused_sN: with N slices;",
+             "# split; staged; lowc), the fastest, and AUTO's choice (wino_plan_r) when taken.",
+             "# one MI355X; command (on the GPU host, from the repository root):",
+             "#   python3 bench.py --planner-table",
+             f"sources_sha256: {sources_hash()}",
+             "N C H W K pad m  times...  best auto"]
+
+    def time_us(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(2):
+                B.check(fn(torch.cuda.current_stream().cuda_stream), "warm-up")
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                B.check(fn(torch.cuda.current_stream().cuda_stream), "capture")
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(5):
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3 / 10)
+        del g
+        return float(np.median(ts))
+
+    for (N, C, H, W, K, pad, m) in planner_layers():
+        x = torch.from_numpy(rng.standard_normal((N, C, H, W)).astype(np.float32)).to(dev)
+        g = torch.from_numpy((rng.standard_normal((K, C, 3, 3)) * np.sqrt(2.0 / (9 * C))).astype(np.float32)).to(dev)
+        U = torch.empty(B.wino_filter_bytes(C, K, m) // 4, dtype=torch.float32, device=dev)
+        B.check(B.wino_filter_transform(g, U, C, K, m), "wino_filter_transform")
+        Ho, Wo = H + 2 * pad - 2, W + 2 * pad - 2
+        y = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=dev)
+        st, algo, nsl = B.wino_plan_r(N, C, H, W, K, pad, m, 3, 0)
+        B.check(st, "wino_plan_r")
+        auto = planner_candidate_name(algo, nsl)
+        cands = [("fused", B.WINO_ALGO_FUSED)] + [(f"fused_s{n}", B.WINO_ALGO_FUSED | B.WINO_CSLICES(n))
+                                                  for n in (2, 4)] + [
+            ("split", B.WINO_ALGO_SPLIT), ("staged", B.WINO_ALGO_STAGED), ("lowc", B.WINO_ALGO_LOWC)]
+        times = {}
+        for cname, fl in cands:
+            wsb = B.wino_workspace_bytes(N, C, H, W, K, pad, m, fl)
+            if wsb == 2**64 - 1:
+                continue
+            if cname.startswith("fused_s"):
+                stc, a2, n2 = B.wino_plan_r(N, C, H, W, K, pad, m, 3, fl)
+                if stc != 0 or n2 <= 1:
+                    continue
+            ws = torch.empty(max(wsb // 4, 1), dtype=torch.float32, device=dev)
+            fn = (lambda sp, fl=fl, ws=ws, wsb=wsb:
+                  B.wino_conv2d(x, U, y, N, C, H, W, K, pad, m, fl, ws if wsb else None, wsb, sp))
+            times[cname] = time_us(fn)
+            del ws
+        best = min(times, key=times.get)
+        log(f"planner N={N} C={C} {H}x{W} K={K} m={m}: " +
+            " ".join(f"{k}={v:.1f}" for k, v in times.items()) + f"  best {best} auto {auto}")
+        lines.append(f"{N} {C} {H} {W} {K} {pad} {m}  " + " ".join(f"{k}={v:.1f}" for k, v in times.items())
+                     + f"  {best} {auto}")
+        del x, g, U, y
+        torch.cuda.empty_cache()
+    text = "\n".join(lines) + "\n"
+    if args.write_summary:
+        with open(PLANNER_TABLE, "w") as fh:
+            fh.write(text)
+    print(text, end="")
+
+
 def sleep_calibration(stream) -> float:
     """GPU cycles per millisecond of torch's spin kernel (torch.cuda._sleep)."""
     import torch
@@ -409,6 +537,8 @@ def main():
     ap.add_argument("--kind", default="fused", help="kernel kind the --pmc-summary covers")
     ap.add_argument("--write-summary", action="store_true",
                     help="with --pmc-summary: also write it to profiles/traffic_<workload>.txt")
+    ap.add_argument("--planner-table", action="store_true",
+                    help="time every algorithm on the planner's reference layers (profiles/planner_table.txt)")
     args = ap.parse_args()
 
     if args.pmc_summary:
@@ -419,6 +549,10 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args)
+        return
+
+    if args.planner_table:
+        planner_table(args)
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

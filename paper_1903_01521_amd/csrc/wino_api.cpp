@@ -128,8 +128,6 @@ double block_util(const Geom& g, int bw) {
     return (double)g.th * g.tw / (rows * cols);
 }
 
-long split_items(const Geom& g) { return split_tail(g).items; }
-
 // Estimated time (ns) of the fused and split algorithms: both kernels run one
 // workgroup per CU, so a launch takes ceil(items/256) rounds of one
 // workgroup's MFMA work at an efficiency measured for each kernel family on
@@ -289,9 +287,8 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
         p->algo = WINO_ALGO_LOWC;
         return WINO_OK;
     }
-    // Split path where the estimates favour it (layers with at least a full
-    // round of its workgroups).
-    if (p->automatic && g.r == 3 && !cs_req && split_items(g) >= (long)kCus && split_ns(g) < fused_ns(g, c))
+    // Split path where the estimates favour it.
+    if (p->automatic && g.r == 3 && !cs_req && split_ns(g) < fused_ns(g, c))
         p->algo = WINO_ALGO_SPLIT;
     // Channel slices over workgroups for fused layers that leave CUs idle with
     // a long channel loop each (deep layers at small batch): double the slices
