@@ -213,8 +213,9 @@ int wino_output_transform(const float* M, float* y, int N, int K, int H, int W,
  * WINO_PREC_BF16; 0 gives the fp32 calls above):
  *   UH[KB][C16][T][64][4] 16-bit values, C16 = ceil(C/16): element (t,c,k) at
  *   lane ((c%16)/4)*16 + k%16, half c%4 of group (k/16, c/16, t) -- one 8-byte
- *   word per lane, the A operand of v_mfma_f32_16x16x16 (four consecutive
- *   channels per lane).  Each value is G g G^T in fp64, rounded to fp32, then to
+ *   word per lane (four consecutive channels per lane; the words of groups
+ *   2j and 2j+1 together form a lane's A operand of v_mfma_f32_16x16x32).
+ *   Each value is G g G^T in fp64, rounded to fp32, then to
  *   the 16-bit format.  Bytes: 2*T*roundup(C,16)*roundup(K,16). */
 size_t wino_filter_bytes_p(int C, int K, int m, unsigned prec);
 int wino_filter_transform_p(const float* g, void* U, int C, int K, int m, unsigned prec, void* stream);
