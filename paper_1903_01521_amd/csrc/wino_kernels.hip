@@ -565,8 +565,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         else if constexpr (R == 1) return xs1;
         else return xs2;
     };
-    // Patch of step j -> stage j % 3 (a step past the last reads zeros into a
-    // stage nobody reads, so every step issues exactly JX loads).
+    // Patch of step j -> stage j % 3 (with KGW > 1 a step past the last reads
+    // zeros into a stage nobody reads, so every step issues exactly JX loads).
     auto issue_x = [&](auto rc, int j) {
         float* xs = xstage(rc);
         const uint32_t cbase = (uint32_t)j * step_b;
@@ -631,16 +631,23 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             else if constexpr (R == 1) return ub;
             else return uc;
         };
+        // No loads past the last step: the last step waits for everything.
         issue_x(IC<0>{}, 0);
         load_u(0, cs, ua);
-        issue_x(IC<1>{}, 1);
-        load_u(1, cs, ub);
+        if (nsteps > 1) {
+            issue_x(IC<1>{}, 1);
+            load_u(1, cs, ub);
+        }
         auto step = [&](auto rc, int s) {  // s % 3 == R
             constexpr int R = decltype(rc)::value;
-            wait_vm_lds<WAITN>();          // patch and filters of step s have landed (for this wave)
+            // patch and filters of step s have landed (for this wave)
+            if (s + 1 < nsteps) wait_vm_lds<WAITN>();
+            else wait_vm_lds<0>();
             wg_barrier();                  // ... for every wave; step s-1 is fully consumed
-            issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
-            load_u(s + 2, cs, uring(IC<(R + 2) % 3>{}));
+            if (s + 2 < nsteps) {
+                issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
+                load_u(s + 2, cs, uring(IC<(R + 2) % 3>{}));
+            }
             __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's work
             float v[TH];
             transform(IC<R>{}, v);
