@@ -644,14 +644,15 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             if (s + 1 < nsteps) wait_vm_lds<WAITN>();
             else wait_vm_lds<0>();
             wg_barrier();                  // ... for every wave; step s-1 is fully consumed
-            if (s + 2 < nsteps) {
-                issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
-                load_u(s + 2, cs, uring(IC<(R + 2) % 3>{}));
-            }
+            // The patch DMA goes out first; the filters of step s+2 only after this
+            // step's MFMAs, so the two bursts do not queue together at the step start.
+            if (s + 2 < nsteps) issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
             __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of this step's work
             float v[TH];
             transform(IC<R>{}, v);
             mfma_quad(v, uring(IC<R>{}));
+            __builtin_amdgcn_sched_barrier(0);
+            if (s + 2 < nsteps) load_u(s + 2, cs, uring(IC<(R + 2) % 3>{}));
         };
         int s = 0;
         for (; s + 3 <= nsteps; s += 3) {   // straight-line body: exact wait analysis
