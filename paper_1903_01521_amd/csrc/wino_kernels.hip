@@ -539,6 +539,15 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 
 template <int R> using IC = std::integral_constant<int, R>;
 
+// f(IC<I>) for I = I0 .. I1-1, in order.
+template <int I0, int I1, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I0 < I1) {
+        f(IC<I0>{});
+        static_for<I0 + 1, I1>(f);
+    }
+}
+
 // f(IC<v>) for the runtime value v in [0, N) (wave-uniform): one instance per value.
 template <typename F, int... I>
 __device__ __forceinline__ void with_ic(int v, F&& f, std::integer_sequence<int, I...>) {
@@ -1312,17 +1321,27 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
     // DMA loads i0 .. i1-1 (of JV) of step j's V into stage rc.  Unit e =
     // i*512 + tid of the stage is unit e of block 0's run or unit e - JV*256 of
     // block 1's; the padding quads of Vb are zeros, so no unit needs a mask.
+    // The lane part of a unit's offset is tid16 (one register); the rest is
+    // wave-uniform and goes into the scalar offset.  Only the load that
+    // straddles the two runs needs a per-lane correction.
     const uint32_t tid16 = ((uint32_t)wave * 64 + lane) * 16u;
     auto issue_v = [&](auto rc, int j, auto i0c, auto i1c) {
         float* vs = stage(rc);
         const uint32_t qoff = (uint32_t)j * NQ * T * 256;       // bytes: NQ quads of T*64 floats
-#pragma unroll
-        for (int i = decltype(i0c)::value; i < decltype(i1c)::value; ++i) {
-            constexpr int RUN = S::JV * 256 * 16;                // bytes of one block's run
-            const uint32_t e16 = (uint32_t)i * 8192u + tid16;   // byte offset of the unit in the stage
-            const uint32_t off = e16 < (uint32_t)RUN ? vbase0 + e16 : vbase1 + (e16 - RUN);
-            lds_dma<16>(vr, vs + (i * 512 + wave * 64) * 4, off + qoff);
-        }
+        static_for<decltype(i0c)::value, decltype(i1c)::value>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr uint32_t RUN = S::JV * 256 * 16;           // bytes of one block's run
+            constexpr uint32_t E0 = (uint32_t)i * 8192u;         // the unit's stage offset is E0 + tid16
+            float* dst = vs + (i * 512 + wave * 64) * 4;
+            if constexpr (E0 + 8192u <= RUN) {
+                lds_dma<16>(vr, dst, tid16, vbase0 + E0 + qoff);
+            } else if constexpr (E0 >= RUN) {
+                lds_dma<16>(vr, dst, tid16, vbase1 + (E0 - RUN) + qoff);
+            } else {
+                const uint32_t voff = tid16 < RUN - E0 ? tid16 : tid16 + (vbase1 - vbase0 - RUN);
+                lds_dma<16>(vr, dst, voff, vbase0 + E0 + qoff);
+            }
+        });
     };
     const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
     const uint32_t ulane = (uint32_t)lane * 16u;
