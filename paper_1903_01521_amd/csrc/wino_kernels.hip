@@ -489,7 +489,19 @@ struct FusedShape {
     static constexpr int XS = 4 * QS * PR * PCP;           // patch floats per step
     static constexpr int JX = (XS / EW + 511) / 512;       // patch loads per thread per step
     static constexpr int XSP = JX * 512 * EW;
-    static constexpr int XST = XSP + 4 * VEC;              // floats of one patch stage
+    // PRIV (one filter block per workgroup, row blocks, 16-byte loads, one row
+    // group): each wave loads its own quad's patch into a region of its own, so
+    // the channel loop needs no workgroup barrier (F(2x2,3x3) on the N=1
+    // 32-channel 56x56 layer: 4.99 -> 4.86 us).  With two row groups a wave
+    // would need PRW = 5 of the 6 region rows (Bt rows 0-2 use region rows
+    // 0-4, rows 3-5 use 1-5), 1.7x the shared patch bytes, and that cost what
+    // the barriers did (10.05 against 10.12 us on the N=1 64-channel layer).
+    static constexpr bool PRIV = !SHARE && BH == 1 && VEC && TS == 1;
+    static constexpr int XW = 4 * A * PCP;                 // floats of a wave's patch (PRIV)
+    static constexpr int JXW = (XW / EW + 63) / 64;        // its loads per lane per step
+    static constexpr int XSTW = JXW * 64 * EW + 4 * VEC;   // floats of a wave's stage region
+    static constexpr int NJ = PRIV ? JXW : JX;             // patch loads per lane per step
+    static constexpr int XST = PRIV ? 8 * XSTW : XSP + 4 * VEC;   // floats of one patch stage
     static constexpr int VSZ = TS * QS * TH * 64;          // floats of one transform stage
     // Epilogue.  Channel sum: value f = r*TH + t of a lane (filter slot r,
     // position t of its row group) goes to wave f / V1 of the CS channel parts;
@@ -556,7 +568,7 @@ __device__ __forceinline__ void with_ic(int v, F&& f, std::integer_sequence<int,
 
 template <int MT, int TS, int CS, int BW, int VEC, int H, int RF>
 __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
-                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW, VEC, RF>::JX],
+                                            const uint32_t (&xoff)[FusedShape<MT, TS, CS, BW, VEC, RF>::NJ],
                                             uint32_t step_b, const float* __restrict__ U, const Geom& g,
                                             const FusedTiling& ft, int kb, int wave, int lane, int kw, int cs,
                                             int bi, int bj, float* xs0, float* xs1, float* xs2, float* vs,
@@ -579,10 +591,17 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
     auto issue_x = [&](auto rc, int j) {
         float* xs = xstage(rc);
         const uint32_t cbase = (uint32_t)j * step_b;
+        if constexpr (S::PRIV) {
 #pragma unroll
-        for (int i = 0; i < S::JX; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + xlo + (i * 512 + wave * 64) * S::EW, 4 * S::EW,
-                                                     xoff[i] + cbase, 0, 0, 0);
+            for (int i = 0; i < S::JXW; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + wave * S::XSTW + xlo + i * 64 * S::EW, 4 * S::EW,
+                                                         xoff[i] + cbase, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < S::JX; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, xs + xlo + (i * 512 + wave * 64) * S::EW, 4 * S::EW,
+                                                         xoff[i] + cbase, 0, 0, 0);
+        }
     };
     // Filters of (step j, quad slot q) of the channel slice [cq0, cq0 + cqn): a
     // quad past the slice repeats a valid block (it meets zero regions, the
@@ -599,7 +618,8 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         // VEC: the patch's first column sits 4 floats in (or at 0 when the
         // chunks start on it), so region rows stay 16-byte aligned (8-byte
         // aligned for m = 2).
-        const float* wp = xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT + (xlo ? 4 : 0);
+        const float* wp = S::PRIV ? xstage(rc) + wave * S::XSTW + cl * A * S::PCP + bj * MT + (xlo ? 4 : 0)
+                                  : xstage(rc) + ((jt * 4 + cl) * S::PR + bi * MT) * S::PCP + bj * MT + (xlo ? 4 : 0);
         float d[A][A];
 #pragma unroll
         for (int u = 0; u < A; ++u) {
@@ -632,7 +652,7 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
         // Step s: transform quad cs of step s (patch landed two steps ago), one
         // quad of MFMAs.  Filters also come two steps ahead, into a ring of three
         // register sets that follows the three patch stages.
-        constexpr int WAITN = S::JX + NG;     // loads issued in the previous step
+        constexpr int WAITN = S::NJ + NG;     // loads issued in the previous step
         f32x4 uc[NG];
         auto uring = [&](auto rc) -> f32x4 (&)[NG] {
             constexpr int R = decltype(rc)::value % 3;
@@ -652,7 +672,9 @@ __device__ __forceinline__ void fused_steps(const __amdgpu_buffer_rsrc_t xr,
             // patch and filters of step s have landed (for this wave)
             if (s + 1 < nsteps) wait_vm_lds<WAITN>();
             else wait_vm_lds<0>();
-            wg_barrier();                  // ... for every wave; step s-1 is fully consumed
+            // ... for every wave; step s-1 is fully consumed (PRIV: the wave's
+            // own loads are all it reads)
+            if constexpr (!S::PRIV) wg_barrier();
             // The patch DMA goes out first; the filters of step s+2 only after this
             // step's MFMAs, so the two bursts do not queue together at the step start.
             if (s + 2 < nsteps) issue_x(IC<(R + 2) % 3>{}, s + 2);   // that stage held step s-1's patch
@@ -830,17 +852,32 @@ __global__ __launch_bounds__(512) void k_fused(const float* __restrict__ x, cons
     // patch's first column (xsh floats into its chunk) on a 16-byte boundary.
     const int xsh = VEC ? (4 - g.pad % 4) % 4 : 0, xlo = (4 - xsh) % 4;
     const int row0 = ti0 * MT - g.pad, col0 = tj0 * MT - g.pad - xsh;
-    uint32_t xoff[S::JX];
+    uint32_t xoff[S::NJ];
+    if constexpr (S::PRIV) {
+        // load e = j*64 + lane of the wave's [4 channels of its quad][A rows][NE]
 #pragma unroll
-    for (int j = 0; j < S::JX; ++j) {
-        const int e = j * 512 + tid;
-        const int ch = e / (S::PR * S::NE), rem = e - ch * (S::PR * S::NE);
-        const int r = rem / S::NE, c = (rem - r * S::NE) * S::EW;
-        const int row = row0 + r, col = col0 + c;
-        const bool ok = (e * S::EW < S::XS) & (VEC || c < S::PC) & ((unsigned)row < (unsigned)g.H) &
-                        ((unsigned)col < (unsigned)g.W);
-        const uint32_t off = (uint32_t)ch * plane_b + ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u;
-        xoff[j] = ok ? off : kInvalid;
+        for (int j = 0; j < S::JXW; ++j) {
+            const int e = j * 64 + lane;
+            const int ch = e / (S::A * S::NE), rem = e - ch * (S::A * S::NE);
+            const int r = rem / S::NE, c = (rem - r * S::NE) * S::EW;
+            const int row = row0 + r, col = col0 + c;
+            const bool ok = (e * S::EW < S::XW) & ((unsigned)row < (unsigned)g.H) & ((unsigned)col < (unsigned)g.W);
+            const uint32_t off =
+                (uint32_t)((kw * CS + cs) * 4 + ch) * plane_b + ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u;
+            xoff[j] = ok ? off : kInvalid;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < S::JX; ++j) {
+            const int e = j * 512 + tid;
+            const int ch = e / (S::PR * S::NE), rem = e - ch * (S::PR * S::NE);
+            const int r = rem / S::NE, c = (rem - r * S::NE) * S::EW;
+            const int row = row0 + r, col = col0 + c;
+            const bool ok = (e * S::EW < S::XS) & (VEC || c < S::PC) & ((unsigned)row < (unsigned)g.H) &
+                            ((unsigned)col < (unsigned)g.W);
+            const uint32_t off = (uint32_t)ch * plane_b + ((uint32_t)row * (uint32_t)g.W + (uint32_t)col) * 4u;
+            xoff[j] = ok ? off : kInvalid;
+        }
     }
     const uint32_t step_b = 4u * S::QS * plane_b;
 
