@@ -54,7 +54,8 @@ PROFILES = os.path.join(HERE, "profiles")
 AXIS = {"w": 1, "h": 2}   # WINO_AXIS_W, WINO_AXIS_H
 
 KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", "lowc": "void wino::k_lowc",
-                "input": "void wino::k_input", "gemm": "void wino::k_gemm",
+                # the staged input transform: by tile rows, or by tiles for very wide images
+                "input": "void wino::k_vrows|void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
                 "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
                 "gemm16": "void wino::k_gemm16",
@@ -426,7 +427,7 @@ def planner_table(args):
              "# (fused: the planner's fused variant without channel slices; fused_sN: with N slices;",
              "# split; staged; lowc), the fastest, and AUTO's choice (wino_plan_r) when taken.",
              "# one MI355X; command (on the GPU host, from the repository root):",
-             "#   python3 bench.py --planner-table",
+             "#   python3 bench.py --planner-table --write-summary",
              f"sources_sha256: {sources_hash()}",
              "N C H W K pad m  times...  best auto"]
 
