@@ -465,8 +465,8 @@ __global__ __launch_bounds__(256) void k_output(const float* __restrict__ M, flo
 // that are distinct LDS objects, so the compiler can see that reading one stage
 // never waits for loads still landing in another.  Rows, columns and channels
 // outside the image and the alignment columns are offsets past the buffer
-// record and read as 0.  Filters go straight to registers, one quad ahead (no
-// other wave uses them), one 16-byte load per 4 positions.  The region's input
+// record and read as 0.  Filters go straight to registers ahead of their use
+// (no other wave uses them), one 16-byte load per 4 positions.  The region's input
 // transform gives exactly the B operand of v_mfma_f32_16x16x4_f32.  At the end
 // the CS channel parts of a (filter block, row group) first sum their
 // accumulators through LDS, each wave keeping a 1/CS share of the (filter,
@@ -493,9 +493,9 @@ struct FusedShape {
     // group): each wave loads its own quad's patch into a region of its own, so
     // the channel loop needs no workgroup barrier (F(2x2,3x3) on the N=1
     // 32-channel 56x56 layer: 4.99 -> 4.86 us).  With two row groups a wave
-    // would need PRW = 5 of the 6 region rows (Bt rows 0-2 use region rows
-    // 0-4, rows 3-5 use 1-5), 1.7x the shared patch bytes, and that cost what
-    // the barriers did (10.05 against 10.12 us on the N=1 64-channel layer).
+    // would need 5 of the 6 region rows (Bt rows 0-2 use region rows 0-4,
+    // rows 3-5 use 1-5), 1.7x the shared patch bytes, and that cost what the
+    // barriers did (10.05 against 10.12 us on the N=1 64-channel layer).
     static constexpr bool PRIV = !SHARE && BH == 1 && VEC && TS == 1;
     static constexpr int XW = 4 * A * PCP;                 // floats of a wave's patch (PRIV)
     static constexpr int JXW = (XW / EW + 63) / 64;        // its loads per lane per step

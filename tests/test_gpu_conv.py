@@ -180,12 +180,15 @@ def test_batch_independence_and_pad_invariance(m):
 
 
 @pytest.mark.parametrize("m", [2, 4])
-@pytest.mark.parametrize("shape", [(1, 12, 16, 16, 20, 1), (2, 8, 10, 24, 16, 2), (1, 20, 9, 12, 24, 0)],
+@pytest.mark.parametrize("shape", [(1, 12, 16, 16, 20, 1), (2, 8, 10, 24, 16, 2), (1, 20, 9, 12, 24, 0),
+                                   (2, 100, 18, 64, 24, 1)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_patch_load_paths_agree(m, shape):
     # With W % 4 == 0 and a 16-byte aligned input the fused kernel loads its
     # patches in 16-byte chunks; an input one float off that alignment takes the
     # one-float path.  Both feed the same arithmetic: bit-identical outputs.
+    # The 100-channel case runs several channel steps through the per-wave
+    # patch regions of the one-row-group F(2x2,3x3) variants (1x16 blocks).
     N, C, H, W, K, pad = shape
     rng = np.random.default_rng(sum(shape) + 17 * m)
     x, g = wl.random_layer(rng, N, C, H, W, K)
