@@ -62,6 +62,9 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 # the split path's call: the input transform (by tile rows, or by 16-tile
                 # patches for very wide images), then the GEMMs with the output transform
                 "split": ("void wino::k_vrows|void wino::k_vblk", "void wino::k_gemm_out"),
+                # the same on channel-last tensors: the NHWC input transform into the
+                # blocked V, then the GEMMs storing y channel-last
+                "split_nhwc": ("void wino::k_input_nhwc", "void wino::k_gemm_out"),
                 # the fused kernel over channel slices, then the sum of the slices
                 "fused_sliced": ("void wino::k_fused", "void wino::k_slice_sum")}
 
@@ -110,6 +113,7 @@ def layer_numbers(N, L):
         "fused": x_b + u_b + y_b,
         "fused_sliced": x_b + u_b + y_b,
         "split": x_b + u_b + y_b,
+        "split_nhwc": x_b + u_b + y_b,
         "lowc": x_b + u_b + y_b,
         "input": x_b + v_b,
         "gemm": v_b + u_b + m_b,
@@ -123,7 +127,7 @@ def layer_numbers(N, L):
         "gemm16": v_b // 2 + u_b // 2 + m_b,
     }
     f["flops"] = {"fused": f["gemm_flops"], "fused_sliced": f["gemm_flops"], "split": f["gemm_flops"],
-                  "gemm": f["gemm_flops"],
+                  "split_nhwc": f["gemm_flops"], "gemm": f["gemm_flops"],
                   "stages": f["gemm_flops"],
                   "stages16": f["gemm_flops"], "gemm16": f["gemm_flops"]}
     return f
@@ -149,7 +153,7 @@ def roofline(kind, nums, seconds):
 def traffic_file(workload: str, kind: str) -> str:
     """Counter summary of a workload's convolution kernel (fused, low-C), or of
     one stage of its staged path (input, gemm, output)."""
-    if kind in ("fused", "fused_sliced", "split", "lowc"):
+    if kind in ("fused", "fused_sliced", "split", "split_nhwc", "lowc"):
         return os.path.join(PROFILES, f"traffic_{workload}.txt")
     return os.path.join(PROFILES, f"traffic_{workload}_{kind}.txt")
 
@@ -632,11 +636,15 @@ def main():
         a = hx
         for i, L in enumerate(w.layers):
             relu = B.WINO_FLAG_RELU if L.relu else 0
-            if L.nhwc:                     # channel-last layer: the three stages in one call
+            if L.nhwc:                     # channel-last layer: split, or the three stages, in one call
                 ws, wsb = wss[i]
                 out.append((f"L{i}.filter", i, "filter", (lambda sp, i=i, L=L: B.wino_filter_transform(
                     hg[i], Us[i], L.C, L.K, L.m, sp))))
-                out.append((f"L{i}.conv", i, "stages", (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
+                # the plan's workspace tells which: the split path's blocked V, or V and M
+                split_wsb = B.wino_workspace_bytes_nhwc(N, L.C, L.H, L.W, L.K, L.pad, L.m,
+                                                        (flags & ~B.WINO_ALGO_MASK) | B.WINO_ALGO_SPLIT)
+                kind = "split_nhwc" if wsb == split_wsb and (flags & B.WINO_ALGO_MASK) != B.WINO_ALGO_STAGED else "stages"
+                out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                          B.wino_conv2d_nhwc(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                             L.pad, L.m, flags | relu, ws, wsb, sp))))
                 a = ys[i]

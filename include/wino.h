@@ -283,9 +283,14 @@ int wino_conv2d_1d(const float* x, const float* U, float* y,
 /* ---- channel-last tensors ---------------------------------------------------
  * The 3x3 layer of wino_conv2d with x as [N][H][W][C] and y as [N][Ho][Wo][K]
  * (NHWC, the layout the paper chooses for its channel-vectorised transforms,
- * Sec. 2.1).  U comes from wino_filter_transform as before; the three stages
- * run through the workspace (flags: WINO_ALGO_AUTO or _STAGED, and
- * WINO_FLAG_RELU).  Errors as for wino_conv2d. */
+ * Sec. 2.1).  U comes from wino_filter_transform as before.  Flags:
+ * WINO_ALGO_STAGED runs the three stages through the workspace (V and M);
+ * WINO_ALGO_SPLIT the split path (input transform into the tile-blocked V
+ * workspace, then GEMMs with the output transform storing y channel-last);
+ * WINO_ALGO_AUTO takes split on layers with at least two rounds of its work
+ * items on the CUs (e.g. N=64, 256 channels, 56x56), else the three stages;
+ * and WINO_FLAG_RELU.  wino_workspace_bytes_nhwc gives the workspace of the
+ * plan the flags choose.  Errors as for wino_conv2d. */
 size_t wino_workspace_bytes_nhwc(int N, int C, int H, int W, int K, int pad, int m, unsigned flags);
 int wino_conv2d_nhwc(const float* x, const float* U, float* y,
                      int N, int C, int H, int W, int K, int pad, int m,

@@ -235,19 +235,27 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     if (algo == WINO_ALGO_LOWC && g.C > 4) return WINO_ERR_UNSUPPORTED;
     const unsigned blk = flags & kBlockMask;
     // 1-D filters, channel-last tensors and 16-bit operands run the three
-    // stages (input transform, GEMMs, output transform); of the one-kernel
-    // variants, the fused kernel also takes 5x5 filters of NCHW tensors, the
-    // split and low-channel ones only 3x3.
+    // stages (input transform, GEMMs, output transform); channel-last 3x3
+    // layers also the split path (its GEMM kernel stores y channel-last).  Of
+    // the other one-kernel variants, the fused kernel also takes 5x5 filters
+    // of NCHW tensors, the split and low-channel ones only 3x3.
     const int prec = prec_of(flags);
     if (prec < 0) return WINO_ERR_UNSUPPORTED;
     if (prec && (g.r != 3 || g.axis != 0 || g.nhwc)) return WINO_ERR_UNSUPPORTED;
     if (g.axis != 0 || g.nhwc || prec) {
-        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED) || blk || (flags >> kCsplitShift) & 0xF ||
-            (flags >> kSliceShift) & 0xF)
+        const bool nhwc_split = g.nhwc && g.axis == 0 && g.r == 3 && !prec &&
+                                (int64_t)g.KB * g.CQ * g.T * 256 <= 0x7fffffffLL;
+        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED && !(algo == WINO_ALGO_SPLIT && nhwc_split)) ||
+            blk || (flags >> kCsplitShift) & 0xF || (flags >> kSliceShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
-        p->algo = WINO_ALGO_STAGED;
         p->automatic = algo == WINO_ALGO_AUTO;
         p->cfg = FusedCfg{1, 16, 1};
+        // AUTO: split on layers with at least two full rounds of its items
+        // (tile-block pair x filter group) on the CUs, where the saved M round
+        // trip outweighs its per-item prologue and epilogue.
+        p->algo = algo == WINO_ALGO_SPLIT || (p->automatic && nhwc_split && split_tail(g).items >= 2 * kSplitCus)
+                      ? WINO_ALGO_SPLIT
+                      : WINO_ALGO_STAGED;
         return WINO_OK;
     }
     if (blk == kBlockMask) return WINO_ERR_UNSUPPORTED;
@@ -626,6 +634,7 @@ size_t wino_workspace_bytes_nhwc(int N, int C, int H, int W, int K, int pad, int
     if (make_geom(N, C, H, W, K, pad, m, &g) != WINO_OK) return (size_t)-1;
     g.nhwc = 1;
     if (make_plan(g, flags, &p) != WINO_OK) return (size_t)-1;
+    if (p.algo == WINO_ALGO_SPLIT) return split_workspace(g);
     return round_up(v_elems(g) * sizeof(float), 256) + m_elems(g) * sizeof(float);
 }
 
@@ -643,12 +652,19 @@ int wino_conv2d_nhwc(const float* x, const float* U, float* y, int N, int C, int
     const size_t yb = (size_t)N * K * g.Ho * g.Wo * sizeof(float);
     const size_t ub = wino_filter_bytes(C, K, m);
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    if (p.algo == WINO_ALGO_SPLIT) {
+        const size_t need = split_workspace(g);
+        if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+        if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+            return WINO_ERR_INVALID_ARG;
+        return hip_status(launch_split(x, U, y, (float*)workspace, g, 16, (flags & WINO_FLAG_RELU) != 0, s));
+    }
     const size_t vb = round_up(v_elems(g) * sizeof(float), 256);
     const size_t need = vb + m_elems(g) * sizeof(float);
     if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
     if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
         return WINO_ERR_INVALID_ARG;
-    hipStream_t s = (hipStream_t)stream;
     float* V = (float*)workspace;
     float* M = (float*)((char*)workspace + vb);
     st = hip_status(launch_input_transform(x, V, g, s));

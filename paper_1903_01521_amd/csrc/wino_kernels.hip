@@ -188,6 +188,33 @@ __device__ __forceinline__ void store_block(float* __restrict__ y, const Geom& g
     for (int i = 0; i < MT; ++i) store_row<MT, NT>(y, g, tc, k, i, o[i], relu, vec_ok);
 }
 
+// Channel-last y [N][Ho][Wo][K]: the m x m outputs of (tile tc, output channels
+// k0 .. k0+3), cropped to Ho x Wo and K; one 16-byte store per pixel when vec
+// (K % 4 == 0 and y 16-byte aligned).
+template <int MT>
+__device__ __forceinline__ void store_tile_nhwc(float* __restrict__ y, const Geom& g, const TileCoord& tc, int k0,
+                                                const float (&o)[4][MT][MT], bool relu, bool vec) {
+    if (!tc.valid || k0 >= g.K) return;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            const int oi = tc.ti * MT + i, oj = tc.tj * MT + j;
+            if (oi >= g.Ho || oj >= g.Wo) continue;
+            float* py = y + (((size_t)tc.n * g.Ho + oi) * g.Wo + oj) * g.K + k0;
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = relu ? fmaxf(o[r][i][j], 0.0f) : o[r][i][j];
+            if (vec && k0 + 4 <= g.K) {
+                *(float4*)py = make_float4(v[0], v[1], v[2], v[3]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (k0 + r < g.K) py[r] = v[r];
+            }
+        }
+}
+
 // Store a lane's T transform-domain values into one (block, quad) group of the
 // U/V layout [T/4][64][4]: one 16-byte store per group of four positions, the
 // wave writing whole 1 KiB runs.  NT: streaming stores (measured: faster for
@@ -1569,7 +1596,18 @@ __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, cons
         float row[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) row[j] = sum[ii * MT + j];
-        store_row<MT>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
+        if (g.nhwc) {                   // channel-last: one value per pixel
+            const int oi = tc.ti * MT + i0 + ii;
+            if (tc.valid && k < g.K && oi < g.Ho)
+#pragma unroll
+                for (int j = 0; j < MT; ++j) {
+                    const int oj = tc.tj * MT + j;
+                    if (oj < g.Wo)
+                        y[(((size_t)tc.n * g.Ho + oi) * g.Wo + oj) * g.K + k] = relu ? fmaxf(row[j], 0.0f) : row[j];
+                }
+        } else {
+            store_row<MT>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
+        }
     }
 }
 
@@ -1652,8 +1690,12 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb) {
             const TileCoord tc = tile_of(bb);
+            if (g.nhwc) {
+                store_tile_nhwc<MT>(y, g, tc, kbase, o[bb], rl, vo);
+            } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+                for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+            }
         }
     } else {
         // Row half h of filter block kw sums tile block h (its own share plus
@@ -1693,14 +1735,18 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
                         for (int j = 0; j < MT; ++j) sl[r][i][j] = slot[((r * MT + i) * MT + j) * 64];
             });
             const TileCoord tc = tile_of(bb);
+            float ob[4][MT][MT];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float ob[MT][MT];
+            for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
 #pragma unroll
-                    for (int j = 0; j < MT; ++j) ob[i][j] = o[bb][r][i][j] + sl[r][i][j];
-                store_block<MT>(y, g, tc, kbase + r, ob, rl, vo);
+                    for (int j = 0; j < MT; ++j) ob[r][i][j] = o[bb][r][i][j] + sl[r][i][j];
+            if (g.nhwc) {
+                store_tile_nhwc<MT>(y, g, tc, kbase, ob, rl, vo);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, ob[r], rl, vo);
             }
         }
     }
@@ -2115,15 +2161,16 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
 // output pixel is one 16-byte store.
 template <int MT>
 __global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x, float* __restrict__ V, Geom g,
-                                                    long nwg) {
+                                                    long nwg, int nq) {
     constexpr int A = MT + 2, T = A * A;
     const int lane = threadIdx.x & 63;
     const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (item >= nwg) return;
     const long w = item * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (w >= (long)g.PB * g.CQ) return;
-    // channel quad fastest: the waves reading one pixel's C channels run together
-    const int pb = (int)(w / g.CQ), cq = (int)(w % g.CQ);
+    if (w >= (long)g.PB * nq) return;
+    // channel quad fastest: the waves reading one pixel's C channels run together;
+    // nq quads per block in V (quads past CQ are zeros)
+    const int pb = (int)(w / nq), cq = (int)(w % nq);
     const TileCoord tc = decode_tile(pb * 16 + (lane & 15), g);
     const int c = cq * 4 + (lane >> 4);
     const bool ok = tc.valid && c < g.C;
@@ -2140,7 +2187,7 @@ __global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x,
         }
     float vv[T];
     input_tf<MT>(d, vv);
-    store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, vv);
+    store_t4<T, true>(V + ((size_t)pb * nq + cq) * T * 64, lane, vv);
 }
 
 // With C % 4 == 0 a channel quad of a pixel is one aligned 16-byte word: one
@@ -2153,7 +2200,7 @@ __global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x,
 // outside the image and quads past CQ read as zero.
 template <int MT>
 __global__ __launch_bounds__(256) void k_input_nhwc4(const float* __restrict__ x, float* __restrict__ V, Geom g,
-                                                     int CG, long nwg) {
+                                                     int CG, long nwg, int nq) {
     constexpr int A = MT + 2, T = A * A;
     const int lane = threadIdx.x & 63;
     const long per = (nwg + 7) / 8, item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
@@ -2182,8 +2229,10 @@ __global__ __launch_bounds__(256) void k_input_nhwc4(const float* __restrict__ x
             const uint32_t off = in ? base + ((uint32_t)row * g.W + (uint32_t)col) * (uint32_t)g.C * 4u : kInvalid;
             d4[u][v] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
         }
-    if (cq >= g.CQ) return;
-    float* blk = V + ((size_t)pb * g.CQ + cq) * T * 64;
+    // nq quads per block in V: CQ (three stages) or CQ rounded up to 4 (the
+    // split path's blocked V, whose padding quads get the zeros read above)
+    if (cq >= nq) return;
+    float* blk = V + ((size_t)pb * nq + cq) * T * 64;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         float d[A][A];
@@ -2218,27 +2267,7 @@ __global__ __launch_bounds__(256) void k_output_nhwc(const float* __restrict__ M
         for (int t = 0; t < T; ++t) m1[t] = mv[t][r];
         output_tf<MT>(m1, o[r]);
     }
-    if (!tc.valid) return;
-    const int k0 = kb * 16 + 4 * (lane >> 4);
-    if (k0 >= g.K) return;
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < MT; ++j) {
-            const int oi = tc.ti * MT + i, oj = tc.tj * MT + j;
-            if (oi >= g.Ho || oj >= g.Wo) continue;
-            float* py = y + (((size_t)tc.n * g.Ho + oi) * g.Wo + oj) * g.K + k0;
-            float v[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = relu ? fmaxf(o[r][i][j], 0.0f) : o[r][i][j];
-            if (vec_ok && k0 + 4 <= g.K) {
-                *(float4*)py = make_float4(v[0], v[1], v[2], v[3]);
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (k0 + r < g.K) py[r] = v[r];
-            }
-        }
+    store_tile_nhwc<MT>(y, g, tc, kb * 16 + 4 * (lane >> 4), o, relu != 0, vec_ok != 0);
 }
 
 // ------------------------------------------------------------------ 1-D
@@ -2420,30 +2449,37 @@ hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int 
     return hipGetLastError();
 }
 
+// Channel-last input transform into V blocks of nq quads ([PB][nq][T/4][64][4]:
+// nq = CQ for the three stages, CQ rounded up to 4 for the split path).
+static hipError_t launch_input_nhwc(const float* x, float* V, const Geom& g, int nq, hipStream_t s) {
+    const long waves = (long)g.PB * nq, nwg = (waves + 3) / 4;
+    if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
+    // 16-byte channel-quad loads when the quads are aligned and the 32-bit
+    // offsets of the images one tile block spans (at most 16 / (th*tw) + 2)
+    // stay below kInvalid
+    const size_t img_b = (size_t)g.H * g.W * g.C * 4;
+    const size_t span = (size_t)(16 / (g.th * g.tw) + 2);
+    if (g.C % 4 == 0 && aligned(x, 16) && span * img_b < (size_t)kInvalid) {
+        const int CG = (nq + 3) / 4;
+        const long nwg4 = ((long)g.PB * CG + 3) / 4;
+        const dim3 grid4((unsigned)((nwg4 + 7) / 8 * 8));
+        if (g.m == 2) hipLaunchKernelGGL(k_input_nhwc4<2>, grid4, block, 0, s, x, V, g, CG, nwg4, nq);
+        else hipLaunchKernelGGL(k_input_nhwc4<4>, grid4, block, 0, s, x, V, g, CG, nwg4, nq);
+    } else if (g.m == 2) {
+        hipLaunchKernelGGL(k_input_nhwc<2>, grid, block, 0, s, x, V, g, nwg, nq);
+    } else {
+        hipLaunchKernelGGL(k_input_nhwc<4>, grid, block, 0, s, x, V, g, nwg, nq);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipStream_t s) {
     if (g.axis != 0) return launch_input_1d(x, V, g, s);
+    if (g.nhwc) return launch_input_nhwc(x, V, g, g.CQ, s);
     const long waves = (long)g.PB * g.CQ, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
-    if (g.nhwc) {
-        // 16-byte channel-quad loads when the quads are aligned and the 32-bit
-        // offsets of the images one tile block spans (at most 16 / (th*tw) + 2)
-        // stay below kInvalid
-        const size_t img_b = (size_t)g.H * g.W * g.C * 4;
-        const size_t span = (size_t)(16 / (g.th * g.tw) + 2);
-        if (g.C % 4 == 0 && aligned(x, 16) && span * img_b < (size_t)kInvalid) {
-            const int CG = (g.CQ + 3) / 4;
-            const long nwg4 = ((long)g.PB * CG + 3) / 4;
-            const dim3 grid4((unsigned)((nwg4 + 7) / 8 * 8));
-            if (g.m == 2) hipLaunchKernelGGL(k_input_nhwc4<2>, grid4, block, 0, s, x, V, g, CG, nwg4);
-            else hipLaunchKernelGGL(k_input_nhwc4<4>, grid4, block, 0, s, x, V, g, CG, nwg4);
-        } else if (g.m == 2) {
-            hipLaunchKernelGGL(k_input_nhwc<2>, grid, block, 0, s, x, V, g, nwg);
-        } else {
-            hipLaunchKernelGGL(k_input_nhwc<4>, grid, block, 0, s, x, V, g, nwg);
-        }
-        return hipGetLastError();
-    }
     if (g.r == 3) {
         // by whole tile rows where the rows' patches fit LDS (the split path's kernel)
         const int vec = g.W % 4 == 0 && aligned(x, 16);
@@ -2707,7 +2743,11 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
     const int ntb = g.N * ft.nbh * ft.nbw;      // 16-tile patches of the input transform
     const int nb = (int)split_blocks(g);        // 16-tile blocks of Vb and the GEMMs
     const int ncq4 = (g.CQ + 3) / 4;
-    {
+    if (g.nhwc) {
+        // channel-last x: the three stages' input transform, into blocks of CQ4 quads
+        const hipError_t e = launch_input_nhwc(x, Vb, g, 4 * ncq4, s);
+        if (e != hipSuccess) return e;
+    } else {
         const int vec = g.W % 4 == 0 && aligned(x, 16);
         const VrowsPlan vp = vrows_plan(g, vec);
         if (vp.R > 0) {
@@ -2736,7 +2776,8 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
         ft.kfast = tile_major < group_major ? 1 : 0;
     }
     const dim3 grid((unsigned)(8 * ft.per + st.tail * st.units)), block(512);
-    const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
+    // 16-byte output stores: whole m-wide rows (NCHW) or four channels of a pixel (NHWC)
+    const int vec_ok = g.nhwc ? (g.K % 4 == 0 && aligned(y, 16)) : ((g.Wo % MT == 0) && aligned(y, 4 * MT));
     hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, nb, (int)relu, vec_ok,
                        (int)st.tail);
     return hipGetLastError();

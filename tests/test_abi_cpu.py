@@ -201,6 +201,19 @@ def test_nhwc_entry_points():
     assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, 0) == staged
     assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_FUSED) == 2**64 - 1
     assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 3, 0) == 2**64 - 1
+    # the split path on channel-last tensors: its blocked V, as for NCHW
+    split = B.wino_workspace_bytes(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_SPLIT)
+    assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_SPLIT) == split
+    # AUTO: the three stages below two rounds of split items (here 25 pairs x 1
+    # filter group), split at N=64, C=K=256, 56x56 (784 pairs x 4 groups)
+    assert B.wino_workspace_bytes_nhwc(1, 64, 112, 112, 64, 1, 4, B.WINO_ALGO_AUTO) == staged
+    big_split = B.wino_workspace_bytes(64, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_SPLIT)
+    assert B.wino_workspace_bytes_nhwc(64, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_AUTO) == big_split
+    assert B.wino_workspace_bytes_nhwc(64, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_STAGED) == \
+        B.wino_workspace_bytes(64, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_STAGED)
+    # no variant overrides or channel slices on channel-last tensors
+    assert B.wino_workspace_bytes_nhwc(64, 256, 56, 56, 256, 1, 4,
+                                       B.WINO_ALGO_SPLIT | B.WINO_BLOCK_4x4) == 2**64 - 1
     y = FAKE + 0x100000
     conv = lambda **kw: B.wino_conv2d_nhwc(kw.get("x", FAKE), FAKE + 0x800000, kw.get("y", y), 1, 4, 8, 8, 4,
                                            kw.get("pad", 1), kw.get("m", 4), kw.get("flags", 0), None, 0, None)

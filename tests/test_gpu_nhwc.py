@@ -1,7 +1,8 @@
 """Channel-last tensors (x [N][H][W][C], y [N][Ho][Wo][K]) through
 wino_conv2d_nhwc: against the fp64 oracle, and bit for bit against the NCHW
-three-stage path on the same data (the two share V, M and the GEMM; only the
-layout of x and y differs)."""
+path of the same algorithm on the same data (three stages: the two share V, M
+and the GEMM; split: the same blocked V and GEMM kernel; only the layout of x
+and y differs)."""
 import numpy as np
 import pytest
 import torch
@@ -100,3 +101,62 @@ def test_conv2d_nhwc_input_paths_agree(m):
     assert np.array_equal(y_al, y_un)
     ref = direct.conv2d(x, g, pad)
     assert h.normwise_err(y_al.transpose(0, 3, 1, 2), ref) <= TOL[m]
+
+
+# (N, C, H, W, K, pad): ragged tiles, K and C not multiples of 4 or 16, several
+# tile-block pairs and filter groups, a batch whose last block is partial
+SPLIT_SHAPES = [(1, 16, 17, 23, 20, 1), (3, 8, 13, 11, 33, 2), (2, 5, 9, 11, 7, 1), (2, 40, 30, 30, 80, 1),
+                (1, 1, 1, 1, 1, 1)]
+
+
+@pytest.mark.parametrize("m", [2, 4])
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv2d_nhwc_split(m, shape):
+    N, C, H, W, K, pad = shape
+    print(f"conv2d_nhwc split m={m} shape={shape}", flush=True)
+    rng = np.random.default_rng(sum(shape) + 90 * m)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    ref = direct.conv2d(x, g, pad)
+    bound = tile_bound(direct.conv2d(x, g, pad, absval=True), m)
+    U = h.filter_transform(g, m)
+    x_nhwc = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    for flags in (0, B.WINO_FLAG_RELU):
+        f = B.WINO_ALGO_SPLIT | flags
+        y = h.host(conv_nhwc(x_nhwc, U, K, pad, m, f)).transpose(0, 3, 1, 2)
+        want = np.maximum(ref, 0.0) if flags else ref
+        assert np.all(np.isfinite(y))
+        assert h.normwise_err(y, want) <= TOL[m]
+        assert np.all(np.abs(y - want) <= ELEM[m] * (bound + 1e-30))
+        y_nchw = h.host(h.conv2d(x, U, K, pad, m, f))
+        assert np.array_equal(y, y_nchw)              # same V, GEMM and output transform
+
+
+@pytest.mark.parametrize("m", [2, 4])
+def test_conv2d_nhwc_split_paths_and_auto(m):
+    # A layer with more than two rounds of split items: AUTO takes split (same
+    # bits as explicit SPLIT); x and y one float off 16-byte alignment take the
+    # 4-byte input loads and output stores: same bits again; and the NCHW
+    # split path on the same data gives the same bits.
+    N, C, H, W, K, pad = 16, 8, 64, 64, 256, 1
+    rng = np.random.default_rng(77 + m)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    U = h.filter_transform(g, m)
+    x_nhwc = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    assert B.wino_workspace_bytes_nhwc(N, C, H, W, K, pad, m, 0) == \
+        B.wino_workspace_bytes_nhwc(N, C, H, W, K, pad, m, B.WINO_ALGO_SPLIT)
+    y_split = h.host(conv_nhwc(x_nhwc, U, K, pad, m, B.WINO_ALGO_SPLIT))
+    assert np.array_equal(h.host(conv_nhwc(x_nhwc, U, K, pad, m, 0)), y_split)
+    Ho, Wo = H + 2 * pad - 2, W + 2 * pad - 2
+    xb = torch.empty(1 + x_nhwc.size, dtype=torch.float32, device=h.DEV)
+    xb[1:] = torch.from_numpy(x_nhwc.ravel()).to(h.DEV)
+    n_out = N * Ho * Wo * K
+    yb = torch.full((1 + n_out + 256,), float("nan"), dtype=torch.float32, device=h.DEV)
+    conv_nhwc(xb[1:].view(N, H, W, C), U, K, pad, m, B.WINO_ALGO_SPLIT, y=yb[1:1 + n_out].view(N, Ho, Wo, K))
+    a = h.host(yb)
+    assert np.isnan(a[0]) and np.all(np.isnan(a[1 + n_out:]))
+    assert np.array_equal(a[1:1 + n_out].reshape(N, Ho, Wo, K), y_split)
+    y_nchw = h.host(h.conv2d(x, U, K, pad, m, B.WINO_ALGO_SPLIT))
+    assert np.array_equal(y_split.transpose(0, 3, 1, 2), y_nchw)
+    # sampled outputs against the fp64 oracle
+    ref = direct.conv2d(x[:1], g[:16], pad)
+    assert h.normwise_err(y_split[:1, :, :, :16].transpose(0, 3, 1, 2), ref) <= TOL[m]
