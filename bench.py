@@ -64,7 +64,8 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 "split": ("void wino::k_vrows|void wino::k_vblk", "void wino::k_gemm_out"),
                 # the same on channel-last tensors: the NHWC input transform into the
                 # blocked V, then the GEMMs storing y channel-last
-                "split_nhwc": ("void wino::k_input_nhwc", "void wino::k_gemm_out"),
+                "split_nhwc": ("void wino::k_vrows_nhwc|void wino::k_input_nhwc4|void wino::k_input_nhwc",
+                               "void wino::k_gemm_out"),
                 # the fused kernel over channel slices, then the sum of the slices
                 "fused_sliced": ("void wino::k_fused", "void wino::k_slice_sum")}
 

@@ -2153,12 +2153,15 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
 
 // ------------------------------------------------------------------ NHWC
 // Channel-last tensors (x [N][H][W][C], y [N][Ho][Wo][K]) on the three-stage
-// path: only the input and output transforms see the layout; V, M and the GEMM
-// are the same.  Input: one wave per (16-tile block, channel quad), quads of a
-// block consecutive, each lane loading its region of one channel (the 4 lanes
-// of a tile read 16 contiguous bytes per pixel).  Output: one wave per (16-tile block,
-// 16-filter block); a lane holds its tile's four consecutive filters, so every
-// output pixel is one 16-byte store.
+// and split paths: only the input and output transforms see the layout; V, M
+// and the GEMMs are the same.  Input: by tile rows through LDS (k_vrows_nhwc)
+// where C % 4 == 0, x is 16-byte aligned and a tile row fits; else per 16-tile
+// block: 16-byte channel-quad loads (k_input_nhwc4) or, for other C or
+// alignments, one wave per (16-tile block, channel quad), quads of a block
+// consecutive, each lane loading its region of one channel (the 4 lanes of a
+// tile read 16 contiguous bytes per pixel).  Output (three stages): one wave
+// per (16-tile block, 16-filter block); a lane holds its tile's four
+// consecutive filters, so every output pixel is one 16-byte store.
 template <int MT>
 __global__ __launch_bounds__(256) void k_input_nhwc(const float* __restrict__ x, float* __restrict__ V, Geom g,
                                                     long nwg, int nq) {
@@ -2243,6 +2246,101 @@ __global__ __launch_bounds__(256) void k_input_nhwc4(const float* __restrict__ x
         float vv[T];
         input_tf<MT>(d, vv);
         store_t4<T, true>(blk, e * 16 + t, vv);
+    }
+}
+
+// With C % 4 == 0 and room in LDS, by whole tile rows as k_vrows does: one
+// workgroup per (R consecutive tile rows of the batch, group of QG = 2^lqg <= 4
+// channel quads), the groups of one row range consecutive in the XCD-aware
+// item order (they share x's cache lines).  A thread loads, for columns
+// (c / QG) and quads (c % QG) of the chunks c = tid, tid + 256, ..., the
+// 16-byte channel quads of every region row (a pixel's QG quads are one
+// contiguous run, so a wave reads whole runs and each x byte once per tile
+// row), and writes them to LDS as [r][A rows][pitch][QGP] floats: the pixel
+// pitch QGP = 4*QG + 1 (m = 4) or + 2 (m = 2) puts the 16 tiles x 4 channels
+// that a wave reads on distinct banks.  Wave w then transforms (block, quad)
+// tasks w, w+4, ..., lane = (channel, tile), and stores each block's
+// position groups as whole 1 KiB runs; a block that two row ranges share is
+// completed by the other workgroup, and the batch's last partial block gets
+// zeros past the last tile.  Quads past CQ (the split path's padding) read as
+// zeros.  Offsets are 32-bit from the first image the rows touch (the host
+// checks that they fit below kInvalid).  Plain stores: the blocks two
+// workgroups share meet in L2 (streaming stores measured 1.7x slower).
+template <int MT>
+__global__ __launch_bounds__(256) void k_vrows_nhwc(const float* __restrict__ x, float* __restrict__ V, Geom g,
+                                                    int R, int lqg, int QGP, int pitch, int nq, int nitems) {
+    constexpr int A = MT + 2, T = A * A;
+    extern __shared__ float4 xs4[];
+    float* xs = (float*)xs4;
+    const int QG = 1 << lqg;
+    const int nrows = g.N * g.th;
+    const int nqg = (nq + QG - 1) >> lqg;
+    const int per = (nitems + 7) / 8, item = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
+    if (item >= nitems) return;
+    const int qg = item % nqg, gr0 = item / nqg * R;
+    const int q0 = qg * QG, nqw = min(QG, nq - q0);     // this workgroup's quads [q0, q0 + nqw)
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n0 = gr0 / g.th;
+    const size_t img = (size_t)g.H * g.W * g.C;
+    const size_t left = ((size_t)g.N - n0) * img * 4;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + (size_t)n0 * img), (short)0, (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
+    const uint32_t img_b = (uint32_t)(img * 4), row_b = (uint32_t)g.W * (uint32_t)g.C * 4u;
+    for (int c = tid; c < pitch * QG; c += 256) {
+        const int lc = c >> lqg, q = c & (QG - 1);
+        const int col = lc - g.pad, cq = q0 + q;
+        const bool cok = (unsigned)col < (unsigned)g.W && q < nqw && cq < g.CQ;
+        const uint32_t coff = (uint32_t)col * (uint32_t)g.C * 4u + (uint32_t)cq * 16u;
+        float* const lp = xs + lc * QGP + 4 * q;
+        for (int r = 0; r < R; ++r) {
+            const int gr = gr0 + r, n = gr / g.th, ti = gr - n * g.th;
+            const bool rok = cok && gr < nrows;
+            f32x4 v[A];
+#pragma unroll
+            for (int u = 0; u < A; ++u) {
+                const int row = ti * MT - g.pad + u;
+                const bool ok = rok && (unsigned)row < (unsigned)g.H;
+                const uint32_t off = ok ? (uint32_t)(n - n0) * img_b + (uint32_t)row * row_b + coff : kInvalid;
+                v[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0));
+            }
+#pragma unroll
+            for (int u = 0; u < A; ++u) {
+                float* d = lp + (r * A + u) * pitch * QGP;
+                d[0] = v[u][0];
+                d[1] = v[u][1];
+                d[2] = v[u][2];
+                d[3] = v[u][3];
+            }
+        }
+    }
+    __syncthreads();
+    const int l16 = lane & 15, cl = lane >> 4;
+    const int t0 = gr0 * g.tw, t1 = min(gr0 + R, nrows) * g.tw;   // this workgroup's tiles [t0, t1)
+    const int b0 = t0 >> 4, nblk = ((t1 - 1) >> 4) - b0 + 1;
+    const size_t qstride = (size_t)nq * T * 64;                   // floats of one block
+    const bool last_tail = t1 == g.P && (g.P & 15);               // the batch's last block is partial
+    for (int task = wave; task < nblk * nqw; task += 4) {
+        const int bi = task / nqw, q = task - bi * nqw;
+        const int blk = b0 + bi, p = blk * 16 + l16;
+        float* dst = V + (size_t)blk * qstride + (size_t)(q0 + q) * T * 64 + lane * 4;
+        if (p >= t0 && p < t1) {
+            const int pr = p / g.tw, r = pr - gr0, tj = p - pr * g.tw;
+            const float* wp = xs + (r * A * pitch + tj * MT) * QGP + 4 * q + cl;
+            float d[A][A];
+#pragma unroll
+            for (int u = 0; u < A; ++u)
+#pragma unroll
+                for (int v = 0; v < A; ++v) d[u][v] = wp[(u * pitch + v) * QGP];
+            float vv[T];
+            input_tf<MT>(d, vv);
+#pragma unroll
+            for (int g4 = 0; g4 < T / 4; ++g4)
+                store_out<false>(dst + g4 * 256, vv[4 * g4], vv[4 * g4 + 1], vv[4 * g4 + 2], vv[4 * g4 + 3]);
+        } else if (last_tail && p >= g.P) {
+#pragma unroll
+            for (int g4 = 0; g4 < T / 4; ++g4) store_out<false>(dst + g4 * 256, 0.f, 0.f, 0.f, 0.f);
+        }
     }
 }
 
@@ -2449,12 +2547,71 @@ hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int 
     return hipGetLastError();
 }
 
+// Row-wise channel-last input transform: tile rows per workgroup, log2 of the
+// quads per workgroup, LDS pixel pitch and row pitch (floats), dynamic LDS
+// bytes; R = 0 where one tile row of at least one quad does not fit, or the
+// images a row range spans do not fit the 32-bit load offsets.
+struct NhwcRowsPlan {
+    int R, lqg, QGP, pitch;
+    size_t lds;
+};
+// Three workgroups per CU; at most 4 quads per workgroup (measured on the
+// N=64 256-channel 56x56 layer: 8 quads and one tile row 12 us slower, and
+// every larger LDS share slower still).
+constexpr size_t kNhwcRowsLds = 52 << 10;
+
+static NhwcRowsPlan nhwc_rows_plan(const Geom& g, int nq) {
+    NhwcRowsPlan p{0, 0, 0, 0, 0};
+    p.pitch = g.tw * g.m + 2;
+    int lqg = 0;
+    while (lqg < 2 && (1 << lqg) < nq) ++lqg;           // the quads a workgroup needs, at most 4
+    size_t row_b = 0;
+    for (; lqg >= 0; --lqg) {
+        p.QGP = 4 * (1 << lqg) + (g.m == 4 ? 1 : 2);
+        row_b = (size_t)g.A * p.pitch * p.QGP * sizeof(float);
+        if (row_b <= kNhwcRowsLds) break;
+    }
+    if (lqg < 0) return p;
+    int gcd = 16, t = g.tw;
+    while (t) {
+        const int r = gcd % t;
+        gcd = t;
+        t = r;
+    }
+    int R = 16 / gcd;
+    while (R > 1 && (size_t)R * row_b > kNhwcRowsLds) --R;
+    const size_t img_b = (size_t)g.C * g.H * g.W * sizeof(float);
+    while (R > 1 && (size_t)(R / g.th + 2) * img_b >= (size_t)kInvalid) --R;
+    if ((size_t)(R / g.th + 2) * img_b >= (size_t)kInvalid) return p;
+    const long items = ((long)g.N * g.th + R - 1) / R * (((long)nq + (1 << lqg) - 1) >> lqg);
+    if ((items + 7) / 8 * 8 > 0x7fffffffL) return p;
+    p.R = R;
+    p.lqg = lqg;
+    p.lds = R * row_b;
+    return p;
+}
+
 // Channel-last input transform into V blocks of nq quads ([PB][nq][T/4][64][4]:
 // nq = CQ for the three stages, CQ rounded up to 4 for the split path).
 static hipError_t launch_input_nhwc(const float* x, float* V, const Geom& g, int nq, hipStream_t s) {
+    const dim3 block(256);
+    if (g.C % 4 == 0 && aligned(x, 16)) {
+        const NhwcRowsPlan rp = nhwc_rows_plan(g, nq);
+        if (rp.R > 0) {
+            const int nitems = (int)(((long)g.N * g.th + rp.R - 1) / rp.R * ((nq + (1 << rp.lqg) - 1) >> rp.lqg));
+            const dim3 grid((unsigned)((nitems + 7) / 8 * 8));
+            if (g.m == 2)
+                hipLaunchKernelGGL(k_vrows_nhwc<2>, grid, block, rp.lds, s, x, V, g, rp.R, rp.lqg, rp.QGP, rp.pitch,
+                                   nq, nitems);
+            else
+                hipLaunchKernelGGL(k_vrows_nhwc<4>, grid, block, rp.lds, s, x, V, g, rp.R, rp.lqg, rp.QGP, rp.pitch,
+                                   nq, nitems);
+            return hipGetLastError();
+        }
+    }
     const long waves = (long)g.PB * nq, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)((nwg + 7) / 8 * 8)), block(256);
+    const dim3 grid((unsigned)((nwg + 7) / 8 * 8));
     // 16-byte channel-quad loads when the quads are aligned and the 32-bit
     // offsets of the images one tile block spans (at most 16 / (th*tw) + 2)
     // stay below kInvalid

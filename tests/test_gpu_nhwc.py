@@ -86,21 +86,27 @@ def test_conv2d_nhwc_unaligned_output_and_guards(m):
 
 
 @pytest.mark.parametrize("m", [2, 4])
-def test_conv2d_nhwc_input_paths_agree(m):
-    # C % 4 == 0 with x 16-byte aligned takes the 16-byte channel-quad loads; the
-    # same x one float off that alignment takes the 4-byte loads: same bits.
-    N, C, H, W, K, pad = 2, 20, 11, 14, 18, 1
+@pytest.mark.parametrize("wide", [False, True])
+def test_conv2d_nhwc_input_paths_agree(m, wide):
+    # C % 4 == 0 with x 16-byte aligned takes the input transform by tile rows
+    # through LDS, or, for an image too wide for one tile row of one channel
+    # quad in its LDS budget, the 16-byte channel-quad loads per tile block; the
+    # same x one float off that alignment takes the 4-byte loads: same bits,
+    # on both the three stages and the split path.
+    N, C, H, W, K, pad = (1, 4, 5, 444 if m == 4 else 556, 8, 1) if wide else (2, 20, 11, 14, 18, 1)
+    print(f"nhwc input paths m={m} shape={(N, C, H, W, K, pad)}", flush=True)
     rng = np.random.default_rng(41 + m)
     x, g = wl.random_layer(rng, N, C, H, W, K)
     U = h.filter_transform(g, m)
     x_nhwc = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
-    y_al = h.host(conv_nhwc(x_nhwc, U, K, pad, m))
     xb = torch.empty(1 + x_nhwc.size, dtype=torch.float32, device=h.DEV)
     xb[1:] = torch.from_numpy(x_nhwc.ravel()).to(h.DEV)
-    y_un = h.host(conv_nhwc(xb[1:].view(N, H, W, C), U, K, pad, m))
-    assert np.array_equal(y_al, y_un)
     ref = direct.conv2d(x, g, pad)
-    assert h.normwise_err(y_al.transpose(0, 3, 1, 2), ref) <= TOL[m]
+    for algo in (B.WINO_ALGO_STAGED, B.WINO_ALGO_SPLIT):
+        y_al = h.host(conv_nhwc(x_nhwc, U, K, pad, m, algo))
+        y_un = h.host(conv_nhwc(xb[1:].view(N, H, W, C), U, K, pad, m, algo))
+        assert np.array_equal(y_al, y_un)
+        assert h.normwise_err(y_al.transpose(0, 3, 1, 2), ref) <= TOL[m]
 
 
 # (N, C, H, W, K, pad): ragged tiles, K and C not multiples of 4 or 16, several
