@@ -126,9 +126,14 @@ def layer_numbers(N, L):
         "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
         # the 16-bit GEMM stage alone: 16-bit V and U read, fp32 M written
         "gemm16": v_b // 2 + u_b // 2 + m_b,
+        # the split path's two kernels: the input transform ("input"), then the
+        # GEMMs with the output transform (V and U read, y written)
+        "gemm_out": v_b + u_b + y_b,
+        # the 16-bit input transform (16-bit V written)
+        "input16": x_b + v_b // 2,
     }
     f["flops"] = {"fused": f["gemm_flops"], "fused_sliced": f["gemm_flops"], "split": f["gemm_flops"],
-                  "split_nhwc": f["gemm_flops"], "gemm": f["gemm_flops"],
+                  "split_nhwc": f["gemm_flops"], "gemm": f["gemm_flops"], "gemm_out": f["gemm_flops"],
                   "stages": f["gemm_flops"],
                   "stages16": f["gemm_flops"], "gemm16": f["gemm_flops"]}
     return f
@@ -372,6 +377,97 @@ def trace_summary(args):
     print(text, end="")
 
 
+# Stage of a kernel of the step, by name (the first prefix that matches).
+STAGE_OF = (("k_gemm_out", "gemm_out"), ("k_gemm16", "gemm16"), ("k_gemm", "gemm"), ("k_fused", "fused"),
+            ("k_slice_sum", "slice_sum"), ("k_lowc", "lowc"), ("k_maxpool2x2", "maxpool"),
+            ("k_vrows", "input"), ("k_vblk", "input"), ("k_input", "input"), ("k_output", "output"))
+STAGE_MARKER = "FillFunctor"      # the torch fill that --stage-trace launches before every launch
+
+
+def stage_table(args):
+    """Per-layer, per-kernel durations of the step and each kernel's fraction of
+    its own roofline, from a rocprofv3 --kernel-trace csv run of
+    `bench.py --stage-trace DIR` (no GPU needed): the marker kernels split the
+    trace into the step's launches; medians over the timed steps."""
+    import re
+    from paper_1903_01521_amd import workloads as wl
+    d = args.stage_table
+    meta = json.load(open(os.path.join(d, "launches.json")))
+    name = meta["workload"]
+    w = wl.WORKLOADS[name]
+    nums = [layer_numbers(w.N, L) for L in w.layers]
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one kernel_trace.csv under {d}, found {len(files)}")
+    rows = sorted(csv.DictReader(open(files[0])), key=lambda r: int(r["Dispatch_Id"]))
+    launches = meta["launches"]                      # [[label, layer index], ...] of one step
+    nl, steps = len(launches), meta["steps"]
+    marks = [i for i, r in enumerate(rows) if STAGE_MARKER in r["Kernel_Name"]]
+    if len(marks) < nl * steps:
+        raise SystemExit(f"{len(marks)} marker kernels in the trace, expected at least {nl * steps}")
+    marks = marks[-nl * steps:]
+    per = {}                                         # (launch, kernel position) -> (name, [ns])
+    for j, m0 in enumerate(marks):
+        m1 = marks[j + 1] if j + 1 < len(marks) else len(rows)
+        ks = [r for r in rows[m0 + 1:m1] if "wino::" in r["Kernel_Name"]]
+        for q, r in enumerate(ks):
+            key = (j % nl, q)
+            nm = re.sub(r"\(.*$", "", re.sub(r"^void ", "", r["Kernel_Name"]))
+            nm = nm.replace("wino::", "").replace(" ", "")
+            per.setdefault(key, (nm, []))[1].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    prec = (meta["flags"] & 0x30) != 0               # 16-bit GEMM operands
+    fl = f" --flags {meta['flags']:#x}" if meta["flags"] else ""
+    lines = [f"# Per-layer, per-kernel durations of the timed step: workload {name}{fl}",
+             "# one MI355X; each kernel's median over the timed steps (eager launches in",
+             "# sequence, so every kernel runs after its real predecessor), and its fraction",
+             "# of its own roofline from the algorithmic FLOPs or bytes of its stage",
+             "# (input/output transforms and pools: HBM bytes; GEMMs: MFMA FLOPs or HBM",
+             "# bytes, whichever bounds them; peaks 157.3 TFLOP/s fp32, 8 TB/s).",
+             "# commands (on the GPU host; <repo> is the repository root):",
+             "#   cd /tmp && export TMPDIR=/tmp",
+             f"#   rocprofv3 --kernel-trace --output-format csv -d <out>/st -o run -- python3 <repo>/bench.py "
+             f"--workload {name}{fl} --steps {steps} --warmup {meta['warmup']} --stage-trace <out>/st",
+             f"#   python3 <repo>/bench.py --stage-table <out>/st",
+             f"sources_sha256: {sources_hash()}",
+             "",
+             f"{'launch':<10}{'layer':<22}{'kernel':<34}{'stage':<10}{'med_us':>9}{'p10':>9}{'p90':>9}"
+             f"  {'bound':<5}{'achieved':>10} {'unit':<8}{'frac':>7}"]
+    total_ns = 0.0
+    conv_ns = [0.0] * len(w.layers)
+    for (li, q) in sorted(per):
+        nm, ns = per[(li, q)]
+        label, layer = launches[li]
+        L, f = w.layers[layer], nums[layer]
+        base = nm.split("<")[0]
+        stage = next((st for pre, st in STAGE_OF if base.startswith(pre)), None)
+        if stage == "input" and prec:
+            stage = "input16"
+        med, p10, p90 = float(np.median(ns)), float(np.percentile(ns, 10)), float(np.percentile(ns, 90))
+        total_ns += med
+        if stage != "maxpool":
+            conv_ns[layer] += med
+        shape = f"{L.C}->{L.K} @{L.H}x{L.W} m{L.m}" + (f" r{L.r}" if L.r != 3 else "")
+        rf = roofline(stage, f, med * 1e-9) if stage in f["bytes"] else None
+        if stage == "maxpool":             # the pool reads this layer's y and writes a quarter of it
+            rf = roofline("maxpool", f, med * 1e-9)
+        tail = (f"  {rf['bound']:<5}{rf['achieved']:>10} {rf['unit']:<8}{rf['frac']:>7.3f}" if rf
+                else "  -")
+        lines.append(f"{label:<10}{shape:<22}{nm[:33]:<34}{stage or '-':<10}{med / 1e3:>9.1f}{p10 / 1e3:>9.1f}"
+                     f"{p90 / 1e3:>9.1f}{tail}")
+    lines.append("")
+    lines.append(f"step: {total_ns / 1e3:.1f} us (sum of the kernel medians)")
+    for i, (L, f) in enumerate(zip(w.layers, nums)):
+        if conv_ns[i] > 0:
+            lines.append(f"L{i} conv: {conv_ns[i] / 1e3:.1f} us, {f['direct_flops'] / conv_ns[i] / 1e3:.1f} "
+                         f"TFLOP/s effective (direct-conv FLOPs)")
+    text = "\n".join(lines) + "\n"
+    if args.write_summary:
+        tag = f"_{args.tag}" if args.tag else ""
+        with open(os.path.join(PROFILES, f"stage_table_{name}{tag}.txt"), "w") as fh:
+            fh.write(text)
+    print(text, end="")
+
+
 # Layers whose algorithm choice the planner table records: the single 3x3
 # layers, one layer of the ResNet stage, and the VGG-16 layers at N=1 and N=32.
 PLANNER_WORKLOADS = ("f2_n1_c32_k32_56x56", "f4_n1_c64_k64_112x112", "f4_n1_c48_k48_57x57",
@@ -543,6 +639,11 @@ def main():
     ap.add_argument("--kind", default="fused", help="kernel kind the --pmc-summary covers")
     ap.add_argument("--write-summary", action="store_true",
                     help="with --pmc-summary: also write it to profiles/traffic_<workload>.txt")
+    ap.add_argument("--stage-trace", metavar="DIR",
+                    help="run only the step (W + K times), a marker kernel before every launch, and write "
+                         "DIR/launches.json; for a rocprofv3 --kernel-trace run that --stage-table reads")
+    ap.add_argument("--stage-table", metavar="DIR",
+                    help="per-layer, per-kernel durations and stage rooflines from such a run (no GPU needed)")
     ap.add_argument("--planner-table", action="store_true",
                     help="time every algorithm on the planner's reference layers (profiles/planner_table.txt)")
     args = ap.parse_args()
@@ -555,6 +656,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args)
+        return
+    if args.stage_table:
+        stage_table(args)
         return
 
     if args.planner_table:
@@ -718,6 +822,24 @@ def main():
                 run(fns)
         torch.cuda.synchronize()
         return g
+
+    if args.stage_trace:
+        # The step alone, a torch fill (the marker) before every launch; the
+        # launch list goes beside the trace for --stage-table.
+        layer_of = {label: i for label, i, kind, _ in step if kind != "filter"}
+        mk = torch.empty(1024, dtype=torch.float32, device=dev)
+        run(filter_fns)
+        for _ in range(args.warmup + args.steps):
+            for label, fn in step_fns:
+                mk.fill_(1.0)
+                run([(label, fn)])
+        torch.cuda.synchronize()
+        os.makedirs(args.stage_trace, exist_ok=True)
+        with open(os.path.join(args.stage_trace, "launches.json"), "w") as fh:
+            json.dump({"workload": name, "flags": flags, "steps": args.steps, "warmup": args.warmup,
+                       "launches": [[label, layer_of[label]] for label, _ in step_fns]}, fh)
+        print(f"stage trace: {args.warmup + args.steps} steps of {len(step_fns)} launches", flush=True)
+        return
 
     stream = torch.cuda.current_stream()
     GS = 10

@@ -131,3 +131,37 @@ def test_gemm16_accounting():
     assert f["bytes"]["gemm16"] == 2 * 36 * P * 256 + 2 * 36 * 256 * 256 + 4 * 36 * P * 256
     r = bench.roofline("gemm16", f, 150e-6)
     assert r["bound"] == "hbm" and r["peak"] == 8000.0
+
+
+def test_stage_table_from_trace(tmp_path, capsys):
+    # A synthetic kernel trace of `bench.py --stage-trace` on the N=64 256-channel
+    # layer: a weight transform, then per step a marker fill and the split
+    # call's two kernels; the first of the four steps is the warm-up.
+    import argparse
+    import json
+    name = "f4_n64_c256_k256_56x56"
+    with open(tmp_path / "launches.json", "w") as f:
+        json.dump({"workload": name, "flags": 0, "steps": 3, "warmup": 1, "launches": [["L0.conv", 0]]}, f)
+    rows = [("void wino::k_filter<4, true, true, 3>(float const*, float*, int, int, int, long)", 5000)]
+    for step, (tv, tg) in enumerate([(900e3, 900e3), (110e3, 520e3), (100e3, 500e3), (120e3, 540e3)]):
+        rows.append(("void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<float>>()", 2000))
+        rows.append(("void wino::k_vrows<4, 1, 0>(float const*, float*, wino::Geom, int, int, int)", tv))
+        rows.append(("void wino::k_gemm_out<4>(float const*, float const*, float*, wino::Geom)", tg))
+    t = 1000
+    with open(tmp_path / "run_kernel_trace.csv", "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Start_Timestamp,End_Timestamp\n")
+        for i, (k, d) in enumerate(rows):
+            f.write(f'{i + 1},"{k}",{t},{t + int(d)}\n')
+            t += int(d) + 100
+    args = argparse.Namespace(stage_table=str(tmp_path), write_summary=False, tag="")
+    bench.stage_table(args)
+    out = capsys.readouterr().out.splitlines()
+    body = [l.split() for l in out if l.startswith("L0.conv")]
+    assert [r[5] for r in body] == ["input", "gemm_out"]
+    f = bench.layer_numbers(64, wl.WORKLOADS[name].first)
+    # medians of the three timed steps (the warm-up's 900 us is dropped)
+    assert float(body[0][6]) == pytest.approx(110.0) and float(body[1][6]) == pytest.approx(520.0)
+    # input transform: x read, V written, against HBM; GEMMs: against the fp32 MFMA peak
+    assert body[0][9] == "hbm" and float(body[0][12]) == pytest.approx(f["bytes"]["input"] / 110e-6 / 8e12, abs=1e-3)
+    assert body[1][9] == "mfma" and float(body[1][12]) == pytest.approx(f["gemm_flops"] / 520e-6 / 157.3e12, abs=1e-3)
+    assert any(l.startswith("step: 630.0 us") for l in out)
