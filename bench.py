@@ -58,6 +58,9 @@ KERNEL_NAMES = {"filter": "void wino::k_filter", "fused": "void wino::k_fused", 
                 "input": "void wino::k_vrows|void wino::k_input", "gemm": "void wino::k_gemm",
                 "output": "void wino::k_output", "maxpool": "void wino::k_maxpool2x2",
                 "stages": "void wino::k_gemm", "stages16": "void wino::k_gemm16",
+                # the split path on 16-bit operands: the 16-bit input transform, then
+                # the GEMMs (16-bit MFMAs) with the output transform
+                "split16": ("void wino::k_vrows|void wino::k_input16", "void wino::k_gemm_out"),
                 "gemm16": "void wino::k_gemm16",
                 # the split path's call: the input transform (by tile rows, or by 16-tile
                 # patches for very wide images), then the GEMMs with the output transform
@@ -124,6 +127,8 @@ def layer_numbers(N, L):
         "stages": x_b + 2 * v_b + u_b + 2 * m_b + y_b,
         # the same with 16-bit V and U (fp16 / bf16 GEMM operands)
         "stages16": x_b + v_b + u_b // 2 + 2 * m_b + y_b,
+        # the split path on 16-bit operands: x and 16-bit U read, y written
+        "split16": x_b + u_b // 2 + y_b,
         # the 16-bit GEMM stage alone: 16-bit V and U read, fp32 M written
         "gemm16": v_b // 2 + u_b // 2 + m_b,
         # the split path's two kernels: the input transform ("input"), then the
@@ -135,14 +140,14 @@ def layer_numbers(N, L):
     f["flops"] = {"fused": f["gemm_flops"], "fused_sliced": f["gemm_flops"], "split": f["gemm_flops"],
                   "split_nhwc": f["gemm_flops"], "gemm": f["gemm_flops"], "gemm_out": f["gemm_flops"],
                   "stages": f["gemm_flops"],
-                  "stages16": f["gemm_flops"], "gemm16": f["gemm_flops"]}
+                  "stages16": f["gemm_flops"], "gemm16": f["gemm_flops"], "split16": f["gemm_flops"]}
     return f
 
 
 def roofline(kind, nums, seconds):
     b = nums["bytes"].get(kind, 0)
     fl = nums["flops"].get(kind, 0)
-    peak = FP16_MFMA_PEAK if kind in ("stages16", "gemm16") else FP32_MFMA_PEAK   # the GEMM's own operand type
+    peak = FP16_MFMA_PEAK if kind in ("stages16", "gemm16", "split16") else FP32_MFMA_PEAK   # the GEMM's own operand type
     t_hbm = b / HBM_PEAK
     t_mfma = fl / peak
     if t_mfma >= t_hbm and fl > 0:
@@ -781,8 +786,11 @@ def main():
                 ws, wsb = wss[i]
                 st, algo, nsl = B.wino_plan_r(N, L.C, L.H, L.W, L.K, L.pad, L.m, L.r, flags | relu)
                 B.check(st, "wino_plan_r")
-                kind = "stages16" if prec else {B.WINO_ALGO_LOWC: "lowc", B.WINO_ALGO_SPLIT: "split"}.get(
-                    algo, "fused_sliced" if nsl > 1 else "fused")
+                if prec:
+                    kind = "split16" if algo == B.WINO_ALGO_SPLIT else "stages16"
+                else:
+                    kind = {B.WINO_ALGO_LOWC: "lowc", B.WINO_ALGO_SPLIT: "split"}.get(
+                        algo, "fused_sliced" if nsl > 1 else "fused")
                 out.append((f"L{i}.conv", i, kind, (lambda sp, i=i, L=L, a=a, relu=relu, ws=ws, wsb=wsb:
                                                        B.wino_conv2d_r(a, Us[i], ys[i], N, L.C, L.H, L.W, L.K,
                                                                        L.pad, L.m, L.r, flags | relu,

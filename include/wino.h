@@ -95,10 +95,14 @@ extern "C" {
 #define WINO_ALGO_LOWC     0x400u   /* one kernel for C <= 4 (a network's first layer): a
                                        lane per tile, vector FMAs over the channels */
 #define WINO_ALGO_MASK     0xF00u
-/* Reduced-precision GEMM operands (three-stage algorithm, 3x3 NCHW layers only):
- * U and V rounded to fp16 or bf16 (nearest, ties to even), the T per-position
- * GEMMs on 16-bit MFMA with fp32 accumulation, M and the output transform in
- * fp32.  U must come from wino_filter_transform_p with the same format.  Not
+/* Reduced-precision GEMM operands (3x3 NCHW layers only): U and V rounded to
+ * fp16 or bf16 (nearest, ties to even), the T per-position GEMMs on 16-bit MFMA
+ * with fp32 accumulation, the output transform in fp32.  Algorithms: the three
+ * stages (WINO_ALGO_STAGED; fp32 M through the workspace) or the split path
+ * (WINO_ALGO_SPLIT; the GEMM kernel applies the output transform to its
+ * accumulators); AUTO takes split on layers with at least two rounds of its
+ * work items on the CUs, else the three stages.  U must come from
+ * wino_filter_transform_p with the same format.  Not
  * within the fp32 gates: measured normwise errors against the exact result are
  * about 5e-4 (fp16) and 4e-3 (bf16) for m = 2, 7e-3 and 6e-2 for m = 4. */
 #define WINO_PREC_F16      0x010u
@@ -144,7 +148,7 @@ size_t wino_gemm_out_bytes(int N, int K, int H, int W, int pad, int m);
 /* Workspace bytes wino_conv2d needs for this layer and flags word.  The
  * result depends on the whole word as wino_conv2d reads it: the algorithm
  * (and, for WINO_ALGO_AUTO, the planner's choice of split, channel slices or
- * staged), WINO_PREC_* (16-bit V plus fp32 M), WINO_CSLICES(n) (the partial
+ * staged), WINO_PREC_* (16-bit V plus fp32 M, or the split path's 16-bit V), WINO_CSLICES(n) (the partial
  * outputs) and the variant overrides.  0 means the plan needs none (workspace
  * may then be NULL).  Returns (size_t)-1 for invalid arguments and for flag
  * sets or layers that wino_conv2d would reject as WINO_ERR_UNSUPPORTED. */
@@ -211,12 +215,13 @@ int wino_output_transform(const float* M, float* y, int N, int K, int H, int W,
 
 /* Transformed filters in a 16-bit GEMM format (prec = WINO_PREC_F16 or
  * WINO_PREC_BF16; 0 gives the fp32 calls above):
- *   UH[KB][C16][T][64][4] 16-bit values, C16 = ceil(C/16): element (t,c,k) at
- *   lane ((c%16)/4)*16 + k%16, half c%4 of group (k/16, c/16, t) -- one 8-byte
- *   word per lane (four consecutive channels per lane; the words of groups
- *   2j and 2j+1 together form a lane's A operand of v_mfma_f32_16x16x32).
- *   Each value is G g G^T in fp64, rounded to fp32, then to
- *   the 16-bit format.  Bytes: 2*T*roundup(C,16)*roundup(K,16). */
+ *   UH[KB][C32][T][64][8] 16-bit values, C32 = ceil(C/32): element (t,c,k) at
+ *   lane ((c%16)/4)*16 + k%16, half ((c%32)/16)*4 + c%4 of block (k/16, c/32,
+ *   t) -- one 16-byte word per lane, the lane's A operand of
+ *   v_mfma_f32_16x16x32 (four consecutive channels of each 16-channel half of
+ *   the 32-channel chunk; padding zero).  Each value is G g G^T in fp64,
+ *   rounded to fp32, then to the 16-bit format.
+ *   Bytes: 2*T*roundup(C,32)*roundup(K,16). */
 size_t wino_filter_bytes_p(int C, int K, int m, unsigned prec);
 int wino_filter_transform_p(const float* g, void* U, int C, int K, int m, unsigned prec, void* stream);
 

@@ -22,8 +22,9 @@ int prec_of(unsigned flags) {
     return p == 0 ? 0 : p == WINO_PREC_F16 ? 1 : p == WINO_PREC_BF16 ? 2 : -1;
 }
 
-size_t c16_elems(const Geom& g) { return (size_t)(g.C + 15) / 16; }
-size_t vh_bytes(const Geom& g) { return (size_t)g.PB * c16_elems(g) * g.T * 64 * 8; }
+// 16-bit operands: 32-channel chunks, 1 KB per (block, chunk, position).
+size_t c32_elems(const Geom& g) { return (size_t)(g.C + 31) / 32; }
+size_t vh_bytes(const Geom& g) { return (size_t)g.PB * c32_elems(g) * g.T * 1024; }
 
 // Checked product of non-negative int64 values; false on overflow past kMaxElems.
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
@@ -158,6 +159,9 @@ double split_ns(const Geom& g) {
 
 size_t split_workspace(const Geom& g) { return vblk_elems(g) * sizeof(float); }
 
+// The 16-bit split path's VH: tile blocks x C32 chunks x T x 1 KB.
+size_t split16_workspace(const Geom& g) { return (size_t)split_blocks(g) * c32_elems(g) * g.T * 1024; }
+
 // Partial outputs of the channel slices: [slices used][N][K][Ho][Wo].
 size_t slice_workspace(const Geom& g, int nsl) {
     return (size_t)slices_used(g, nsl) * g.N * g.K * g.Ho * g.Wo * sizeof(float);
@@ -195,6 +199,14 @@ bool split_offsets_fit(const Geom& g) {
     return (int64_t)kInvalidOffset + ncq4 * 16 * plane_b < kOffsetLimit;
 }
 
+// 16-bit input transforms: per 16-tile block (k_input16) a channel past C adds
+// its plane offset (up to C rounded up to 32) to kInvalidOffset; by tile rows
+// the images a row range spans must fit.
+bool prec_offsets_fit(const Geom& g) {
+    const int64_t plane_b = (int64_t)g.H * g.W * 4;
+    return block_images_fit(g) && (int64_t)kInvalidOffset + (int64_t)c32_elems(g) * 32 * plane_b < kOffsetLimit;
+}
+
 bool plan_fits(const Geom& g, const Plan& p) {
     if (p.algo == WINO_ALGO_STAGED) return block_images_fit(g);
     if (p.algo == WINO_ALGO_FUSED) return image_fits(g) && fused_offsets_fit(g, p.cfg);
@@ -210,6 +222,7 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p);
 int make_plan(const Geom& g, unsigned flags, Plan* p) {
     const int st = make_plan_unchecked(g, flags, p);
     if (st != WINO_OK || g.axis != 0 || g.nhwc) return st;
+    if (prec_of(flags)) return prec_offsets_fit(g) ? WINO_OK : WINO_ERR_UNSUPPORTED;
     if (plan_fits(g, *p)) return WINO_OK;
     if (!p->automatic) return WINO_ERR_UNSUPPORTED;
     if (p->algo == WINO_ALGO_FUSED && g.r == 3) {
@@ -236,16 +249,19 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
     const unsigned blk = flags & kBlockMask;
     // 1-D filters, channel-last tensors and 16-bit operands run the three
     // stages (input transform, GEMMs, output transform); channel-last 3x3
-    // layers also the split path (its GEMM kernel stores y channel-last).  Of
-    // the other one-kernel variants, the fused kernel also takes 5x5 filters
-    // of NCHW tensors, the split and low-channel ones only 3x3.
+    // layers and 16-bit operands also the split path (its GEMM kernel stores y
+    // channel-last, or runs on 16-bit MFMAs).  Of the other one-kernel
+    // variants, the fused kernel also takes 5x5 filters of NCHW tensors, the
+    // split and low-channel ones only 3x3.
     const int prec = prec_of(flags);
     if (prec < 0) return WINO_ERR_UNSUPPORTED;
     if (prec && (g.r != 3 || g.axis != 0 || g.nhwc)) return WINO_ERR_UNSUPPORTED;
     if (g.axis != 0 || g.nhwc || prec) {
-        const bool nhwc_split = g.nhwc && g.axis == 0 && g.r == 3 && !prec &&
-                                (int64_t)g.KB * g.CQ * g.T * 256 <= 0x7fffffffLL;
-        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED && !(algo == WINO_ALGO_SPLIT && nhwc_split)) ||
+        // the split GEMM kernel addresses U through a 32-bit buffer range
+        const bool can_split = g.axis == 0 && g.r == 3 &&
+                               (prec ? (int64_t)g.KB * (int64_t)c32_elems(g) * g.T * 1024 <= 0x7fffffffLL
+                                     : g.nhwc && (int64_t)g.KB * g.CQ * g.T * 256 <= 0x7fffffffLL);
+        if ((algo != WINO_ALGO_AUTO && algo != WINO_ALGO_STAGED && !(algo == WINO_ALGO_SPLIT && can_split)) ||
             blk || (flags >> kCsplitShift) & 0xF || (flags >> kSliceShift) & 0xF)
             return WINO_ERR_UNSUPPORTED;
         p->automatic = algo == WINO_ALGO_AUTO;
@@ -253,7 +269,7 @@ int make_plan_unchecked(const Geom& g, unsigned flags, Plan* p) {
         // AUTO: split on layers with at least two full rounds of its items
         // (tile-block pair x filter group) on the CUs, where the saved M round
         // trip outweighs its per-item prologue and epilogue.
-        p->algo = algo == WINO_ALGO_SPLIT || (p->automatic && nhwc_split && split_tail(g).items >= 2 * kSplitCus)
+        p->algo = algo == WINO_ALGO_SPLIT || (p->automatic && can_split && split_tail(g).items >= 2 * kSplitCus)
                       ? WINO_ALGO_SPLIT
                       : WINO_ALGO_STAGED;
         return WINO_OK;
@@ -350,7 +366,7 @@ size_t wino_filter_bytes_p(int C, int K, int m, unsigned prec) {
     if (prec == 0) return wino_filter_bytes(C, K, m);
     if (C <= 0 || K <= 0 || (m != 2 && m != 4) || prec_of(prec) <= 0 || (prec & ~WINO_PREC_MASK)) return 0;
     int64_t e;
-    if (!mul_ok((int64_t)(C + 15) / 16 * 16, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, (m + 2) * (m + 2), &e))
+    if (!mul_ok((int64_t)(C + 31) / 32 * 32, (int64_t)(K + 15) / 16 * 16, &e) || !mul_ok(e, (m + 2) * (m + 2), &e))
         return 0;
     return (size_t)e * 2;
 }
@@ -380,6 +396,7 @@ size_t wino_workspace_bytes_r(int N, int C, int H, int W, int K, int pad, int m,
     Plan p;
     if (make_geom_r(N, C, H, W, K, pad, m, r, &g) != WINO_OK || make_plan(g, flags, &p) != WINO_OK)
         return (size_t)-1;
+    if (prec_of(flags) && p.algo == WINO_ALGO_SPLIT) return split16_workspace(g);
     if (prec_of(flags)) return round_up(vh_bytes(g), 256) + m_elems(g) * sizeof(float);
     if (p.algo == WINO_ALGO_FUSED && p.cfg.nsl > 1) return slice_workspace(g, p.cfg.nsl);
     if (p.algo == WINO_ALGO_FUSED || p.algo == WINO_ALGO_LOWC) return 0;
@@ -444,6 +461,13 @@ int wino_conv2d_r(const float* x, const float* U, float* y, int N, int C, int H,
     if (overlap(x, xb, y, yb) || overlap(U, ub, y, yb)) return WINO_ERR_INVALID_ARG;
     const bool relu = (flags & WINO_FLAG_RELU) != 0;
     hipStream_t s = (hipStream_t)stream;
+    if (prec && p.algo == WINO_ALGO_SPLIT) {
+        const size_t need = split16_workspace(g);
+        if (!workspace || workspace_bytes < need) return WINO_ERR_WORKSPACE;
+        if (overlap(workspace, need, x, xb) || overlap(workspace, need, y, yb) || overlap(workspace, need, U, ub))
+            return WINO_ERR_INVALID_ARG;
+        return hip_status(launch_split16(x, U, y, workspace, g, prec, relu, s));
+    }
     if (prec) {
         const size_t vb = round_up(vh_bytes(g), 256);
         const size_t need = vb + m_elems(g) * sizeof(float);

@@ -102,6 +102,10 @@ struct VrowsPlan {
     size_t lds;
 };
 VrowsPlan vrows_plan(const Geom& g, int vec);
+// The split path on fp16 (prec 1) / bf16 (prec 2) operands: VH = the workspace
+// of split16_workspace bytes, UH from the 16-bit filter transform.
+hipError_t launch_split16(const float* x, const void* UH, float* y, void* VH, const Geom& g, int prec, bool relu,
+                          hipStream_t s);
 hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,
                         hipStream_t s);
 // Low-C path (C <= 4): a lane per tile, vector FMAs over the few channels.

@@ -36,6 +36,21 @@ __device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// The 16-bit form: fp16 (PREC 1) or bf16 (PREC 2), eight reduction slots per
+// lane in a 16-byte operand, fp32 accumulation.
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <int PREC>
+__device__ __forceinline__ f32x4 mfma16x16x32(uint4 a, uint4 b, f32x4 c) {
+    if constexpr (PREC == 1)
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b),
+                                                       c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                        __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
 // ------------------------------------------------------------------ helpers
 
 __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) { return (__umulhi(n, d.m) + n) >> d.l; }
@@ -1253,10 +1268,10 @@ __device__ __forceinline__ uint32_t to16(float v) {
 // partly covers is completed by the neighbouring workgroup).  VEC: 16-byte
 // loads of column chunks starting xsh columns before the patch.
 // LDS: [row r][channel][A rows][pitch] floats, shifted so that a tile's first
-// column sits at a multiple of 4.  OUT = 1 / 2: the 16-bit three-stage path's
-// VH (fp16 / bf16, 16-channel groups, a lane's word holding four channels):
-// the lane stores its channel's 16 bits, and a wave's store covers its quad's
-// 128 contiguous bytes of a group's position block; nq = 4 * C16.
+// column sits at a multiple of 4.  OUT = 1 / 2: the 16-bit paths' VH (fp16 /
+// bf16, 16-channel groups, a lane's word holding four channels): the lane
+// stores its channel's 16 bits, and a wave's store covers its quad's 128
+// contiguous bytes of a group's position block; nq = 4 * C16.
 template <int MT, int VEC, int OUT = 0>
 __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
                                                int R, int pitch, int nq) {
@@ -1482,6 +1497,108 @@ __device__ __forceinline__ void go_steps(const __amdgpu_buffer_rsrc_t vr, uint32
     __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
 }
 
+// The same GEMMs on 16-bit operands (fp16 PREC 1, bf16 PREC 2) for the
+// split path: v_mfma_f32_16x16x32_{f16,bf16} leaves its 16 x 16 result in the
+// lane layout of v_mfma_f32_16x16x4_f32 (lane = tile, four consecutive
+// filters), so the accumulators, and with them the epilogue, are the fp32
+// kernel's.  A step is one 32-channel chunk: groups 2s and 2s+1 of the blocked
+// VH ([block][C16][T][64][4 halves]), exactly the bytes of an fp32 step of 16
+// channels, so the V DMA and its two LDS stages are go_steps's.  A position's
+// B operand is the lane's 8-byte words of the two groups (two LDS reads); its
+// A operand the lane's word of chunk s of UH ([KB][C32][T][64][8 halves], one
+// 16-byte load).  The filters of position t come D positions ahead, into a
+// ring of D operand registers: after t's products the ring slot takes
+// position t + D (of this step, or of the next).  The V DMA of step s+1
+// goes out in three parts at positions 0, TH/3 and 2*TH/3 of step s.
+template <int MT, int H, int PREC>
+__device__ __forceinline__ void go_steps16(const __amdgpu_buffer_rsrc_t vr, uint32_t vbase0, uint32_t vbase1,
+                                           const __amdgpu_buffer_rsrc_t ur, uint32_t ubase, const Geom& g,
+                                           int nsteps, int wave, int lane, float* vs0, float* vs1,
+                                           f32x4 (&acc)[2][GoShape<MT>::TH]) {
+    using S = GoShape<MT>;
+    constexpr int A = S::A, X0 = H * S::RN, TH = S::TH, T = S::T;
+    // filter lead: a third of a step for F(4x4) (TH = 18; the kernel's VGPRs
+    // also hold the tail units' operands), half a step for F(2x2) (TH = 16)
+    constexpr int D = MT == 4 ? TH / 3 : TH / 2;
+    static_assert(TH % D == 0, "the ring wraps onto the next step's slots");
+    auto stage = [&](auto rc) -> float* {
+        if constexpr (decltype(rc)::value == 0) return vs0;
+        else return vs1;
+    };
+    const uint32_t tid16 = ((uint32_t)wave * 64 + lane) * 16u;
+    auto issue_v = [&](auto rc, int j, auto i0c, auto i1c) {
+        float* vs = stage(rc);
+        const uint32_t qoff = (uint32_t)j * T * 1024;             // bytes: two groups of T*512
+        static_for<decltype(i0c)::value, decltype(i1c)::value>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr uint32_t RUN = S::JV * 256 * 16;           // bytes of one block's run
+            constexpr uint32_t E0 = (uint32_t)i * 8192u;
+            float* dst = vs + (i * 512 + wave * 64) * 4;
+            if constexpr (E0 + 8192u <= RUN) {
+                lds_dma<16>(vr, dst, tid16, vbase0 + E0 + qoff);
+            } else if constexpr (E0 >= RUN) {
+                lds_dma<16>(vr, dst, tid16, vbase1 + (E0 - RUN) + qoff);
+            } else {
+                const uint32_t voff = tid16 < RUN - E0 ? tid16 : tid16 + (vbase1 - vbase0 - RUN);
+                lds_dma<16>(vr, dst, voff, vbase0 + E0 + qoff);
+            }
+        });
+    };
+    static_assert(T * 1024 == S::JV * 256 * 16, "a 16-bit step moves the bytes of an fp32 step");
+    const uint32_t l16 = (uint32_t)lane * 16u;
+    // A operand of (step s, position X0*A + t)
+    auto load_u = [&](int s, int t, uint4& u) {
+        const uint32_t go = __builtin_amdgcn_readfirstlane(ubase + (uint32_t)s * T * 1024u +
+                                                           (uint32_t)(X0 * A + t) * 1024u);
+        u = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ur, (int)l16, (int)go, 0));
+    };
+    // B operand of (block b, position X0*A + t) from a stage ([b][group][T][64][8 bytes])
+    auto v_op = [&](const float* vs, int b, int t) {
+        const uint2* w = (const uint2*)vs + (size_t)((b * 2) * T + X0 * A + t) * 64 + lane;
+        const uint2 a = w[0], c = w[(size_t)T * 64];
+        return make_uint4(a.x, a.y, c.x, c.y);
+    };
+    uint4 ur_[D];
+    // Loads a step issues after its last V DMA part: the filter loads of
+    // positions 2*PS .. TH-1, one each.  (The prologue issues D >= WAITN
+    // filter loads after step 0's V.)
+    constexpr int PS = TH / 3;
+    constexpr int WAITN = TH - 2 * PS;
+    static_assert(D >= WAITN, "the first wait covers step 0's V");
+    issue_v(IC<0>{}, 0, IC<0>{}, IC<S::JV>{});
+#pragma unroll
+    for (int t = 0; t < D; ++t) load_u(0, t, ur_[t]);
+    constexpr int JV = S::JV, JP = (JV + 2) / 3;
+    auto step = [&](auto rc, int s) {  // s % 2 == R
+        constexpr int R = decltype(rc)::value;
+        wait_vm_lds<WAITN>();          // V of step s has landed (this wave)
+        wg_barrier();                  // ... every wave's; stage R^1 (step s-1) is consumed
+        const float* vs = stage(IC<R>{});
+        const int sn = min(s + 1, nsteps - 1);
+        static_for<0, TH>([&](auto tc) {
+            constexpr int t = decltype(tc)::value;
+            if constexpr (t % PS == 0 && t / PS < 3) {
+                constexpr int P = t / PS;
+                constexpr int A0 = P * JP < JV ? P * JP : JV, A1 = (P + 1) * JP < JV ? (P + 1) * JP : JV;
+                issue_v(IC<R ^ 1>{}, s + 1, IC<A0>{}, IC<A1>{});
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            const uint4 v0 = v_op(vs, 0, t), v1 = v_op(vs, 1, t);
+            acc[0][t] = mfma16x16x32<PREC>(ur_[t % D], v0, acc[0][t]);
+            acc[1][t] = mfma16x16x32<PREC>(ur_[t % D], v1, acc[1][t]);
+            if constexpr (t + D < TH) load_u(s, t + D, ur_[t % D]);
+            else load_u(sn, t + D - TH, ur_[t % D]);
+        });
+    };
+    int s = 0;
+    for (; s + 2 <= nsteps; s += 2) {      // straight-line body: exact wait analysis
+        step(IC<0>{}, s);
+        step(IC<1>{}, s + 1);
+    }
+    if (s < nsteps) step(IC<0>{}, s);
+    __builtin_amdgcn_s_waitcnt(0);         // no load outlives the loop
+}
+
 // The tile of lane l16 in block tb (16 consecutive tiles).
 __device__ __forceinline__ TileCoord block_tile(int tb, int l16, const Geom& g) {
     return decode_tile(tb * 16 + l16, g);
@@ -1529,7 +1646,42 @@ __device__ __forceinline__ void unit_steps(const __amdgpu_buffer_rsrc_t vr, cons
     }
 }
 
-template <int MT>
+// The 16-bit form of unit_steps: 32-channel chunks [c0, c1) of tile block
+// (vr) and filter block (ubase into UH); per chunk and half of the wave's TH
+// positions, the operands straight to registers (one 16-byte filter load, two
+// 8-byte V loads per position), then their products.
+template <int MT, int H, int PREC>
+__device__ __forceinline__ void unit_steps16(const __amdgpu_buffer_rsrc_t vr, const __amdgpu_buffer_rsrc_t ur,
+                                             uint32_t ubase, int c0, int c1, int lane,
+                                             f32x4 (&acc)[GoShape<MT>::TH]) {
+    using S = GoShape<MT>;
+    constexpr int A = S::A, X0 = H * S::RN, TH = S::TH, T = S::T, HT = TH / 2;
+    static_assert(TH % 2 == 0, "two halves");
+    const uint32_t l16 = (uint32_t)lane * 16u, l8 = (uint32_t)lane * 8u;
+    for (int c = c0; c < c1; ++c) {
+        const uint32_t uo = __builtin_amdgcn_readfirstlane(ubase + (uint32_t)c * T * 1024u + (uint32_t)(X0 * A) * 1024u);
+        const uint32_t vo = __builtin_amdgcn_readfirstlane((uint32_t)c * T * 1024u + (uint32_t)(X0 * A) * 512u);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            uint4 u[HT], v[HT];
+#pragma unroll
+            for (int i = 0; i < HT; ++i) {
+                const uint32_t t = (uint32_t)(hh * HT + i);
+                u[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ur, (int)l16, (int)(uo + t * 1024u), 0));
+                const uint2 a = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(vr, (int)l8, (int)(vo + t * 512u), 0));
+                const uint2 b = __builtin_bit_cast(
+                    uint2, __builtin_amdgcn_raw_buffer_load_b64(vr, (int)l8, (int)(vo + (uint32_t)T * 512u + t * 512u), 0));
+                v[i] = make_uint4(a.x, a.y, b.x, b.y);
+            }
+#pragma unroll
+            for (int i = 0; i < HT; ++i) acc[hh * HT + i] = mfma16x16x32<PREC>(u[i], v[i], acc[hh * HT + i]);
+        }
+    }
+}
+
+// PREC 0: fp32 (nq = ncq4*4 channel quads per Vb block); 1 / 2: 16-bit (VH
+// and UH, ncq4 = C32 chunks).
+template <int MT, int PREC = 0>
 __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, const float* __restrict__ U,
                                               float* __restrict__ y, const Geom& g, int tb, int kb, int ncq4,
                                               bool relu, bool vec_ok, float4* vs0, float4* vs1, int wave,
@@ -1539,27 +1691,37 @@ __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, cons
     static_assert(4 * NV * 64 <= S::VST, "four partial-output slots per LDS stage");
     static_assert(VPW % MT == 0, "whole output rows per wave");
     const int h = wave % TS, cp = wave / TS;
-    const int nq = ncq4 * 4;
+    const int nq = PREC ? ncq4 : ncq4 * 4;                  // quads, or 32-channel chunks
     const int qpp = (nq + CP - 1) / CP;
     const int q0 = min(cp * qpp, nq), q1 = min(nq, q0 + qpp);
-    const size_t blk_b = (size_t)nq * T * 256;
+    const size_t blk_b = PREC ? (size_t)nq * T * 1024 : (size_t)nq * T * 256;
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)((const char*)Vb + (size_t)tb * blk_b), (short)0, (int)(blk_b < kInvalid ? blk_b : kInvalid),
         kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t ur = u_rsrc(U, g);
     f32x4 acc[TH];
 #pragma unroll
     for (int t = 0; t < TH; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float o[4][MT][MT];
+    auto steps = [&](auto hc) {
+        constexpr int HH = decltype(hc)::value;
+        if constexpr (PREC == 0) {
+            unit_steps<MT, HH>(vr, u_rsrc(U, g), g, kb, q0, q1, lane, acc);
+        } else {
+            const size_t uh_b = (size_t)g.KB * nq * T * 1024;
+            const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)U, (short)0, (int)(uh_b < 0x7fffffffu ? uh_b : 0x7fffffffu), kRsrcWord3);
+            unit_steps16<MT, HH, PREC>(vr, ur, (uint32_t)kb * (uint32_t)nq * T * 1024u, q0, q1, lane, acc);
+        }
+    };
     if constexpr (TS == 1) {
-        unit_steps<MT, 0>(vr, ur, g, kb, q0, q1, lane, acc);
+        steps(IC<0>{});
         fused_share<MT, 1, 1, 16, 0, 0>(acc, o);
     } else {
         if (h == 0) {
-            unit_steps<MT, 0>(vr, ur, g, kb, q0, q1, lane, acc);
+            steps(IC<0>{});
             fused_share<MT, 2, 1, 16, 0, 0>(acc, o);
         } else {
-            unit_steps<MT, 1>(vr, ur, g, kb, q0, q1, lane, acc);
+            steps(IC<1>{});
             fused_share<MT, 2, 1, 16, 0, 1>(acc, o);
         }
     }
@@ -1611,7 +1773,9 @@ __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, cons
     }
 }
 
-template <int MT>
+// PREC 0: fp32 operands (Vb, U); 1 / 2: fp16 / bf16 (VH in 16-channel groups,
+// UH in 32-channel chunks), through go_steps16 (and unit_steps16 for the tail).
+template <int MT, int PREC = 0>
 __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, const float* __restrict__ U,
                                                   float* __restrict__ y, Geom g, FusedTiling ft, int nb,
                                                   int relu, int vec_ok, int ntail) {
@@ -1636,7 +1800,8 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
         decode(it, kgi, tp);
         const int tb = 2 * tp + sub / KGW, kb = kgi * KGW + sub % KGW;
         if (tb >= nb || kb >= g.KB) return;
-        gemm_out_unit<MT>(Vb, U, y, g, tb, kb, (g.CQ + 3) / 4, relu != 0, vec_ok != 0, vs0, vs1, wave, lane);
+        gemm_out_unit<MT, PREC>(Vb, U, y, g, tb, kb, PREC ? (g.C + 31) / 32 : (g.CQ + 3) / 4, relu != 0,
+                                vec_ok != 0, vs0, vs1, wave, lane);
         return;
     }
     const int item = (b & 7) * ft.per + (b >> 3);
@@ -1648,7 +1813,8 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
     const int cl = lane >> 4;
 
     // Vb as a buffer: a block past the last reads zeros
-    const size_t blk_b = (size_t)((g.CQ + 3) / 4 * 4) * g.T * 256;   // bytes of one tile block
+    const size_t blk_b = PREC ? (size_t)((g.C + 31) / 32) * g.T * 1024   // bytes of one tile block
+                              : (size_t)((g.CQ + 3) / 4 * 4) * g.T * 256;
     const size_t tot_b = (size_t)nb * blk_b;
     const size_t first = (size_t)(2 * tp) * blk_b;
     const size_t left = tot_b - first;
@@ -1662,7 +1828,20 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
         for (int t = 0; t < TH; ++t) acc[bb][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float* v0 = (float*)vs0;
     float* v1 = (float*)vs1;
-    if constexpr (TS == 1) {
+    if constexpr (PREC != 0) {
+        // UH as a buffer (the host keeps it below 2 GiB)
+        const int c32 = (g.C + 31) / 32;
+        const size_t uh_b = (size_t)g.KB * c32 * g.T * 1024;
+        const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)U, (short)0, (int)(uh_b < 0x7fffffffu ? uh_b : 0x7fffffffu), kRsrcWord3);
+        const uint32_t ubase = (uint32_t)kb * (uint32_t)c32 * (uint32_t)g.T * 1024u;
+        if constexpr (TS == 1) {
+            go_steps16<MT, 0, PREC>(vr, 0u, (uint32_t)blk_b, ur, ubase, g, ft.nsteps, wave, lane, v0, v1, acc);
+        } else {
+            if (h == 0) go_steps16<MT, 0, PREC>(vr, 0u, (uint32_t)blk_b, ur, ubase, g, ft.nsteps, wave, lane, v0, v1, acc);
+            else go_steps16<MT, 1, PREC>(vr, 0u, (uint32_t)blk_b, ur, ubase, g, ft.nsteps, wave, lane, v0, v1, acc);
+        }
+    } else if constexpr (TS == 1) {
         go_steps<MT, 0>(vr, 0u, (uint32_t)blk_b, U, g, ft.nsteps, kb, wave, lane, v0, v1, acc);
     } else {
         if (h == 0) go_steps<MT, 0>(vr, 0u, (uint32_t)blk_b, U, g, ft.nsteps, kb, wave, lane, v0, v1, acc);
@@ -1856,15 +2035,20 @@ __global__ __launch_bounds__(256) void k_lowc(const float* __restrict__ x, const
 // Reduced-precision three-stage path: U and V are rounded to fp16 (PREC 1) or
 // bf16 (PREC 2), to nearest with ties to even, and the T per-position GEMMs run
 // on v_mfma_f32_16x16x32_{f16,bf16} with fp32 accumulation; M and the output
-// transform stay fp32.  The 16-bit layouts hold 16-channel groups, a lane
-// carrying four consecutive channels of its group:
-//   UH[KB][C16][T][64][4]: element (t, c, k) at lane ((c%16)/4)*16 + k%16, half c%4
+// transform stay fp32.  Filters come in 32-channel chunks, a lane carrying
+// eight channels of its chunk -- four consecutive channels of each of its two
+// 16-channel groups -- in one 16-byte word; inputs in 16-channel groups, a lane
+// carrying four consecutive channels in one 8-byte word:
+//   UH[KB][C32][T][64][8]: element (t, c, k) at lane ((c%16)/4)*16 + k%16,
+//                          half ((c%32)/16)*4 + c%4
 //   VH[PB][C16][T][64][4]: element (t, c, p) at lane ((c%16)/4)*16 + p%16, half c%4
-// (C16 = ceil(C/16), padding zero): one 8-byte word per lane and position.
-// The MFMA's 16-byte operand of lane l holds A[l%16] (or B[.][l%16]) at eight
-// reduction slots, here two such words: groups 2j and 2j+1.
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+// (C32 = ceil(C/32), C16 = 2*C32 groups, padding zero).  A UH word is exactly
+// the lane's A operand of v_mfma_f32_16x16x32_{f16,bf16} (A[l%16] at eight
+// reduction slots): one 16-byte load; the B operand is the lane's VH words of
+// groups 2j and 2j+1 side by side.  The filter transform writes one 16-channel
+// group at a time, the lane's 8-byte half (c%32)/16 of each word; the input
+// transforms write whole 8-byte words (as 16-bit values of one channel per
+// lane of a quad, 128 contiguous bytes per store, for k_vrows).
 
 
 template <int PREC>
@@ -1872,18 +2056,11 @@ __device__ __forceinline__ uint2 pack16(float a, float b, float c, float d) {
     return make_uint2(to16<PREC>(a) | (to16<PREC>(b) << 16), to16<PREC>(c) | (to16<PREC>(d) << 16));
 }
 
-template <int PREC>
-__device__ __forceinline__ f32x4 mfma16x16x32(uint4 a, uint4 b, f32x4 c) {
-    if constexpr (PREC == 1)
-        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b),
-                                                       c, 0, 0, 0);
-    else
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                        __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
 
 // One wave per (16-filter block, 16-channel group): lane = (k%16, channel
-// quad); four channels' transforms per lane, one 8-byte store per position.
+// quad); four channels' transforms per lane, one 8-byte store per position
+// (positions 128 words apart: the other half of each 16-byte word is the
+// chunk's other group).
 template <int MT, int PREC, int... G>
 __device__ __forceinline__ void filter16_groups(const float (&gg)[4][3][3], uint2* __restrict__ dst,
                                                 std::integer_sequence<int, G...>) {
@@ -1892,22 +2069,23 @@ __device__ __forceinline__ void filter16_groups(const float (&gg)[4][3][3], uint
         float4 f[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) f[e] = filter_tf4<MT, 4 * GG>(gg[e]);
-        dst[(4 * GG + 0) * 64] = pack16<PREC>(f[0].x, f[1].x, f[2].x, f[3].x);
-        dst[(4 * GG + 1) * 64] = pack16<PREC>(f[0].y, f[1].y, f[2].y, f[3].y);
-        dst[(4 * GG + 2) * 64] = pack16<PREC>(f[0].z, f[1].z, f[2].z, f[3].z);
-        dst[(4 * GG + 3) * 64] = pack16<PREC>(f[0].w, f[1].w, f[2].w, f[3].w);
+        dst[(4 * GG + 0) * 128] = pack16<PREC>(f[0].x, f[1].x, f[2].x, f[3].x);
+        dst[(4 * GG + 1) * 128] = pack16<PREC>(f[0].y, f[1].y, f[2].y, f[3].y);
+        dst[(4 * GG + 2) * 128] = pack16<PREC>(f[0].z, f[1].z, f[2].z, f[3].z);
+        dst[(4 * GG + 3) * 128] = pack16<PREC>(f[0].w, f[1].w, f[2].w, f[3].w);
     };
     (one(std::integral_constant<int, G>{}), ...);
 }
 
+// C16P = 2 * C32 groups per filter block (a padding group is written zero).
 template <int MT, int PREC>
 __global__ __launch_bounds__(256) void k_filter16(const float* __restrict__ gw, uint2* __restrict__ UH, int C,
-                                                  int K, int C16, long nw) {
+                                                  int K, int C16P, long nw) {
     constexpr int T = (MT + 2) * (MT + 2), TG = T / 4;
     const int lane = threadIdx.x & 63;
     const long w = (long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (w >= nw) return;
-    const int kb = (int)(w / C16), c16 = (int)(w % C16);
+    const int kb = (int)(w / C16P), c16 = (int)(w % C16P);
     const int k = kb * 16 + (lane & 15), c0 = c16 * 16 + (lane >> 4) * 4;
     float gg[4][3][3];
 #pragma unroll
@@ -1919,12 +2097,13 @@ __global__ __launch_bounds__(256) void k_filter16(const float* __restrict__ gw, 
 #pragma unroll
             for (int s2 = 0; s2 < 3; ++s2) gg[e][r][s2] = ok ? src[r * 3 + s2] : 0.0f;
     }
-    filter16_groups<MT, PREC>(gg, UH + (size_t)w * T * 64 + lane, std::make_integer_sequence<int, TG>{});
+    uint2* dst = UH + (((size_t)kb * (C16P >> 1) + (c16 >> 1)) * T * 64 + lane) * 2 + (c16 & 1);
+    filter16_groups<MT, PREC>(gg, dst, std::make_integer_sequence<int, TG>{});
 }
 
 // One wave per (16-tile block, 16-channel group), XCD-contiguous runs; lane =
 // (tile p%16, channel quad): four regions, their transforms packed four
-// channels to an 8-byte word.
+// channels to an 8-byte word.  C16 = 2 * C32 groups (a padding group: zeros).
 template <int MT, int PREC>
 __global__ __launch_bounds__(256) void k_input16(const float* __restrict__ x, uint2* __restrict__ VH, Geom g,
                                                  int C16, long nwg) {
@@ -1969,19 +2148,18 @@ __global__ __launch_bounds__(256) void k_input16(const float* __restrict__ x, ui
 }
 
 // The T GEMMs on 16-bit operands, on v_mfma_f32_16x16x32_{f16,bf16}: one
-// instruction takes two 16-channel groups, the lane's words of groups 2j and
-// 2j+1 side by side in its 16-byte operand (A and B place the same channel in
-// the same operand slot, so the instruction's reduction covers all 32).
-// Workgroup = NP positions x 8 k-blocks x 8 p-blocks, 8 waves of NP x 4
-// k-blocks x 2 p-blocks each (XCD-contiguous item order).  A chunk of 32
-// channels is 16*NP pairs (U of position x k-block, then V of position x
-// p-block) of two 512-byte group blocks and comes into one of three LDS stages
-// by DMA two chunks ahead: one 16-byte load per lane moves one pair (lanes
-// 0-31 the first group, 32-63 the second).  Blocks and groups past the last
-// read zero.
+// instruction takes a 32-channel chunk, the lane's 16-byte word of UH and of
+// VH (A and B place the same channel in the same operand slot, so the
+// instruction's reduction covers all 32).  Workgroup = NP positions x 8
+// k-blocks x 8 p-blocks, 8 waves of NP x 4 k-blocks x 2 p-blocks each
+// (XCD-contiguous item order).  A chunk is 16*NP 1 KB blocks (U of position x
+// k-block: one UH block; then V of position x p-block: the two 512-byte group
+// blocks of VH, lanes 0-31 the first, 32-63 the second) and comes into one of
+// three LDS stages by DMA two chunks ahead, one 16-byte load per lane and
+// block.  Blocks past the last read zero.
 template <int PREC, int NP>
 __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, const uint2* __restrict__ VH,
-                                                float* __restrict__ M, Geom g, int C16) {
+                                                float* __restrict__ M, Geom g, int C32) {
     constexpr int NPAIR = 16 * NP, PPW = NPAIR / 8;       // pairs per chunk, per wave
     __shared__ uint4 st0[NPAIR * 64], st1[NPAIR * 64], st2[NPAIR * 64];   // three stages of pairs x 1 KB
     const int T = g.T, TN = g.T / NP;
@@ -1996,9 +2174,9 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wk = wave >> 2, wp = wave & 3;              // k-blocks 4*wk .. +3, p-blocks 2*wp, +1
-    const int NC = (C16 + 1) / 2;
-    const uint32_t gstride = (uint32_t)T * 512;          // bytes between groups of one block
-    const uint32_t bstride = (uint32_t)C16 * gstride;    // bytes between blocks
+    const int NC = C32;
+    const uint32_t gstride = (uint32_t)T * 1024;         // bytes between chunks of one block
+    const uint32_t bstride = (uint32_t)C32 * gstride;    // bytes between blocks (UH and VH alike)
     // U and V of this item's blocks as buffers: a block past the last reads zeros
     const size_t ub = (size_t)min(g.KB - kb0, 8) * bstride, vb = (size_t)min(g.PB - pb0, 8) * bstride;
     const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
@@ -2011,18 +2189,21 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
         else if constexpr (S == 1) return st1;
         else return st2;
     };
-    // DMA of chunk c into stage sc: wave w moves pairs PPW*w .. PPW*w+PPW-1.
-    const uint32_t lane_off = (uint32_t)(lane >> 5) * gstride + (uint32_t)(lane & 31) * 16u;
+    // DMA of chunk c into stage sc: wave w moves blocks PPW*w .. PPW*w+PPW-1.
+    const uint32_t u_off = (uint32_t)lane * 16u;
+    const uint32_t v_off = (uint32_t)(lane >> 5) * (uint32_t)T * 512u + (uint32_t)(lane & 31) * 16u;
     auto issue = [&](auto sc, int c) {
         uint4* s = stage(sc);
-        const bool g1ok = 2 * c + 1 < C16;
-        const uint32_t voff = lane_off + ((lane >> 5) && !g1ok ? kInvalid : 0u);
 #pragma unroll
         for (int i = 0; i < PPW; ++i) {
             const int q = wave * PPW + i, qq = q < 8 * NP ? q : q - 8 * NP, pos = qq >> 3, blk = qq & 7;
-            const uint32_t soff = (uint32_t)blk * bstride + (uint32_t)(2 * c) * gstride + (uint32_t)(t0 + pos) * 512u;
-            if (q < 8 * NP) lds_dma<16>(ur, (float*)(s + q * 64), voff, __builtin_amdgcn_readfirstlane(soff));
-            else lds_dma<16>(vr, (float*)(s + q * 64), voff, __builtin_amdgcn_readfirstlane(soff));
+            if (q < 8 * NP) {
+                const uint32_t soff = (uint32_t)blk * bstride + (uint32_t)c * gstride + (uint32_t)(t0 + pos) * 1024u;
+                lds_dma<16>(ur, (float*)(s + q * 64), u_off, __builtin_amdgcn_readfirstlane(soff));
+            } else {
+                const uint32_t soff = (uint32_t)blk * bstride + (uint32_t)c * gstride + (uint32_t)(t0 + pos) * 512u;
+                lds_dma<16>(vr, (float*)(s + q * 64), v_off, __builtin_amdgcn_readfirstlane(soff));
+            }
         }
     };
     f32x4 acc[NP][4][2];
@@ -2033,7 +2214,9 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
 #pragma unroll
             for (int j = 0; j < 2; ++j) acc[p][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     // operand of lane l from pair q: its words of both groups
-    auto operand = [&](const uint4* s, int q) {
+    // U: the lane's word; V: the lane's words of the two groups
+    auto u_operand = [&](const uint4* s, int q) { return s[q * 64 + lane]; };
+    auto v_operand = [&](const uint4* s, int q) {
         const uint2* w = (const uint2*)(s + q * 64);
         const uint2 a = w[lane], b = w[64 + lane];
         return make_uint4(a.x, a.y, b.x, b.y);
@@ -2055,9 +2238,9 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
         for (int p = 0; p < NP; ++p) {
             uint4 a[4], b[2];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = operand(s, p * 8 + wk * 4 + i);
+            for (int i = 0; i < 4; ++i) a[i] = u_operand(s, p * 8 + wk * 4 + i);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = operand(s, 8 * NP + p * 8 + wp * 2 + j);
+            for (int j = 0; j < 2; ++j) b[j] = v_operand(s, 8 * NP + p * 8 + wp * 2 + j);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -2087,21 +2270,22 @@ __global__ __launch_bounds__(512) void k_gemm16(const uint2* __restrict__ UH, co
 static inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 hipError_t launch_filter_transform16(const float* gw, void* UH, int C, int K, int m, int prec, hipStream_t s) {
-    const int C16 = (C + 15) / 16, KB = (K + 15) / 16;
-    const long waves = (long)KB * C16;
+    // every group of C32 chunks (a padding group is written zero)
+    const int C16P = (C + 31) / 32 * 2, KB = (K + 15) / 16;
+    const long waves = (long)KB * C16P;
     if ((waves + 3) / 4 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
     uint2* u = (uint2*)UH;
-    if (m == 2 && prec == 1) hipLaunchKernelGGL((k_filter16<2, 1>), grid, block, 0, s, gw, u, C, K, C16, waves);
-    else if (m == 2) hipLaunchKernelGGL((k_filter16<2, 2>), grid, block, 0, s, gw, u, C, K, C16, waves);
-    else if (prec == 1) hipLaunchKernelGGL((k_filter16<4, 1>), grid, block, 0, s, gw, u, C, K, C16, waves);
-    else hipLaunchKernelGGL((k_filter16<4, 2>), grid, block, 0, s, gw, u, C, K, C16, waves);
+    if (m == 2 && prec == 1) hipLaunchKernelGGL((k_filter16<2, 1>), grid, block, 0, s, gw, u, C, K, C16P, waves);
+    else if (m == 2) hipLaunchKernelGGL((k_filter16<2, 2>), grid, block, 0, s, gw, u, C, K, C16P, waves);
+    else if (prec == 1) hipLaunchKernelGGL((k_filter16<4, 1>), grid, block, 0, s, gw, u, C, K, C16P, waves);
+    else hipLaunchKernelGGL((k_filter16<4, 2>), grid, block, 0, s, gw, u, C, K, C16P, waves);
     return hipGetLastError();
 }
 
 hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, float* M, const Geom& g, int prec,
                            bool relu, hipStream_t s) {
-    const int C16 = (g.C + 15) / 16;
+    const int C32 = (g.C + 31) / 32, C16 = 2 * C32;   // groups of the input transforms
     const long waves = (long)g.PB * C16, nwg = (waves + 3) / 4;
     if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 gi((unsigned)((nwg + 7) / 8 * 8)), block(256);
@@ -2137,15 +2321,15 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
     if (e != hipSuccess) return e;
     // one position per workgroup: 48 KB of LDS, so up to three workgroups share a CU
     constexpr int NP = 1;
-    if ((size_t)8 * C16 * g.T * 512 >= (size_t)kInvalid) return hipErrorInvalidConfiguration;   // 32-bit offsets
+    if ((size_t)8 * C32 * g.T * 1024 >= (size_t)kInvalid) return hipErrorInvalidConfiguration;   // 32-bit offsets
     const long nitems = (long)((g.PB + 7) / 8) * ((g.KB + 7) / 8) * (g.T / NP);
     const long wgs = (nitems + 7) / 8 * 8;
     if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 b512(512);
     if (prec == 1)
-        hipLaunchKernelGGL((k_gemm16<1, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C16);
+        hipLaunchKernelGGL((k_gemm16<1, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C32);
     else
-        hipLaunchKernelGGL((k_gemm16<2, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C16);
+        hipLaunchKernelGGL((k_gemm16<2, NP>), dim3((unsigned)wgs), b512, 0, s, (const uint2*)UH, vh, M, g, C32);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_output_transform(M, y, g, relu, s);
@@ -2938,6 +3122,61 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
     hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, nb, (int)relu, vec_ok,
                        (int)st.tail);
     return hipGetLastError();
+}
+
+// The split path on 16-bit operands: the input transform into VH blocks of
+// 2*C32 groups (by tile rows, or per 16-tile block for very wide images), then
+// the GEMMs + output transform on 16-bit MFMAs (the last items as units, as
+// for fp32).
+template <int MT, int PREC>
+static hipError_t split16_instance(const float* x, const void* UH, float* y, void* VH, const Geom& g, bool relu,
+                                   hipStream_t s) {
+    using GS = GoShape<MT>;
+    const int c32 = (g.C + 31) / 32, c16p = 2 * c32;
+    const int vec = g.W % 4 == 0 && aligned(x, 16);
+    const VrowsPlan vp = vrows_plan(g, vec);
+    if (vp.R > 0) {
+        const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
+        const dim3 gr((unsigned)(ngr * 4 * c16p)), b256(256);
+        if (vec) hipLaunchKernelGGL((k_vrows<MT, 1, PREC>), gr, b256, vp.lds, s, x, (float*)VH, g, vp.R, vp.pitch,
+                                    4 * c16p);
+        else hipLaunchKernelGGL((k_vrows<MT, 0, PREC>), gr, b256, vp.lds, s, x, (float*)VH, g, vp.R, vp.pitch,
+                                4 * c16p);
+    } else {
+        const long waves = (long)g.PB * c16p, nwg = (waves + 3) / 4;
+        if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL((k_input16<MT, PREC>), dim3((unsigned)((nwg + 7) / 8 * 8)), dim3(256), 0, s, x,
+                           (uint2*)VH, g, c16p, nwg);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    FusedTiling ft{};
+    const int nb = (int)split_blocks(g);
+    const SplitTail st = split_tail(g);
+    ft.nt = (nb + 1) / 2;
+    ft.nkg = (g.KB + GS::KGW - 1) / GS::KGW;
+    ft.per = (int)(((long)ft.nt * ft.nkg - st.tail + 7) / 8);
+    ft.nsteps = c32;
+    {   // item order: V of a tile pair is read by every filter group
+        const double vb = 1024.0 * nb * c32 * g.T, ub = 1024.0 * g.T * c32 * g.KB;
+        const double sets = (double)ft.nt * ft.nkg / 32.0;
+        const double group_major = vb * ft.nkg + ub * sets / ft.nkg;
+        const double tile_major = vb + ub * sets * (ft.nkg < 32 ? 1.0 : 32.0 / ft.nkg);
+        ft.kfast = tile_major < group_major ? 1 : 0;
+    }
+    const dim3 grid((unsigned)(8 * ft.per + st.tail * st.units)), block(512);
+    const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
+    hipLaunchKernelGGL((k_gemm_out<MT, PREC>), grid, block, 0, s, (const float*)VH, (const float*)UH, y, g, ft, nb,
+                       (int)relu, vec_ok, (int)st.tail);
+    return hipGetLastError();
+}
+
+hipError_t launch_split16(const float* x, const void* UH, float* y, void* VH, const Geom& g, int prec, bool relu,
+                          hipStream_t s) {
+    if (g.m == 2) return prec == 1 ? split16_instance<2, 1>(x, UH, y, VH, g, relu, s)
+                                   : split16_instance<2, 2>(x, UH, y, VH, g, relu, s);
+    return prec == 1 ? split16_instance<4, 1>(x, UH, y, VH, g, relu, s)
+                     : split16_instance<4, 2>(x, UH, y, VH, g, relu, s);
 }
 
 hipError_t launch_split(const float* x, const float* U, float* y, float* Vb, const Geom& g, int bw, bool relu,

@@ -227,9 +227,10 @@ def test_nhwc_entry_points():
 
 def test_16bit_operand_entry_points():
     F16, BF16 = B.WINO_PREC_F16, B.WINO_PREC_BF16
-    # UH: 2 bytes x T x roundup(C,16) x roundup(K,16)
+    # UH: 2 bytes x T x roundup(C,32) x roundup(K,16)
     assert B.wino_filter_bytes_p(20, 20, 4, F16) == 2 * 36 * 32 * 32
     assert B.wino_filter_bytes_p(20, 20, 2, BF16) == 2 * 16 * 32 * 32
+    assert B.wino_filter_bytes_p(37, 5, 4, F16) == 2 * 36 * 64 * 16    # C in 32-channel chunks
     assert B.wino_filter_bytes_p(20, 20, 4, 0) == B.wino_filter_bytes(20, 20, 4)
     assert B.wino_filter_bytes_p(20, 20, 4, 0x30) == 0          # both formats at once
     assert B.wino_filter_bytes_p(20, 20, 3, F16) == 0
@@ -237,8 +238,18 @@ def test_16bit_operand_entry_points():
     ws = B.wino_workspace_bytes(1, 20, 16, 16, 20, 1, 4, F16)
     vh = 1 * 2 * 36 * 64 * 8                                  # PB = 1 (16 tiles), C16 = 2
     assert ws == (vh + 255) // 256 * 256 + B.wino_gemm_out_bytes(1, 20, 16, 16, 1, 4)
-    for flags in (F16 | B.WINO_ALGO_FUSED, BF16 | B.WINO_ALGO_SPLIT, F16 | B.WINO_ALGO_LOWC, 0x30):
+    for flags in (F16 | B.WINO_ALGO_FUSED, F16 | B.WINO_ALGO_LOWC, 0x30):
         assert B.wino_workspace_bytes(1, 20, 16, 16, 20, 1, 4, flags) == 2**64 - 1
+    # the split path on 16-bit operands: VH of C16 rounded up to even groups
+    # (2 for C = 20: one 32-channel step; 4 for C = 40), no M
+    assert B.wino_workspace_bytes(1, 20, 16, 16, 20, 1, 4, BF16 | B.WINO_ALGO_SPLIT) == 1 * 2 * 36 * 64 * 8
+    assert B.wino_workspace_bytes(1, 40, 16, 16, 20, 1, 2, F16 | B.WINO_ALGO_SPLIT) == 4 * 4 * 16 * 64 * 8   # 8x8 tiles
+    # AUTO: the three stages on small layers, split from two rounds of split
+    # items on (N=64, 256 channels, 56x56: 392 tile-block pairs x 4 filter groups)
+    assert B.wino_plan_r(1, 20, 16, 16, 20, 1, 4, 3, F16)[1] == B.WINO_ALGO_STAGED
+    st, algo, _ = B.wino_plan_r(64, 256, 56, 56, 256, 1, 4, 3, F16)
+    assert st == B.WINO_OK and algo == B.WINO_ALGO_SPLIT
+    assert B.wino_workspace_bytes(64, 256, 56, 56, 256, 1, 4, F16) == 392 * 2 * 16 * 36 * 64 * 8
     assert B.wino_workspace_bytes_r(1, 20, 16, 16, 20, 2, 2, 5, F16) == 2**64 - 1   # 3x3 only
     assert B.wino_filter_transform_p(None, FAKE, 4, 4, 4, F16) == B.WINO_ERR_INVALID_ARG
     assert B.wino_filter_transform_p(FAKE, FAKE + 0x10000, 4, 4, 4, 0x40) == B.WINO_ERR_UNSUPPORTED

@@ -35,13 +35,14 @@ def filter16(g, m, flag):
     return U, nb
 
 
-def unpack_UH(raw: np.ndarray, C, K, m):
-    """UH[KB][C16][T][64][4] (lane = ((c%16)/4)*16 + k%16, half c%4) -> [T][C][K]."""
+def unpack_UH(raw: np.ndarray, C, K, m, full=False):
+    """UH[KB][C32][T][64][8] (lane = ((c%16)/4)*16 + k%16, half ((c%32)/16)*4 +
+    c%4) -> [T][C][K] (full: with the padding, [T][32*C32][16*KB])."""
     T = (m + 2) ** 2
-    C16, KB = -(-C // 16), -(-K // 16)
-    a = raw[:KB * C16 * T * 256].reshape(KB, C16, T, 4, 16, 4)          # kb, c16, t, cq, kl, e
-    a = a.transpose(2, 1, 3, 5, 0, 4).reshape(T, C16 * 16, KB * 16)     # t, c, k
-    return a[:, :C, :K]
+    C32, KB = -(-C // 32), -(-K // 16)
+    a = raw[:KB * C32 * T * 512].reshape(KB, C32, T, 4, 16, 2, 4)       # kb, c32, t, q, kl, half group, e
+    a = a.transpose(2, 1, 5, 3, 6, 0, 4).reshape(T, C32 * 32, KB * 16)  # t, c, k
+    return a if full else a[:, :C, :K]
 
 
 @pytest.mark.parametrize("prec", list(PRECS))
@@ -61,14 +62,10 @@ def test_filter_transform_16(prec, m, C, K):
     # double-rounding ties, and never more than one 16-bit ulp away
     assert np.all(np.abs(got - want) <= 2 * u * np.abs(U64) + 1e-30)
     assert np.mean(got == want) > 0.999
-    full = from16(raw, prec)
-    T = (m + 2) ** 2
-    C16, KB = -(-C // 16), -(-K // 16)
-    pad = np.ones((T, C16 * 16, KB * 16), bool)
+    allv = unpack_UH(from16(raw, prec), C, K, m, full=True)
+    pad = np.ones(allv.shape, bool)
     pad[:, :C, :K] = False
-    allv = full[:KB * C16 * T * 256].reshape(KB, C16, T, 4, 16, 4).transpose(2, 1, 3, 5, 0, 4).reshape(
-        T, C16 * 16, KB * 16)
-    assert np.all(allv[pad] == 0)
+    assert allv.size * 2 == nb and np.all(allv[pad] == 0)
 
 
 def conv16(x, U16, K, pad, m, flag, relu=False):
@@ -138,3 +135,77 @@ def test_error_study_at_layer_size(prec, m):
     err = h.normwise_err(y, direct.conv2d(x, g, 1))
     print(f"error study {prec} m={m}: normwise {err:.3e}", flush=True)
     assert err <= STUDY[(prec, m)]
+
+
+# (N, C, H, W, K, pad): ragged tiles; C not a multiple of 16 or 32 (an odd
+# number of 16-channel groups: a zero padding group); K not a multiple of 16;
+# several tile-block pairs and filter groups; a last partial tile block
+SPLIT_SHAPES = [(1, 16, 17, 23, 20, 1), (2, 40, 30, 30, 80, 1), (3, 8, 13, 11, 33, 2), (1, 1, 1, 1, 1, 1),
+                (2, 48, 20, 20, 64, 1), (1, 96, 12, 12, 130, 1)]
+
+
+@pytest.mark.parametrize("prec", list(PRECS))
+@pytest.mark.parametrize("m", [2, 4])
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv2d_16_split(prec, m, shape):
+    # The split path on 16-bit operands against the reduced-precision reference,
+    # and against the three 16-bit stages on the same data: the same rounded U
+    # and V and the same 32-channel MFMA sequence, so the two differ only in the
+    # output transform's fp32 summation order.
+    flag, u, rnd = PRECS[prec]
+    N, C, H, W, K, pad = shape
+    print(f"conv2d split {prec} m={m} shape={shape}", flush=True)
+    rng = np.random.default_rng(sum(shape) + 31 * m)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    U16, _ = filter16(g, m, flag)
+    y = conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_SPLIT)
+    y16, bound = reference_and_bound(x, g, pad, m, rnd)
+    assert np.all(np.isfinite(y))
+    tol = (2 * u + 4 * C * 2.0 ** -24 + 2.0 ** -20) * bound
+    assert np.all(np.abs(y - y16) <= tol + 1e-30)
+    assert h.normwise_err(y, direct.conv2d(x, g, pad)) <= STUDY[(prec, m)]
+    ys = conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_STAGED)
+    assert np.all(np.abs(y - ys) <= 16 * 2.0 ** -24 * bound + 1e-30)
+    yr = conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_SPLIT, relu=True)
+    assert np.array_equal(yr, np.maximum(y, 0.0))
+
+
+@pytest.mark.parametrize("prec", list(PRECS))
+def test_conv2d_16_auto_takes_split_on_large_layers(prec):
+    # N=32, 64 channels, 64x64, m=4: 256 tile-block pairs x 2 filter groups, two
+    # rounds of split items: AUTO runs the split path (same bits as asking for it)
+    flag, _, rnd = PRECS[prec]
+    N, C, H, W, K, pad, m = 32, 64, 64, 64, 128, 1, 4
+    st, algo, _ = B.wino_plan_r(N, C, H, W, K, pad, m, 3, flag)
+    assert st == B.WINO_OK and algo == B.WINO_ALGO_SPLIT
+    rng = np.random.default_rng(99)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    U16, _ = filter16(g, m, flag)
+    ya = conv16(x, U16, K, pad, m, flag)
+    assert np.array_equal(ya, conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_SPLIT))
+    # sampled: the first image's first 16 filters against the exact result
+    err = h.normwise_err(ya[:1, :16], direct.conv2d(x[:1], g[:16], pad))
+    print(f"16-bit split {prec}: normwise {err:.3e} on the sampled outputs", flush=True)
+    assert err <= STUDY[(prec, m)]
+
+
+@pytest.mark.parametrize("prec", list(PRECS))
+@pytest.mark.parametrize("m,shape", [(4, (33, 16, 64, 64, 64, 1)), (2, (15, 16, 48, 48, 64, 1))],
+                         ids=["m4", "m2"])
+def test_conv2d_16_split_tail_units(prec, m, shape):
+    # Just over a round of split items (m=4: 264 tile-block pairs x 1 filter
+    # group; m=2: 270): the last 8 / 14 items run as units of one tile block and
+    # one filter block, their channel parts summed through LDS.
+    flag, u, rnd = PRECS[prec]
+    N, C, H, W, K, pad = shape
+    print(f"conv2d split tail {prec} m={m} shape={shape}", flush=True)
+    rng = np.random.default_rng(5 + m)
+    x, g = wl.random_layer(rng, N, C, H, W, K)
+    U16, _ = filter16(g, m, flag)
+    y = conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_SPLIT)
+    y16, bound = reference_and_bound(x, g, pad, m, rnd)
+    assert np.all(np.isfinite(y))
+    tol = (2 * u + 4 * C * 2.0 ** -24 + 2.0 ** -20) * bound
+    assert np.all(np.abs(y - y16) <= tol + 1e-30)
+    ys = conv16(x, U16, K, pad, m, flag | B.WINO_ALGO_STAGED)
+    assert np.all(np.abs(y - ys) <= 16 * 2.0 ** -24 * bound + 1e-30)
