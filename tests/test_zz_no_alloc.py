@@ -19,14 +19,16 @@ TOL = {2: 1e-4, 4: 1e-3}
 
 # (N, C, H, W, K, pad, m, flags): split (31.5 MiB of scratch), split (18 MiB),
 # AUTO on two channel slices (3 MiB of partial outputs), staged (0.9 MiB),
-# staged with fp16 operands (1.4 MiB), and AUTO on a layer whose split
-# workspace (504 MiB) is past the scratch, so the fused kernel runs.
+# staged with fp16 operands (1.4 MiB), split with bf16 operands (3.5 MiB),
+# and AUTO on a layer whose split workspace (504 MiB) is past the scratch, so
+# the fused kernel runs.
 CASES = [
     (4, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_SPLIT),
     (8, 256, 28, 28, 256, 1, 4, B.WINO_ALGO_SPLIT),
     (1, 512, 28, 28, 512, 1, 4, B.WINO_ALGO_AUTO | B.WINO_FLAG_RELU),
     (1, 64, 20, 20, 64, 1, 2, B.WINO_ALGO_STAGED),
     (2, 64, 30, 30, 48, 1, 4, B.WINO_ALGO_STAGED | B.WINO_PREC_F16),
+    (4, 64, 56, 56, 64, 1, 4, B.WINO_ALGO_SPLIT | B.WINO_PREC_BF16 | B.WINO_FLAG_RELU),
 ]
 BIG_AUTO = (64, 256, 56, 56, 256, 1, 4, B.WINO_ALGO_AUTO)
 
@@ -68,6 +70,8 @@ def _check_oracle(case, x, g, y, sample):
         prec = "fp16" if flags & B.WINO_PREC_MASK == B.WINO_PREC_F16 else "bf16"
         _, u, rnd = PRECS[prec]
         ref, bound = reference_and_bound(xs, g, pad, m, rnd)
+        if flags & B.WINO_FLAG_RELU:           # 1-Lipschitz: the bound still holds
+            ref = np.maximum(ref, 0.0)
         assert np.all(np.abs(y[sample] - ref) <= (2 * u + 4 * C * 2.0 ** -24 + 2.0 ** -20) * bound + 1e-30)
         return
     ref = direct.conv2d(xs, g, pad)
