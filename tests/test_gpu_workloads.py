@@ -117,3 +117,53 @@ def test_vgg16_stack(name, sample):
     err = h.normwise_err(out, ref)
     print(f"  end-to-end normwise err {err:.2e}", flush=True)
     assert err <= E2E_TOL
+
+
+def test_large_batch_nhwc_split_sampled():
+    """The 256-channel 56x56 layer at N=64 in channel-last layout on the split
+    path (the launch the channel-last bench line times): sampled images against
+    the fp64 oracle, and the whole batch bit for bit against the NCHW split
+    path (the same V, GEMM and output transform; only x's and y's layout
+    differ)."""
+    from test_gpu_nhwc import conv_nhwc
+    w = wl.WORKLOADS["f4_n64_c256_k256_56x56"]
+    L = w.first
+    x, (g,) = wl.generate(w)
+    sample = [0, w.N // 2, w.N - 1]
+    print(f"{w.name} channel-last split, sample {sample}", flush=True)
+    U = h.filter_transform(g, L.m)
+    x_nhwc = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    y = h.host(conv_nhwc(x_nhwc, U, L.K, L.pad, L.m, B.WINO_ALGO_SPLIT))
+    del x_nhwc
+    err = h.normwise_err(y[sample].transpose(0, 3, 1, 2), direct.conv2d(x[sample], g, L.pad))
+    print(f"  normwise err {err:.2e}", flush=True)
+    assert err <= TOL[L.m]
+    y_nchw = h.host(h.conv2d(x, U, L.K, L.pad, L.m, B.WINO_ALGO_SPLIT))
+    assert np.array_equal(y.transpose(0, 3, 1, 2), y_nchw)
+
+
+@pytest.mark.parametrize("prec", ["fp16", "bf16"])
+def test_large_batch_16bit_split_sampled(prec):
+    """The same layer with 16-bit transform-domain operands on the split path
+    (AUTO's choice there, and the launch the 16-bit bench line times): sampled
+    images against the reduced-precision reference (U and V rounded once) within
+    the rounding bound of the fp32 transforms and accumulation, and against the
+    exact result within the error study's bound."""
+    from test_gpu_prec16 import PRECS, STUDY, conv16, filter16, reference_and_bound
+    flag, u, rnd = PRECS[prec]
+    w = wl.WORKLOADS["f4_n64_c256_k256_56x56"]
+    L = w.first
+    x, (g,) = wl.generate(w)
+    st, algo, _ = B.wino_plan_r(w.N, L.C, L.H, L.W, L.K, L.pad, L.m, 3, flag)
+    assert st == B.WINO_OK and algo == B.WINO_ALGO_SPLIT
+    sample = [0, w.N - 1]
+    print(f"{w.name} 16-bit split {prec}, sample {sample}", flush=True)
+    U16, _ = filter16(g, L.m, flag)
+    y = conv16(x, U16, L.K, L.pad, L.m, flag | B.WINO_ALGO_SPLIT)[sample]
+    assert np.all(np.isfinite(y))
+    y16, bound = reference_and_bound(x[sample], g, L.pad, L.m, rnd)
+    tol = (2 * u + 4 * L.C * 2.0 ** -24 + 2.0 ** -20) * bound
+    assert np.all(np.abs(y - y16) <= tol + 1e-30)
+    err = h.normwise_err(y, direct.conv2d(x[sample], g, L.pad))
+    print(f"  normwise err against the exact result {err:.2e}", flush=True)
+    assert err <= STUDY[(prec, L.m)]
