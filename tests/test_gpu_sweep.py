@@ -4,7 +4,8 @@ layout, with and without ReLU, against the fp64 direct oracle; and the 16-bit
 operand paths against the oracle's reduced-precision reference.  The shapes
 lean on the edges: images of one or two pixels, odd channel and filter counts,
 C <= 4 (the low-C kernel), padding up to 3, ragged tiles.  Layers with Ho or
-Wo below 1 must be refused as invalid arguments by every entry point."""
+Wo below 1 must be refused as invalid arguments by every entry point.  The
+same over F(2x2,5x5) layers and the 1-D layers of both axes."""
 import numpy as np
 import pytest
 import torch
@@ -127,3 +128,88 @@ def test_sweep_16bit(case, prec):
         y = conv16(x, U16, K, pad, m, flag | algo, relu=relu)
         assert np.all(np.isfinite(y)), algo
         assert np.all(np.abs(y - y16) <= tol), algo
+
+
+def _cases_rs(n, seed, rmin):
+    """(N, C, H, W, K, pad, relu) for layers of an r x r or 1 x r filter."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        N = int(rng.integers(1, 4))
+        C = int(rng.choice([1, 2, 3, 5]) if rng.random() < 0.25 else rng.integers(1, 73))
+        K = int(rng.integers(1, 73))
+        H = int(rng.integers(1, 41))
+        W = int(rng.integers(1, 41))
+        pad = int(rng.integers(0, rmin))
+        out.append((N, C, H, W, K, pad, bool(rng.random() < 0.5)))
+    return out
+
+
+CASES_R5 = _cases_rs(40, 2027, 4)
+
+
+@pytest.mark.parametrize("case", CASES_R5, ids=lambda c: "x".join(map(str, c[:6])) + ("r" if c[6] else ""))
+def test_sweep_5x5(case):
+    # F(2x2,5x5): every algorithm the library accepts for the layer (AUTO at least)
+    import test_gpu_r5 as r5
+    N, C, H, W, K, pad, relu = case
+    print(f"sweep 5x5 {case}", flush=True)
+    rng = np.random.default_rng(sum(case[:6]) * 13)
+    x, g = r5.random_layer(rng, N, C, H, W, K)
+    U = r5.filter_transform(g)
+    rf = B.WINO_FLAG_RELU if relu else 0
+    Ho, Wo = H + 2 * pad - 4, W + 2 * pad - 4
+    if Ho < 1 or Wo < 1:
+        assert B.wino_workspace_bytes_r(N, C, H, W, K, pad, 2, 5, rf) == BAD
+        return
+    ref = direct.conv2d(x, g, pad)
+    bound = tile_bound(direct.conv2d(x, g, pad, absval=True), 2)
+    if relu:
+        ref = np.maximum(ref, 0.0)
+    ran = []
+    for name, fl in ALGOS.items():
+        if B.wino_workspace_bytes_r(N, C, H, W, K, pad, 2, 5, fl | rf) == BAD:
+            continue
+        y = h.host(r5.conv(x, U, K, pad, fl | rf))
+        assert np.all(np.isfinite(y)), name
+        assert np.all(np.abs(y - ref) <= r5.ELEM * (bound + 1e-30)), name
+        ran.append(name)
+    print(f"  ran {ran}", flush=True)
+    assert "auto" in ran
+
+
+CASES_1D = [c + (v, ax) for c, v, ax in zip(_cases_rs(48, 2028, 4),
+                                          [(6, 3), (4, 5), (2, 7)] * 16, ["w", "h"] * 24)]
+
+
+@pytest.mark.parametrize("case", CASES_1D,
+                         ids=lambda c: "x".join(map(str, c[:6])) + ("r" if c[6] else "") + f"-F{c[7][0]}r{c[7][1]}{c[8]}")
+def test_sweep_1d(case):
+    # F(1xm,1xr,1x8) along W or H: every algorithm the library accepts (AUTO at least)
+    import test_gpu_1d as d1
+    N, C, H, W, K, pad, relu, (m, r), axis = case
+    print(f"sweep 1-D {case}", flush=True)
+    rng = np.random.default_rng(sum(case[:6]) * 17 + m)
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    g = (rng.standard_normal(d1.filt_shape(K, C, r, axis)) * np.sqrt(2.0 / (r * C))).astype(np.float32)
+    U = d1.filter_transform(g, m, r)
+    rf = B.WINO_FLAG_RELU if relu else 0
+    ax = d1.AXES[axis]
+    L = (W if axis == "w" else H) + 2 * pad - (r - 1)
+    if L < 1:
+        assert B.wino_workspace_bytes_1d(N, C, H, W, K, pad, m, r, ax, rf) == BAD
+        return
+    ref = d1.direct_1d(x, g, pad, axis)
+    bound = d1.tile_bound(d1.direct_1d(x, g, pad, axis, absval=True), m, axis)
+    if relu:
+        ref = np.maximum(ref, 0.0)
+    ran = []
+    for name, fl in ALGOS.items():
+        if B.wino_workspace_bytes_1d(N, C, H, W, K, pad, m, r, ax, fl | rf) == BAD:
+            continue
+        y = h.host(d1.conv(x, U, K, pad, m, r, axis, fl | rf))
+        assert np.all(np.isfinite(y)), name
+        assert np.all(np.abs(y - ref) <= d1.ELEM * (bound + 1e-30)), name
+        ran.append(name)
+    print(f"  ran {ran}", flush=True)
+    assert "auto" in ran
