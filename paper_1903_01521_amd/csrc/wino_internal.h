@@ -94,8 +94,9 @@ struct SplitTail {
 };
 SplitTail split_tail(const Geom& g);
 // The split path's input transform by whole tile rows: R rows of the batch
-// per workgroup (0: the 16-tile patch kernel instead), LDS row pitch in
-// floats, dynamic LDS bytes.
+// per workgroup (0: the 16-tile patch kernel instead, always for vec = 0,
+// i.e. a width that is not a multiple of 4 or an unaligned x), LDS row pitch
+// in floats, dynamic LDS bytes.
 constexpr size_t kVrowsLds = 64 << 10;
 struct VrowsPlan {
     int R, pitch;

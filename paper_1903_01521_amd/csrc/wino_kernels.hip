@@ -185,12 +185,12 @@ __device__ __forceinline__ void store_row(float* __restrict__ y, const Geom& g, 
             store_out<NT>(row, v[0], v[1]);
         }
     } else {
+        // Plain 4-byte stores, whatever NT says: they merge into whole lines
+        // in L2, where non-temporal ones went out as partial-line writes
+        // (25-30% of the split and fused calls on 26-30 pixel wide layers).
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-            if (oj0 + j < g.Wo) {
-                if constexpr (NT) __builtin_nontemporal_store(v[j], row + j);
-                else row[j] = v[j];
-            }
+            if (oj0 + j < g.Wo) row[j] = v[j];
     }
 }
 
@@ -1265,17 +1265,19 @@ __device__ __forceinline__ uint32_t to16(float v) {
 // tile), and stores each block's 9 (m = 4) or 4 (m = 2) groups as whole 1 KiB
 // runs.  The host picks R so that R*tw is a multiple of 16 where LDS allows:
 // every block is then written by one workgroup (a block the row range only
-// partly covers is completed by the neighbouring workgroup).  VEC: 16-byte
-// loads of column chunks starting xsh columns before the patch.
+// partly covers is completed by the neighbouring workgroup).  Loads are
+// 16-byte column chunks starting xsh columns before the patch (the host takes
+// this kernel only for widths that are a multiple of 4 and a 16-byte aligned
+// x, so every chunk lies wholly inside or outside a row).
 // LDS: [row r][channel][A rows][pitch] floats, shifted so that a tile's first
 // column sits at a multiple of 4.  OUT = 1 / 2: the 16-bit paths' VH (fp16 /
 // bf16, 16-channel groups, a lane's word holding four channels): the lane
 // stores its channel's 16 bits, and a wave's store covers its quad's 128
 // contiguous bytes of a group's position block; nq = 4 * C16.
-template <int MT, int VEC, int OUT = 0>
+template <int MT, int OUT = 0>
 __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, float* __restrict__ Vb, Geom g,
                                                int R, int pitch, int nq) {
-    constexpr int A = MT + 2, T = A * A, EW = VEC ? 4 : 1;
+    constexpr int A = MT + 2, T = A * A, EW = 4;
     extern __shared__ float4 xs4[];
     float* xs = (float*)xs4;
     const int nrows = g.N * g.th;                        // tile rows of the batch
@@ -1289,7 +1291,7 @@ __global__ __launch_bounds__(256) void k_vrows(const float* __restrict__ x, floa
     const size_t left = ((size_t)g.N - n0) * img * 4;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(x + (size_t)n0 * img), (short)0, (int)(left < kInvalid ? left : kInvalid), kRsrcWord3);
-    const int xsh = VEC ? (4 - g.pad % 4) % 4 : 0, xlo = (4 - xsh) % 4;
+    const int xsh = (4 - g.pad % 4) % 4, xlo = (4 - xsh) % 4;
     const int cs = -g.pad - xsh;                         // image column of a patch row's first unit
     const int ne = pitch / EW;                           // units per patch row
     const int units = R * 4 * A * ne;
@@ -2297,21 +2299,12 @@ hipError_t launch_staged16(const float* x, const void* UH, float* y, void* VH, f
         const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
         const dim3 gr((unsigned)(ngr * 4 * C16)), b256(256);
         float* vf = (float*)VH;
-#define WINO_VROWS16(MT, VEC, P) \
-    hipLaunchKernelGGL((k_vrows<MT, VEC, P>), gr, b256, vp.lds, s, x, vf, g, vp.R, vp.pitch, 4 * C16)
-        if (g.m == 2 && prec == 1) {
-            if (vec) WINO_VROWS16(2, 1, 1);
-            else WINO_VROWS16(2, 0, 1);
-        } else if (g.m == 2) {
-            if (vec) WINO_VROWS16(2, 1, 2);
-            else WINO_VROWS16(2, 0, 2);
-        } else if (prec == 1) {
-            if (vec) WINO_VROWS16(4, 1, 1);
-            else WINO_VROWS16(4, 0, 1);
-        } else {
-            if (vec) WINO_VROWS16(4, 1, 2);
-            else WINO_VROWS16(4, 0, 2);
-        }
+#define WINO_VROWS16(MT, P) \
+    hipLaunchKernelGGL((k_vrows<MT, P>), gr, b256, vp.lds, s, x, vf, g, vp.R, vp.pitch, 4 * C16)
+        if (g.m == 2 && prec == 1) WINO_VROWS16(2, 1);
+        else if (g.m == 2) WINO_VROWS16(2, 2);
+        else if (prec == 1) WINO_VROWS16(4, 1);
+        else WINO_VROWS16(4, 2);
 #undef WINO_VROWS16
     } else if (g.m == 2 && prec == 1) hipLaunchKernelGGL((k_input16<2, 1>), gi, block, 0, s, x, vh, g, C16, nwg);
     else if (g.m == 2) hipLaunchKernelGGL((k_input16<2, 2>), gi, block, 0, s, x, vh, g, C16, nwg);
@@ -2828,16 +2821,8 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
         if (vp.R > 0) {
             const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
             const dim3 gr((unsigned)(ngr * g.CQ)), b256(256);
-#define WINO_VROWS(MT, VEC) \
-    hipLaunchKernelGGL((k_vrows<MT, VEC>), gr, b256, vp.lds, s, x, V, g, vp.R, vp.pitch, g.CQ)
-            if (g.m == 2) {
-                if (vec) WINO_VROWS(2, 1);
-                else WINO_VROWS(2, 0);
-            } else {
-                if (vec) WINO_VROWS(4, 1);
-                else WINO_VROWS(4, 0);
-            }
-#undef WINO_VROWS
+            if (g.m == 2) hipLaunchKernelGGL((k_vrows<2>), gr, b256, vp.lds, s, x, V, g, vp.R, vp.pitch, g.CQ);
+            else hipLaunchKernelGGL((k_vrows<4>), gr, b256, vp.lds, s, x, V, g, vp.R, vp.pitch, g.CQ);
             return hipGetLastError();
         }
     }
@@ -3044,7 +3029,12 @@ size_t vblk_elems(const Geom& g) { return (size_t)split_blocks(g) * ((g.CQ + 3) 
 // range spans do not fit the 32-bit load offsets.
 VrowsPlan vrows_plan(const Geom& g, int vec) {
     VrowsPlan p{0, 0, 0};
-    const int xsh = vec ? (4 - g.pad % 4) % 4 : 0;
+    // Rows whose width is not a multiple of 4 floats (or an unaligned x) would
+    // come in by 4-byte DMA, one float per lane: the per-block and per-region
+    // kernels are faster there (VGG-16's 14x14 layers at N = 32: 20 -> 14 us;
+    // 26-57 pixel wide layers: 7-12% of the split call, 4-13% of the staged one).
+    if (!vec) return p;
+    const int xsh = (4 - g.pad % 4) % 4;
     p.pitch = (xsh + g.tw * g.m + 2 + 3) / 4 * 4;
     const size_t row_b = (size_t)4 * g.A * p.pitch * sizeof(float);    // one tile row, 4 channels
     int gcd = 16, t = g.tw;
@@ -3094,8 +3084,7 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
         if (vp.R > 0) {
             const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
             const dim3 grid((unsigned)(ngr * ncq4 * 4)), block(256);
-            if (vec) hipLaunchKernelGGL((k_vrows<MT, 1>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, 4 * ncq4);
-            else hipLaunchKernelGGL((k_vrows<MT, 0>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, 4 * ncq4);
+            hipLaunchKernelGGL((k_vrows<MT>), grid, block, vp.lds, s, x, Vb, g, vp.R, vp.pitch, 4 * ncq4);
         } else {
             const dim3 grid((unsigned)((long)ntb * ncq4)), block(256);
             if (vec) hipLaunchKernelGGL((k_vblk<MT, BW, 1>), grid, block, 0, s, x, Vb, g, ft.nbh, ft.nbw, ncq4);
@@ -3138,10 +3127,7 @@ static hipError_t split16_instance(const float* x, const void* UH, float* y, voi
     if (vp.R > 0) {
         const long ngr = ((long)g.N * g.th + vp.R - 1) / vp.R;
         const dim3 gr((unsigned)(ngr * 4 * c16p)), b256(256);
-        if (vec) hipLaunchKernelGGL((k_vrows<MT, 1, PREC>), gr, b256, vp.lds, s, x, (float*)VH, g, vp.R, vp.pitch,
-                                    4 * c16p);
-        else hipLaunchKernelGGL((k_vrows<MT, 0, PREC>), gr, b256, vp.lds, s, x, (float*)VH, g, vp.R, vp.pitch,
-                                4 * c16p);
+        hipLaunchKernelGGL((k_vrows<MT, PREC>), gr, b256, vp.lds, s, x, (float*)VH, g, vp.R, vp.pitch, 4 * c16p);
     } else {
         const long waves = (long)g.PB * c16p, nwg = (waves + 3) / 4;
         if ((nwg + 7) / 8 * 8 > 0x7fffffffL) return hipErrorInvalidConfiguration;
