@@ -1686,8 +1686,8 @@ __device__ __forceinline__ void unit_steps16(const __amdgpu_buffer_rsrc_t vr, co
 template <int MT, int PREC = 0>
 __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, const float* __restrict__ U,
                                               float* __restrict__ y, const Geom& g, int tb, int kb, int ncq4,
-                                              bool relu, bool vec_ok, float4* vs0, float4* vs1, int wave,
-                                              int lane) {
+                                              bool relu, bool vec_ok, bool nts, float4* vs0, float4* vs1,
+                                              int wave, int lane) {
     using S = GoShape<MT>;
     constexpr int TS = S::TS, TH = S::TH, T = S::T, CP = 8 / TS, NV = S::NV, VPW = NV / 8;
     static_assert(4 * NV * 64 <= S::VST, "four partial-output slots per LDS stage");
@@ -1770,7 +1770,8 @@ __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, cons
                         y[(((size_t)tc.n * g.Ho + oi) * g.Wo + oj) * g.K + k] = relu ? fmaxf(row[j], 0.0f) : row[j];
                 }
         } else {
-            store_row<MT>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
+            if (nts) store_row<MT, true>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
+            else store_row<MT, false>(y, g, tc, k, i0 + ii, row, relu, vec_ok);
         }
     }
 }
@@ -1780,7 +1781,7 @@ __device__ __forceinline__ void gemm_out_unit(const float* __restrict__ Vb, cons
 template <int MT, int PREC = 0>
 __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, const float* __restrict__ U,
                                                   float* __restrict__ y, Geom g, FusedTiling ft, int nb,
-                                                  int relu, int vec_ok, int ntail) {
+                                                  int relu, int vec_ok, int nts, int ntail) {
     using S = GoShape<MT>;
     constexpr int TS = S::TS, KGW = S::KGW, TH = S::TH, NV = S::NV;
     __shared__ float4 vs0[S::VST / 4], vs1[S::VST / 4];
@@ -1803,7 +1804,7 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
         const int tb = 2 * tp + sub / KGW, kb = kgi * KGW + sub % KGW;
         if (tb >= nb || kb >= g.KB) return;
         gemm_out_unit<MT, PREC>(Vb, U, y, g, tb, kb, PREC ? (g.C + 31) / 32 : (g.CQ + 3) / 4, relu != 0,
-                                vec_ok != 0, vs0, vs1, wave, lane);
+                                vec_ok != 0, nts != 0, vs0, vs1, wave, lane);
         return;
     }
     const int item = (b & 7) * ft.per + (b >> 3);
@@ -1875,7 +1876,10 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
                 store_tile_nhwc<MT>(y, g, tc, kbase, o[bb], rl, vo);
             } else {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+                for (int r = 0; r < 4; ++r) {
+                    if (nts) store_block<MT, true>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+                    else store_block<MT, false>(y, g, tc, kbase + r, o[bb][r], rl, vo);
+                }
             }
         }
     } else {
@@ -1927,7 +1931,10 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
                 store_tile_nhwc<MT>(y, g, tc, kbase, ob, rl, vo);
             } else {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) store_block<MT>(y, g, tc, kbase + r, ob[r], rl, vo);
+                for (int r = 0; r < 4; ++r) {
+                    if (nts) store_block<MT, true>(y, g, tc, kbase + r, ob[r], rl, vo);
+                    else store_block<MT, false>(y, g, tc, kbase + r, ob[r], rl, vo);
+                }
             }
         }
     }
@@ -2700,6 +2707,15 @@ constexpr size_t kStreamStoreBytes = 4u << 20;
 static inline int stream_stores(const Geom& g) {
     return (size_t)g.N * g.K * g.Ho * g.Wo * sizeof(float) > kStreamStoreBytes ? 1 : 0;
 }
+// The split path's GEMM kernel streams y only past half of the 256 MB
+// last-level cache: below that, plain stores leave y there for the next
+// layer and also finish sooner themselves (VGG-16 at N = 32: layers with
+// 51-103 MB of output 2-9% faster per call, the stack 3%); at 205 MB streaming
+// stays ahead (the 112x112 layers 3-6%).
+constexpr size_t kSplitStreamBytes = 128u << 20;
+static inline int split_stream_stores(const Geom& g) {
+    return (size_t)g.N * g.K * g.Ho * g.Wo * sizeof(float) > kSplitStreamBytes ? 1 : 0;
+}
 
 hipError_t launch_filter_transform(const float* gw, float* U, int C, int K, int m, int r, hipStream_t s) {
     const int CQ = (C + 3) / 4, KB = (K + 15) / 16, TG = (m + r - 1) * (m + r - 1) / 4;
@@ -3109,7 +3125,7 @@ static hipError_t split_instance(const float* x, const float* U, float* y, float
     // 16-byte output stores: whole m-wide rows (NCHW) or four channels of a pixel (NHWC)
     const int vec_ok = g.nhwc ? (g.K % 4 == 0 && aligned(y, 16)) : ((g.Wo % MT == 0) && aligned(y, 4 * MT));
     hipLaunchKernelGGL((k_gemm_out<MT>), grid, block, 0, s, Vb, U, y, g, ft, nb, (int)relu, vec_ok,
-                       (int)st.tail);
+                       split_stream_stores(g), (int)st.tail);
     return hipGetLastError();
 }
 
@@ -3153,7 +3169,7 @@ static hipError_t split16_instance(const float* x, const void* UH, float* y, voi
     const dim3 grid((unsigned)(8 * ft.per + st.tail * st.units)), block(512);
     const int vec_ok = (g.Wo % MT == 0) && aligned(y, 4 * MT);
     hipLaunchKernelGGL((k_gemm_out<MT, PREC>), grid, block, 0, s, (const float*)VH, (const float*)UH, y, g, ft, nb,
-                       (int)relu, vec_ok, (int)st.tail);
+                       (int)relu, vec_ok, split_stream_stores(g), (int)st.tail);
     return hipGetLastError();
 }
 
