@@ -205,8 +205,8 @@ __device__ __forceinline__ void store_block(float* __restrict__ y, const Geom& g
 
 // Channel-last y [N][Ho][Wo][K]: the m x m outputs of (tile tc, output channels
 // k0 .. k0+3), cropped to Ho x Wo and K; one 16-byte store per pixel when vec
-// (K % 4 == 0 and y 16-byte aligned).
-template <int MT>
+// (K % 4 == 0 and y 16-byte aligned), streaming when NT.
+template <int MT, bool NT = false>
 __device__ __forceinline__ void store_tile_nhwc(float* __restrict__ y, const Geom& g, const TileCoord& tc, int k0,
                                                 const float (&o)[4][MT][MT], bool relu, bool vec) {
     if (!tc.valid || k0 >= g.K) return;
@@ -221,7 +221,7 @@ __device__ __forceinline__ void store_tile_nhwc(float* __restrict__ y, const Geo
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = relu ? fmaxf(o[r][i][j], 0.0f) : o[r][i][j];
             if (vec && k0 + 4 <= g.K) {
-                *(float4*)py = make_float4(v[0], v[1], v[2], v[3]);
+                store_out<NT>(py, v[0], v[1], v[2], v[3]);
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
@@ -1873,7 +1873,8 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
         for (int bb = 0; bb < 2; ++bb) {
             const TileCoord tc = tile_of(bb);
             if (g.nhwc) {
-                store_tile_nhwc<MT>(y, g, tc, kbase, o[bb], rl, vo);
+                if (nts) store_tile_nhwc<MT, true>(y, g, tc, kbase, o[bb], rl, vo);
+                else store_tile_nhwc<MT, false>(y, g, tc, kbase, o[bb], rl, vo);
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -1928,7 +1929,8 @@ __global__ __launch_bounds__(512) void k_gemm_out(const float* __restrict__ Vb, 
 #pragma unroll
                     for (int j = 0; j < MT; ++j) ob[r][i][j] = o[bb][r][i][j] + sl[r][i][j];
             if (g.nhwc) {
-                store_tile_nhwc<MT>(y, g, tc, kbase, ob, rl, vo);
+                if (nts) store_tile_nhwc<MT, true>(y, g, tc, kbase, ob, rl, vo);
+                else store_tile_nhwc<MT, false>(y, g, tc, kbase, ob, rl, vo);
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -2711,7 +2713,8 @@ static inline int stream_stores(const Geom& g) {
 // last-level cache: below that, plain stores leave y there for the next
 // layer and also finish sooner themselves (VGG-16 at N = 32: layers with
 // 51-103 MB of output 2-9% faster per call, the stack 3%); at 205 MB streaming
-// stays ahead (the 112x112 layers 3-6%).
+// stays ahead (the 112x112 layers 3-6%, the channel-last N = 64 256-channel
+// layer 2%).
 constexpr size_t kSplitStreamBytes = 128u << 20;
 static inline int split_stream_stores(const Geom& g) {
     return (size_t)g.N * g.K * g.Ho * g.Wo * sizeof(float) > kSplitStreamBytes ? 1 : 0;
