@@ -341,108 +341,6 @@ __global__ __launch_bounds__(256) void k_input(const float* __restrict__ x, floa
     store_t4<T, true>(V + ((size_t)pb * g.CQ + cq) * T * 64, lane, v);
 }
 
-// ------------------------------------------------------------------ GEMM
-// M_t[k][p] = sum_c U_t[c][k] V_t[c][p] for each transform position t.
-// Workgroup: 4 positions (one t/4 group) x 4 k-blocks x 4 p-blocks (64 x 64),
-// four waves, each 2 x 2 blocks of 16 x 16 for all 4 positions (16
-// accumulator tiles).  Channels advance 16 at a time (4 quads) through a double
-// buffer in LDS; the next chunk is fetched into registers while the current one
-// feeds the MFMAs.  In LDS a lane's 4 positions are one 16-byte word, so each
-// MFMA operand quadruple is one ds_read_b128.
-__global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
-                                              float* __restrict__ M, Geom g) {
-    // One LDS buffer (32 KB, so that five workgroups fit a CU): measured faster
-    // than a double buffer of 64 KB at every staged shape (N=64 256-channel
-    // layer 595 -> 558 us), the extra occupancy hiding more latency than the
-    // second barrier per chunk costs.
-    __shared__ float4 As[4][4][64];      // [quad][k-block][lane] -> 4 positions
-    __shared__ float4 Bs[4][4][64];      // [quad][p-block][lane]
-    const int T = g.T, TG = g.T / 4;
-    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
-    // Items (position group, p-tile, k-tile), k-tile fastest; each XCD runs one
-    // contiguous range of items (workgroup b takes item (b % 8) * per + b / 8),
-    // so the k-tiles that share a p-tile's V run together and V comes from HBM
-    // into that XCD's L2 once.
-    const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
-    const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
-    if (item >= nitems) return;
-    const int kb0 = (int)(item % KB4) * 4;
-    const long rest = item / KB4;
-    const int pb0 = (int)(rest % PB4) * 4;
-    const int tg = (int)(rest / PB4);     // positions 4*tg .. 4*tg+3
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wk = wave >> 1, wp = wave & 1;
-    const int nchunks = (g.CQ + 3) >> 2;
-
-    // Loader: each chunk is 16 A blocks + 16 B blocks of 64 float4; thread tid
-    // moves float4 number (tid & 63) of blocks (tid >> 6) + 4*i, i < 4.
-    float4 ra[4], rb[4];
-    auto fetch = [&](int chunk) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int blk = (tid >> 6) + 4 * i;          // = quad * 4 + block
-            const int cq = chunk * 4 + (blk >> 2), bi = blk & 3;
-            const int kb = kb0 + bi, pb = pb0 + bi;
-            ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            rb[i] = ra[i];
-            if (cq < g.CQ && kb < g.KB)
-                ra[i] = *(const float4*)(U + ((((size_t)kb * g.CQ + cq) * TG + tg) * 64 + lane) * 4);
-            if (cq < g.CQ && pb < g.PB)
-                rb[i] = *(const float4*)(V + ((((size_t)pb * g.CQ + cq) * TG + tg) * 64 + lane) * 4);
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int blk = (tid >> 6) + 4 * i;
-            As[blk >> 2][blk & 3][lane] = ra[i];
-            Bs[blk >> 2][blk & 3][lane] = rb[i];
-        }
-    };
-
-    f32x4 acc[4][2][2];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    fetch(0);
-    stage();
-    for (int ch = 0; ch < nchunks; ++ch) {
-        __syncthreads();                 // chunk ch is in LDS
-        if (ch + 1 < nchunks) fetch(ch + 1);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float4 a0 = As[q][wk * 2 + 0][lane];
-            const float4 a1 = As[q][wk * 2 + 1][lane];
-            const float4 b0 = Bs[q][wp * 2 + 0][lane];
-            const float4 b1 = Bs[q][wp * 2 + 1][lane];
-            const float av[2][4] = {{a0.x, a0.y, a0.z, a0.w}, {a1.x, a1.y, a1.z, a1.w}};
-            const float bv[2][4] = {{b0.x, b0.y, b0.z, b0.w}, {b1.x, b1.y, b1.z, b1.w}};
-#pragma unroll
-            for (int t4 = 0; t4 < 4; ++t4)
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-#pragma unroll
-                    for (int j = 0; j < 2; ++j) acc[t4][i][j] = mfma16x16x4(av[i][t4], bv[j][t4], acc[t4][i][j]);
-        }
-        __syncthreads();                 // every wave is done with chunk ch
-        if (ch + 1 < nchunks) stage();
-    }
-#pragma unroll
-    for (int t4 = 0; t4 < 4; ++t4)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
-                if (kb < g.KB && pb < g.PB)
-                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
-            }
-}
-
 // ------------------------------------------------------------------ output
 // A workgroup owns whole rows of tiles of one image (R rows of tw <= 64 tiles,
 // or a 64-tile piece of one row) for one 16-filter block: wave = filter quad,
@@ -1161,6 +1059,128 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, ui
     static_assert(BYTES == 4 || BYTES == 16, "dword or 16-byte loads");
     if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, soff, 0, 0);
     else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 4, off, soff, 0, 0);
+}
+
+// ------------------------------------------------------------------ GEMM
+// M_t[k][p] = sum_c U_t[c][k] V_t[c][p] for each transform position t.
+// Workgroup: 4 positions (one t/4 group) x 4 k-blocks x 4 p-blocks (64 x 64),
+// four waves, each 2 x 2 blocks of 16 x 16 for all 4 positions (16
+// accumulator tiles).  Channels advance 8 at a time (2 quads): a chunk is 8
+// U blocks and 8 V blocks of 1 KB (64 lanes x one 16-byte word of 4
+// positions), copied straight into LDS by DMA into a ring of three stages,
+// two chunks ahead of the products, so a chunk's load latency is hidden even
+// when only one or two workgroups share a CU (the 1-D layers' T = 8 GEMMs).
+// Each MFMA operand quadruple is then one ds_read_b128.  Blocks past K or P
+// lie past the item's buffer ranges and quads past C get an out-of-range
+// offset: both read as zero.
+__global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
+                                              float* __restrict__ M, Geom g) {
+    // 16 KB a stage, 48 KB in all: three workgroups share a CU, as their
+    // registers allow.
+    __shared__ float4 st0[16 * 64], st1[16 * 64], st2[16 * 64];   // [A: quad, k-block | B: quad, p-block][lane]
+    const int T = g.T, TG = g.T / 4;
+    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
+    // Items (position group, p-tile, k-tile), k-tile fastest; each XCD runs one
+    // contiguous range of items (workgroup b takes item (b % 8) * per + b / 8),
+    // so the k-tiles that share a p-tile's V run together and V comes from HBM
+    // into that XCD's L2 once.
+    const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
+    const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= nitems) return;
+    const int kb0 = (int)(item % KB4) * 4;
+    const long rest = item / KB4;
+    const int pb0 = (int)(rest % PB4) * 4;
+    const int tg = (int)(rest / PB4);     // positions 4*tg .. 4*tg+3
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wk = wave >> 1, wp = wave & 1;
+    const int NC = (g.CQ + 1) >> 1;      // chunks of two quads
+
+    // This item's U and V blocks as buffers: block j of the tile at
+    // j * CQ * TG KB; a block past K or P lies past the range.
+    const uint32_t bstride = (uint32_t)g.CQ * (uint32_t)TG * 1024u;
+    const size_t ub = (size_t)min(g.KB - kb0, 4) * bstride, vb = (size_t)min(g.PB - pb0, 4) * bstride;
+    const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(U + (size_t)kb0 * g.CQ * TG * 256), (short)0, (int)ub, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(V + (size_t)pb0 * g.CQ * TG * 256), (short)0, (int)vb, kRsrcWord3);
+    auto stage = [&](auto sc) -> float4* {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S == 0) return st0;
+        else if constexpr (S == 1) return st1;
+        else return st2;
+    };
+    // DMA of chunk c into stage sc: wave w moves slots 4w .. 4w+3 of the 16
+    // (slot q < 8: U block q % 4 of quad q / 4; q >= 8: V block (q-8) % 4 of
+    // quad (q-8) / 4), four loads per wave per chunk.
+    const uint32_t l16 = (uint32_t)lane * 16u;
+    auto issue = [&](auto sc, int c) {
+        float4* s = stage(sc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = wave * 4 + i, qq = q & 7, blk = qq & 3;
+            const int cq = 2 * c + (qq >> 2);
+            const uint32_t soff = cq < g.CQ ? (uint32_t)blk * bstride + ((uint32_t)cq * TG + tg) * 1024u
+                                            : (q < 8 ? (uint32_t)ub : (uint32_t)vb);
+            lds_dma<16>(q < 8 ? ur : vr, (float*)(s + q * 64), l16, __builtin_amdgcn_readfirstlane(soff));
+        }
+    };
+
+    f32x4 acc[4][2][2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    issue(IC<0>{}, 0);
+    if (NC > 1) issue(IC<1>{}, 1);
+    // Chunk ch (stage ch % 3): at its start the four DMA loads of chunk ch+1
+    // may still be in flight, not those of chunk ch; the barrier then tells
+    // every wave that chunk ch is in LDS and chunk ch-1's stage is free for
+    // chunk ch+2.
+    auto chunk = [&](auto sc, int ch) {
+        constexpr int S = decltype(sc)::value;
+        if (ch + 1 < NC) wait_vm_lds<4>();
+        else wait_vm_lds<0>();
+        wg_barrier();
+        if (ch + 2 < NC) issue(IC<(S + 2) % 3>{}, ch + 2);
+        const float4* s = stage(sc);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const float4 a0 = s[(q * 4 + wk * 2 + 0) * 64 + lane];
+            const float4 a1 = s[(q * 4 + wk * 2 + 1) * 64 + lane];
+            const float4 b0 = s[(8 + q * 4 + wp * 2 + 0) * 64 + lane];
+            const float4 b1 = s[(8 + q * 4 + wp * 2 + 1) * 64 + lane];
+            const float av[2][4] = {{a0.x, a0.y, a0.z, a0.w}, {a1.x, a1.y, a1.z, a1.w}};
+            const float bv[2][4] = {{b0.x, b0.y, b0.z, b0.w}, {b1.x, b1.y, b1.z, b1.w}};
+#pragma unroll
+            for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) acc[t4][i][j] = mfma16x16x4(av[i][t4], bv[j][t4], acc[t4][i][j]);
+        }
+    };
+    int ch = 0;
+    for (; ch + 3 <= NC; ch += 3) {
+        chunk(IC<0>{}, ch);
+        chunk(IC<1>{}, ch + 1);
+        chunk(IC<2>{}, ch + 2);
+    }
+    if (ch < NC) chunk(IC<0>{}, ch);
+    if (ch + 1 < NC) chunk(IC<1>{}, ch + 1);
+#pragma unroll
+    for (int t4 = 0; t4 < 4; ++t4)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
+                if (kb < g.KB && pb < g.PB)
+                    *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
+            }
 }
 
 template <int MT, int BW, int VEC>
@@ -2855,6 +2875,7 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
 }
 
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s) {
+    if ((size_t)4 * g.CQ * (g.T / 4) * 1024 >= (size_t)kInvalid) return hipErrorInvalidConfiguration;   // 32-bit offsets
     const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
     const long wgs = (nitems + 7) / 8 * 8;
     if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
