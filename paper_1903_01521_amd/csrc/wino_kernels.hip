@@ -1075,8 +1075,7 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, ui
 // offset: both read as zero.
 __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
                                               float* __restrict__ M, Geom g) {
-    // 16 KB a stage, 48 KB in all: three workgroups share a CU, as their
-    // registers allow.
+    // 16 KB a stage, 48 KB in all: three workgroups share a CU's 160 KB.
     __shared__ float4 st0[16 * 64], st1[16 * 64], st2[16 * 64];   // [A: quad, k-block | B: quad, p-block][lane]
     const int T = g.T, TG = g.T / 4;
     const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
