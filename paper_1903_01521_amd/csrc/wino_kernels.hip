@@ -1063,22 +1063,26 @@ __device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float* lds, ui
 
 // ------------------------------------------------------------------ GEMM
 // M_t[k][p] = sum_c U_t[c][k] V_t[c][p] for each transform position t.
-// Workgroup: 4 positions (one t/4 group) x 4 k-blocks x 4 p-blocks (64 x 64),
-// four waves, each 2 x 2 blocks of 16 x 16 for all 4 positions (16
-// accumulator tiles).  Channels advance 8 at a time (2 quads): a chunk is 8
-// U blocks and 8 V blocks of 1 KB (64 lanes x one 16-byte word of 4
+// Workgroup: 4 positions (one t/4 group) x KT k-blocks x 4 p-blocks (64 x 64
+// for KT = 4, 32 x 64 for KT = 2), four waves, each KT/2 x 2 blocks of 16 x 16
+// for all 4 positions.  Channels advance 8 at a time (2 quads): a chunk is
+// 2*KT U blocks and 8 V blocks of 1 KB (64 lanes x one 16-byte word of 4
 // positions), copied straight into LDS by DMA into a ring of three stages,
 // two chunks ahead of the products, so a chunk's load latency is hidden even
 // when only one or two workgroups share a CU (the 1-D layers' T = 8 GEMMs).
 // Each MFMA operand quadruple is then one ds_read_b128.  Blocks past K or P
 // lie past the item's buffer ranges and quads past C get an out-of-range
-// offset: both read as zero.
+// offset: both read as zero.  KT = 2 spreads layers that would give the CUs
+// fewer than four 64 x 64 items each over more workgroups and pads K to 32.
+template <int KT>
 __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const float* __restrict__ V,
                                               float* __restrict__ M, Geom g) {
-    // 16 KB a stage, 48 KB in all: three workgroups share a CU's 160 KB.
-    __shared__ float4 st0[16 * 64], st1[16 * 64], st2[16 * 64];   // [A: quad, k-block | B: quad, p-block][lane]
+    static_assert(KT == 2 || KT == 4, "k-blocks per tile");
+    constexpr int KW = KT / 2, NS = 2 * KT + 8, NPW = NS / 4;   // k-blocks per wave, slots, DMA loads per wave
+    // 12 or 16 KB a stage, at most 48 KB in all: three workgroups share a CU's 160 KB.
+    __shared__ float4 st0[NS * 64], st1[NS * 64], st2[NS * 64];   // [A: quad, k-block | B: quad, p-block][lane]
     const int T = g.T, TG = g.T / 4;
-    const int KB4 = (g.KB + 3) >> 2, PB4 = (g.PB + 3) >> 2;
+    const int KB4 = (g.KB + KT - 1) / KT, PB4 = (g.PB + 3) >> 2;
     // Items (position group, p-tile, k-tile), k-tile fastest; each XCD runs one
     // contiguous range of items (workgroup b takes item (b % 8) * per + b / 8),
     // so the k-tiles that share a p-tile's V run together and V comes from HBM
@@ -1086,7 +1090,7 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
     const long nitems = (long)TG * PB4 * KB4, per = (nitems + 7) / 8;
     const long item = (long)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (item >= nitems) return;
-    const int kb0 = (int)(item % KB4) * 4;
+    const int kb0 = (int)(item % KB4) * KT;
     const long rest = item / KB4;
     const int pb0 = (int)(rest % PB4) * 4;
     const int tg = (int)(rest / PB4);     // positions 4*tg .. 4*tg+3
@@ -1098,7 +1102,7 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
     // This item's U and V blocks as buffers: block j of the tile at
     // j * CQ * TG KB; a block past K or P lies past the range.
     const uint32_t bstride = (uint32_t)g.CQ * (uint32_t)TG * 1024u;
-    const size_t ub = (size_t)min(g.KB - kb0, 4) * bstride, vb = (size_t)min(g.PB - pb0, 4) * bstride;
+    const size_t ub = (size_t)min(g.KB - kb0, KT) * bstride, vb = (size_t)min(g.PB - pb0, 4) * bstride;
     const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(U + (size_t)kb0 * g.CQ * TG * 256), (short)0, (int)ub, kRsrcWord3);
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
@@ -1109,55 +1113,62 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
         else if constexpr (S == 1) return st1;
         else return st2;
     };
-    // DMA of chunk c into stage sc: wave w moves slots 4w .. 4w+3 of the 16
-    // (slot q < 8: U block q % 4 of quad q / 4; q >= 8: V block (q-8) % 4 of
-    // quad (q-8) / 4), four loads per wave per chunk.
+    // DMA of chunk c into stage sc: wave w moves slots NPW*w .. NPW*w+NPW-1
+    // of the NS (slot q < 2*KT: U block q % KT of quad q / KT; q >= 2*KT: V
+    // block (q-2*KT) % 4 of quad (q-2*KT) / 4), NPW loads per wave per chunk.
     const uint32_t l16 = (uint32_t)lane * 16u;
     auto issue = [&](auto sc, int c) {
         float4* s = stage(sc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int q = wave * 4 + i, qq = q & 7, blk = qq & 3;
-            const int cq = 2 * c + (qq >> 2);
+        for (int i = 0; i < NPW; ++i) {
+            const int q = wave * NPW + i;
+            const bool a = q < 2 * KT;
+            const int qq = a ? q : q - 2 * KT, w = a ? KT : 4, blk = qq % w;
+            const int cq = 2 * c + qq / w;
             const uint32_t soff = cq < g.CQ ? (uint32_t)blk * bstride + ((uint32_t)cq * TG + tg) * 1024u
-                                            : (q < 8 ? (uint32_t)ub : (uint32_t)vb);
-            lds_dma<16>(q < 8 ? ur : vr, (float*)(s + q * 64), l16, __builtin_amdgcn_readfirstlane(soff));
+                                            : (a ? (uint32_t)ub : (uint32_t)vb);
+            lds_dma<16>(a ? ur : vr, (float*)(s + q * 64), l16, __builtin_amdgcn_readfirstlane(soff));
         }
     };
 
-    f32x4 acc[4][2][2];
+    f32x4 acc[4][KW][2];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < KW; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) acc[q][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     issue(IC<0>{}, 0);
     if (NC > 1) issue(IC<1>{}, 1);
-    // Chunk ch (stage ch % 3): at its start the four DMA loads of chunk ch+1
+    // Chunk ch (stage ch % 3): at its start the NPW DMA loads of chunk ch+1
     // may still be in flight, not those of chunk ch; the barrier then tells
     // every wave that chunk ch is in LDS and chunk ch-1's stage is free for
     // chunk ch+2.
     auto chunk = [&](auto sc, int ch) {
         constexpr int S = decltype(sc)::value;
-        if (ch + 1 < NC) wait_vm_lds<4>();
+        if (ch + 1 < NC) wait_vm_lds<NPW>();
         else wait_vm_lds<0>();
         wg_barrier();
         if (ch + 2 < NC) issue(IC<(S + 2) % 3>{}, ch + 2);
         const float4* s = stage(sc);
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-            const float4 a0 = s[(q * 4 + wk * 2 + 0) * 64 + lane];
-            const float4 a1 = s[(q * 4 + wk * 2 + 1) * 64 + lane];
-            const float4 b0 = s[(8 + q * 4 + wp * 2 + 0) * 64 + lane];
-            const float4 b1 = s[(8 + q * 4 + wp * 2 + 1) * 64 + lane];
-            const float av[2][4] = {{a0.x, a0.y, a0.z, a0.w}, {a1.x, a1.y, a1.z, a1.w}};
-            const float bv[2][4] = {{b0.x, b0.y, b0.z, b0.w}, {b1.x, b1.y, b1.z, b1.w}};
+            float av[KW][4], bv[2][4];
+#pragma unroll
+            for (int i = 0; i < KW; ++i) {
+                const float4 a = s[(q * KT + wk * KW + i) * 64 + lane];
+                av[i][0] = a.x; av[i][1] = a.y; av[i][2] = a.z; av[i][3] = a.w;
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const float4 b = s[(2 * KT + q * 4 + wp * 2 + j) * 64 + lane];
+                bv[j][0] = b.x; bv[j][1] = b.y; bv[j][2] = b.z; bv[j][3] = b.w;
+            }
 #pragma unroll
             for (int t4 = 0; t4 < 4; ++t4)
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < KW; ++i)
 #pragma unroll
                     for (int j = 0; j < 2; ++j) acc[t4][i][j] = mfma16x16x4(av[i][t4], bv[j][t4], acc[t4][i][j]);
         }
@@ -1173,10 +1184,10 @@ __global__ __launch_bounds__(256) void k_gemm(const float* __restrict__ U, const
 #pragma unroll
     for (int t4 = 0; t4 < 4; ++t4)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < KW; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int kb = kb0 + wk * 2 + i, pb = pb0 + wp * 2 + j;
+                const int kb = kb0 + wk * KW + i, pb = pb0 + wp * 2 + j;
                 if (kb < g.KB && pb < g.PB)
                     *(f32x4*)(M + (((size_t)pb * g.KB + kb) * T + 4 * tg + t4) * 256 + lane * 4) = acc[t4][i][j];
             }
@@ -2875,11 +2886,15 @@ hipError_t launch_input_transform(const float* x, float* V, const Geom& g, hipSt
 
 hipError_t launch_batched_gemm(const float* U, const float* V, float* M, const Geom& g, hipStream_t s) {
     if ((size_t)4 * g.CQ * (g.T / 4) * 1024 >= (size_t)kInvalid) return hipErrorInvalidConfiguration;   // 32-bit offsets
-    const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
+    // 32 x 64 tiles when 64 x 64 ones would give the CUs fewer than four workgroups each
+    const long items4 = (long)((g.PB + 3) / 4) * ((g.KB + 3) / 4) * (g.T / 4);
+    const int kt = items4 < 4 * 256 ? 2 : 4;
+    const long nitems = (long)((g.PB + 3) / 4) * ((g.KB + kt - 1) / kt) * (g.T / 4);
     const long wgs = (nitems + 7) / 8 * 8;
     if (wgs > 0x7fffffffL) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)wgs), block(256);
-    hipLaunchKernelGGL(k_gemm, grid, block, 0, s, U, V, M, g);
+    if (kt == 2) hipLaunchKernelGGL(k_gemm<2>, grid, block, 0, s, U, V, M, g);
+    else hipLaunchKernelGGL(k_gemm<4>, grid, block, 0, s, U, V, M, g);
     return hipGetLastError();
 }
 
